@@ -1,0 +1,190 @@
+#!/usr/bin/env python3
+"""Benchmark of the ResiSpec verification step on one MI355X.
+
+One step = one full verification of a batch of draft trees: every node's outcome
+(row kernel) followed by the walk from each root (walk kernel), on inputs already
+resident in HBM.  Prints one JSON line.
+
+  python bench.py [--gpus 1] [--steps 20] [--warmup 5] [--config 2] [--mode resispec]
+
+The metric is verified tree-node rows per second (B * N / step time) at V = 128,256;
+`roofline.achieved` is the row kernel's algorithmic bytes (every target row once, the
+draft row of every node with children once, plus ids/uniforms/outcomes) divided by its
+average launch duration measured with HIP events on the launch stream.
+"""
+import argparse
+import hashlib
+import json
+import os
+import sys
+import time
+
+ROOT = os.path.dirname(os.path.abspath(__file__))
+HBM_PEAK_GBPS = 8000.0
+KERNEL_SRC = os.path.join(ROOT, "paper_2608_24411_amd", "csrc", "resispec.hip")
+METRIC = "verified tree-node rows/s at V=128256 + achieved HBM GB/s (% of peak)"
+
+
+def kernel_source_hash():
+    with open(KERNEL_SRC, "rb") as f:
+        return hashlib.sha256(f.read()).hexdigest()
+
+
+def measured_traffic(workload, mode):
+    """HBM bytes per launch of the row kernel from the rocprofv3 counter summary, if the
+    summary was taken on the current kernel source."""
+    path = os.path.join(ROOT, "profiles", "traffic_rs_row_kernel_%s_%s.json" % (workload, mode))
+    if not os.path.exists(path):
+        return None
+    with open(path) as f:
+        rec = json.load(f)
+    if rec.get("kernel_source_sha256") != kernel_source_hash():
+        return None
+    return rec.get("hbm_bytes_per_launch")
+
+
+def cpu_baseline(w, seconds, mode):
+    """The fp64 oracle (all-nodes evaluation, single thread) on a bounded sample of the
+    same workload: whole sequences until about `seconds` of CPU time."""
+    import numpy as np
+    import oracle as O
+    from paper_2608_24411_amd import synth
+    B, N = w["B"], w["N"]
+    rows_done, t_used, seqs = 0, 0.0, 0
+    for b in range(B):
+        sel = [b]
+        h = dict(target=synth.to_host(w["target"][sel]), draft=synth.to_host(w["draft"][sel]),
+                 node_token=synth.to_host(w["node_token"][sel]),
+                 parent=synth.to_host(w["parent"][sel]),
+                 u_accept=synth.to_host(w["u_accept"][sel]),
+                 u_resample=synth.to_host(w["u_resample"][sel]))
+        t0 = time.process_time()
+        O.verify_tree_nodes(h["target"], h["draft"], h["node_token"], h["parent"], h["u_accept"],
+                            h["u_resample"], np.arange(N), temperature=w["temperature"],
+                            mode=mode, without_replacement=w["without_replacement"],
+                            bonus=w["bonus"])
+        t_used += time.process_time() - t0
+        rows_done += N
+        seqs += 1
+        if t_used >= seconds:
+            break
+    return {"value": rows_done / t_used, "unit": "rows/s", "cores": 1, "kind": "oracle",
+            "sample": "%d of %d sequences (%d node rows) of %s, every node evaluated, fp64, "
+                      "one thread, %.1f s CPU" % (seqs, B, rows_done, w["cfg"]["name"], t_used)}
+
+
+def time_mode(native, torch, w, mode, steps, warmup, ws, out_tok, out_len, out_st):
+    args = (w["target"], w["draft"], w["node_token"], w["parent"], w["u_accept"], w["u_resample"])
+    kw = dict(temperature=w["temperature"], mode=mode, without_replacement=w["without_replacement"],
+              bonus=w["bonus"])
+
+    def step(ev0=None, ev1=None):
+        if ev0 is not None:
+            ev0.record()
+        native.resispec_verify_nodes(*args, ws, **kw)
+        if ev1 is not None:
+            ev1.record()
+        native.resispec_walk(w["node_token"], ws, out_tok, out_len, out_st,
+                             max_depth=w["max_depth"])
+
+    for _ in range(warmup):
+        step()
+    ev = [(torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True))
+          for _ in range(steps)]
+    torch.cuda.synchronize()
+    t0 = time.perf_counter()
+    for e0, e1 in ev:
+        step(e0, e1)
+    torch.cuda.synchronize()
+    wall = time.perf_counter() - t0
+    kern_ms = [e0.elapsed_time(e1) for e0, e1 in ev]
+    return wall, kern_ms
+
+
+def main():
+    ap = argparse.ArgumentParser(description=__doc__.split("\n")[0])
+    ap.add_argument("--gpus", type=int, default=1)
+    ap.add_argument("--steps", type=int, default=20)
+    ap.add_argument("--warmup", type=int, default=5)
+    ap.add_argument("--config", type=int, default=2)
+    ap.add_argument("--mode", default="resispec", choices=("resispec", "specinfer"))
+    ap.add_argument("--cpu-seconds", type=float, default=15.0)
+    ap.add_argument("--no-cpu-baseline", action="store_true")
+    ap.add_argument("--no-other-mode", action="store_true")
+    args = ap.parse_args()
+
+    world = int(os.environ.get("WORLD_SIZE", "1"))
+    if args.gpus != 1 or world != 1:
+        print("bench.py runs on exactly one GPU: the verification step shards by sequence "
+              "with no exchange, and multi-GPU runs are not part of this build "
+              "(requested --gpus %d, WORLD_SIZE %d)" % (args.gpus, world), file=sys.stderr)
+        sys.exit(2)
+
+    import numpy as np
+    import torch
+    from paper_2608_24411_amd import native, synth
+
+    torch.cuda.set_device(0)
+    w = synth.make_workload(args.config, device="cuda")
+    B, N, V = w["B"], w["N"], w["V"]
+    esz = 2 if w["target"].dtype == torch.bfloat16 else 4
+    logit_bytes, rows_t, rows_d = synth.algorithmic_bytes(w["parent"].cpu().numpy(), V, esz)
+    small_bytes = 16 * B * N + 12 * B * N      # ids, parents, uniforms in; outcomes out
+    alg_bytes = logit_bytes + small_bytes
+
+    ws = torch.empty(native.resispec_workspace_bytes(B, N), dtype=torch.uint8, device="cuda")
+    out_tok = torch.empty((B, w["max_depth"] + 1), dtype=torch.int32, device="cuda")
+    out_len = torch.empty(B, dtype=torch.int32, device="cuda")
+    out_st = torch.empty(B, dtype=torch.int32, device="cuda")
+
+    results = {}
+    modes = [args.mode] + ([] if args.no_other_mode else
+                           [m for m in ("resispec", "specinfer") if m != args.mode])
+    for mode in modes:
+        wall, kern_ms = time_mode(native, torch, w, mode, args.steps, args.warmup, ws, out_tok,
+                                  out_len, out_st)
+        lens = out_len.cpu().numpy()
+        assert (out_st.cpu().numpy() == 0).all(), "device status not OK"
+        kms = float(np.mean(kern_ms))
+        results[mode] = {
+            "ms_per_step": 1e3 * wall / args.steps,
+            "rows_per_s": B * N / (wall / args.steps),
+            "row_kernel_ms": kms,
+            "row_kernel_ms_min": float(np.min(kern_ms)),
+            "row_kernel_gbps": alg_bytes / (kms * 1e-3) / 1e9,
+            "mean_accepted_len": float(lens.mean()),
+        }
+
+    r = results[args.mode]
+    achieved = r["row_kernel_gbps"]
+    out = {
+        "metric": METRIC,
+        "value": r["rows_per_s"],
+        "unit": "rows/s",
+        "n_gpus": 1,
+        "steps": args.steps,
+        "warmup": args.warmup,
+        "ms_per_step": r["ms_per_step"],
+        "higher_is_better": True,
+        "scaling": "weak",
+        "vs_baseline": None,
+        "dtype": "f32",
+        "data": "synthetic",
+        "config": {"workload": w["cfg"]["name"], "B": B, "N": N, "V": V,
+                   "logits": "bf16" if esz == 2 else "f32", "mode": args.mode,
+                   "temperature": w["temperature"],
+                   "without_replacement": bool(w["without_replacement"])},
+        "roofline": {"bound": "hbm", "achieved": achieved, "peak": HBM_PEAK_GBPS, "unit": "GB/s",
+                     "frac": achieved / HBM_PEAK_GBPS,
+                     "traffic": measured_traffic(w["cfg"]["name"], args.mode),
+                     "kernel": "rs_row_kernel", "alg_bytes_per_launch": alg_bytes,
+                     "rows_target": rows_t, "rows_draft": rows_d},
+        "modes": results,
+    }
+    if not args.no_cpu_baseline:
+        out["cpu_baseline"] = cpu_baseline(w, args.cpu_seconds, args.mode)
+    print(json.dumps(out), flush=True)
+
+
+if __name__ == "__main__":
+    main()

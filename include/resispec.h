@@ -1,0 +1,200 @@
+/*
+ * resispec.h -- C ABI of libresispec.so, the MI355X (gfx950) verification step of
+ * ResiSpec multi-candidate speculative sampling.
+ *
+ * What it computes (paper: "ResiSpec: Enhancing Multi-Candidate Speculative
+ * Sampling via Residual Distribution Shaping"):
+ *   for every node of a batch of draft trees, the temperature softmax of the
+ *   target and draft logits over the whole vocabulary (Preliminary), the
+ *   sequential accept/reject of the node's candidates with acceptance
+ *   min(1, R(x)/D(x)) against the current residual R (Eq. 2, Algorithm 1), the
+ *   residual update after each rejection -- the standard norm(max(R - D, 0))
+ *   (Eq. 1/2, mode RS_MODE_SPECINFER) or ResiSpec's proxy-shaped residual
+ *   norm(max(R - GetProxy(R, D, x), 0)) (Algorithm 1, mode RS_MODE_RESISPEC) --
+ *   and the inverse-CDF draw from the final residual when every candidate is
+ *   rejected; then a walk from each root that follows accepted children and
+ *   returns the accepted tokens (Preliminary, tree-structured verification).
+ *
+ * Conventions shared by every entry point:
+ *   - All array arguments are DEVICE pointers owned by the caller unless stated
+ *     otherwise.  The library never allocates, frees or keeps them.
+ *   - Calls are asynchronous on `stream` (a hipStream_t; NULL = the default
+ *     stream).  Results are valid once the stream reaches the call.  No entry
+ *     point synchronises the device.
+ *   - Argument errors are returned synchronously as rs_status and nothing is
+ *     launched.  Data faults found on the device (bad token ids, a candidate
+ *     with zero draft probability, a malformed tree, out-of-range uniforms) are
+ *     reported per row / per sequence in out_status (rs_seq_status); the outputs
+ *     of such a row/sequence are -1.
+ *   - Logits rows are contiguous over the vocabulary.  fp32 or bf16 (raw bf16,
+ *     widened exactly to fp32 in the kernel).  Rows whose byte length is a
+ *     multiple of 16 and whose base pointer is 16-byte aligned take the
+ *     vectorised path; any other V or alignment is handled element by element.
+ *   - Uniforms are fp32 in [0, 1).  The accept test is strict: u < ratio.
+ *   - Thread safety: calls are stateless and re-entrant.
+ */
+#ifndef RESISPEC_H
+#define RESISPEC_H
+
+#include <stddef.h>
+#include <stdint.h>
+
+#ifdef __cplusplus
+extern "C" {
+#endif
+
+#define RESISPEC_ABI_VERSION 1
+
+/* Largest number of candidates (children) one node may have. */
+#define RS_MAX_CANDIDATES 64
+/* Largest supported vocabulary. */
+#define RS_MAX_VOCAB (1 << 22)
+
+typedef enum {
+    RS_OK = 0,
+    RS_ERR_INVALID_ARG = 1,  /* NULL pointer, non-positive size, T <= 0, unknown mode/dtype */
+    RS_ERR_WORKSPACE = 2,    /* workspace NULL or smaller than resispec_workspace_bytes() */
+    RS_ERR_UNSUPPORTED = 3,  /* size beyond RS_MAX_VOCAB / RS_MAX_CANDIDATES */
+    RS_ERR_HIP = 4           /* a HIP launch error */
+} rs_status;
+
+/* Per-row / per-sequence device-side status (out_status). */
+typedef enum {
+    RS_SEQ_OK = 0,
+    RS_SEQ_BAD_TOKEN = 1,        /* candidate id outside [0, V) */
+    RS_SEQ_ZERO_DRAFT = 2,       /* a tested candidate has current draft probability 0 */
+    RS_SEQ_UNDERFLOW = 3,        /* softmax or residual total is 0 (e.g. an all -inf row) */
+    RS_SEQ_BAD_TREE = 4,         /* parent[.,0] != -1 or parent[n] not in [0, n) */
+    RS_SEQ_BAD_UNIFORM = 5,      /* a used uniform outside [0, 1) */
+    RS_SEQ_DEPTH_EXCEEDED = 6,   /* accepted path longer than max_depth */
+    RS_SEQ_TOO_MANY_CHILDREN = 7 /* a node with more than RS_MAX_CANDIDATES children */
+} rs_seq_status;
+
+typedef enum { RS_MODE_RESISPEC = 0, RS_MODE_SPECINFER = 1 } rs_mode;
+typedef enum { RS_F32 = 0, RS_BF16 = 1 } rs_dtype;
+
+typedef struct {
+    int32_t mode;                /* rs_mode */
+    int32_t logits_dtype;        /* rs_dtype, same for target and draft */
+    float   temperature;         /* > 0; softmax((l - max l) / T) for target and draft alike */
+    int32_t without_replacement; /* 1: candidates of a node were drawn without replacement;
+                                    each rejected id leaves the draft, which is renormalised
+                                    before the next sibling is tested */
+    int32_t bonus;               /* tree only: 1 = a walk that ends at a leaf draws one more
+                                    token from that leaf's target distribution */
+} rs_params;
+
+/*
+ * Flat verify: row b of the target/draft logits is one position with k candidates
+ * (Eq. 2 / Algorithm 1 on a single node per row).
+ *   target_logits, draft_logits : [B][V] fp32 or bf16 (prm->logits_dtype)
+ *   cand_ids                    : [B][k] int32, verified in column order
+ *   u_accept                    : [B][k] fp32, column i is the uniform of candidate i
+ *   u_resample                  : [B]    fp32, uniform of the final draw
+ *   out_token                   : [B] int32  accepted candidate id, or the id drawn
+ *                                 from the final residual when all k are rejected
+ *   out_accepted_len            : [B] int32  1 if a candidate was accepted, else 0
+ *   out_status                  : [B] int32  rs_seq_status; may be NULL
+ * k = 0 draws directly from the target distribution.  B = 0 is a no-op.
+ */
+rs_status resispec_verify(const void* target_logits, const void* draft_logits,
+                          const int32_t* cand_ids, const float* u_accept,
+                          const float* u_resample, int32_t B, int32_t V, int32_t k,
+                          const rs_params* prm, int32_t* out_token,
+                          int32_t* out_accepted_len, int32_t* out_status, void* stream);
+
+/*
+ * Tree verify over B sequences of N nodes each (node 0 = root).
+ *   target_logits, draft_logits : [B][N][V]; row n is the target / draft distribution
+ *                                 over the tokens that follow node n (the distribution
+ *                                 node n's children were drawn from).  Draft rows of
+ *                                 leaf nodes are never read.
+ *   node_token                  : [B][N] int32 token of each node (entry 0 ignored)
+ *   parent                      : [B][N] int32 parent node, parent[.,0] = -1 and
+ *                                 parent[.,n] in [0, n) (topological numbering)
+ *   u_accept                    : [B][N] fp32, entry n is used when node n is tested
+ *   u_resample                  : [B][N] fp32, entry n is used when node n draws from its
+ *                                 final residual (all children rejected) or its bonus
+ *   max_depth                   : >= depth of the deepest node; out_tokens row width is
+ *                                 max_depth + 1
+ *   out_tokens                  : [B][max_depth+1] int32 accepted draft tokens followed by
+ *                                 the drawn token, padded with -1
+ *   out_accepted_len            : [B] int32 number of accepted draft tokens (-1 on a fault)
+ *   out_status                  : [B] int32 rs_seq_status; may be NULL
+ *   workspace                   : device buffer of at least resispec_workspace_bytes(B, N)
+ *                                 bytes (per-node outcomes); contents on entry are ignored
+ * Children of a node are tested in ascending node index.  Every node's outcome is
+ * computed independently (each node owns its uniforms), then a walk from the root
+ * follows accepted children; the result equals the sequential walk.
+ */
+rs_status resispec_verify_tree(const void* target_logits, const void* draft_logits,
+                               const int32_t* node_token, const int32_t* parent,
+                               const float* u_accept, const float* u_resample,
+                               int32_t B, int32_t N, int32_t V, int32_t max_depth,
+                               const rs_params* prm, int32_t* out_tokens,
+                               int32_t* out_accepted_len, int32_t* out_status,
+                               void* workspace, size_t workspace_bytes, void* stream);
+
+/*
+ * The two stages of resispec_verify_tree, for callers that schedule them separately
+ * (same kernels, same results):
+ *   resispec_verify_nodes: every node's own outcome (accepted child or drawn token) into
+ *     `workspace`, from the same inputs as resispec_verify_tree;
+ *   resispec_walk: the walk from each root over the outcomes in `workspace` (written by
+ *     resispec_verify_nodes with the same B and N, earlier on the same stream).
+ * The workspace layout is private to the library.
+ */
+rs_status resispec_verify_nodes(const void* target_logits, const void* draft_logits,
+                                const int32_t* node_token, const int32_t* parent,
+                                const float* u_accept, const float* u_resample,
+                                int32_t B, int32_t N, int32_t V, const rs_params* prm,
+                                void* workspace, size_t workspace_bytes, void* stream);
+
+rs_status resispec_walk(const int32_t* node_token, int32_t B, int32_t N, int32_t max_depth,
+                        const void* workspace, size_t workspace_bytes, int32_t* out_tokens,
+                        int32_t* out_accepted_len, int32_t* out_status, void* stream);
+
+/* Workspace bytes resispec_verify_tree needs for B sequences of N nodes. */
+size_t resispec_workspace_bytes(int32_t B, int32_t N);
+
+/*
+ * Host-side check of a tree batch (HOST pointers, synchronous, no device work).
+ * Returns RS_OK when every sequence has parent[.,0] = -1, parent[.,n] in [0, n),
+ * at most RS_MAX_CANDIDATES children per node and every node_token (n >= 1) in
+ * [0, V); RS_ERR_INVALID_ARG otherwise.  If first_bad is not NULL it receives the
+ * flat index b*N+n of the first offending entry (or -1).
+ */
+rs_status resispec_validate_tree_host(const int32_t* parent, const int32_t* node_token,
+                                      int32_t B, int32_t N, int32_t V, int64_t* first_bad);
+
+/*
+ * Same as resispec_verify_tree, and also writes each node's own outcome (testing and
+ * debugging; not the timed path):
+ *   node_child  : [B][N] int32 accepted child node index, -1 if none
+ *   node_token_out : [B][N] int32 token the node emits (accepted candidate, drawn token,
+ *                 or -1)
+ *   node_status : [B][N] int32 rs_seq_status of the node
+ *   residual_out: [B][N][V] fp32 or NULL; for nodes that drew a token, the normalised
+ *                 distribution of the draw (final residual, or the target for a bonus);
+ *                 other rows are zero.  Costs one more pass over the logits.
+ */
+rs_status resispec_verify_tree_debug(const void* target_logits, const void* draft_logits,
+                                     const int32_t* node_token, const int32_t* parent,
+                                     const float* u_accept, const float* u_resample,
+                                     int32_t B, int32_t N, int32_t V, int32_t max_depth,
+                                     const rs_params* prm, int32_t* out_tokens,
+                                     int32_t* out_accepted_len, int32_t* out_status,
+                                     void* workspace, size_t workspace_bytes,
+                                     int32_t* node_child, int32_t* node_token_out,
+                                     int32_t* node_status, float* residual_out, void* stream);
+
+/* Static description of a status code. */
+const char* resispec_status_string(int32_t status);
+
+/* RESISPEC_ABI_VERSION of the loaded library. */
+int32_t resispec_abi_version(void);
+
+#ifdef __cplusplus
+}
+#endif
+#endif /* RESISPEC_H */

@@ -67,7 +67,7 @@ def _load():
     lib.or_verify_tree_walk.argtypes = [P, P, i32, P, P, P, P, i32, i32, i64, i32, f32,
                                         i32, i32, i32, P, P, P, P]
     lib.or_verify_tree_nodes.argtypes = [P, P, i32, P, P, P, P, i32, i32, i64, f32,
-                                         i32, i32, i32, P, i64, P, P, P, P, P]
+                                         i32, i32, i32, P, i64, P, P, P, P, P, P]
     for name in ("or_softmax", "or_get_proxy", "or_residual_update", "or_draft_remove",
                  "or_invcdf", "or_verify_node", "or_verify_node_batch", "or_enumerate",
                  "or_verify_tree_walk", "or_verify_tree_nodes"):
@@ -227,15 +227,17 @@ def verify_tree_nodes(target, draft, node_token, parent, u_accept, u_resample, r
     token = np.empty(n, dtype=np.int32)
     status = np.empty(n, dtype=np.int32)
     flagged = np.empty(n, dtype=np.int32)
+    margin = np.empty(n, dtype=np.float64)
     fr = np.empty((n, V)) if want_residual else None
     st = _load().or_verify_tree_nodes(_ptr(t), _ptr(d), dt, _ptr(tok), _ptr(par), _ptr(ua),
                                       _ptr(ur), B, N, V, float(temperature), _MODES[mode],
                                       int(bool(without_replacement)), int(bool(bonus)),
                                       _ptr(rows), n, _ptr(child), _ptr(token), _ptr(status),
-                                      _ptr(flagged), _ptr(fr))
+                                      _ptr(flagged), _ptr(margin), _ptr(fr))
     if st != OK:
         raise ValueError("or_verify_tree_nodes failed (%d)" % st)
-    out = {"child": child, "token": token, "status": status, "flagged": flagged}
+    out = {"child": child, "token": token, "status": status, "flagged": flagged,
+           "margin": margin}
     if want_residual:
         out["final_R"] = fr
     return out

@@ -458,7 +458,7 @@ int32_t or_verify_tree_nodes(const void* target, const void* draft, int32_t dtyp
                              int32_t mode, int32_t without_replacement, int32_t bonus,
                              const int64_t* rows, int64_t n_rows,
                              int32_t* out_child, int32_t* out_token, int32_t* out_status,
-                             int32_t* out_flagged, double* out_final_R) {
+                             int32_t* out_flagged, double* out_margin, double* out_final_R) {
     if (!target || !draft || !node_token || !parent || !u_accept || !u_resample || !rows) return OR_BAD_ARG;
     if (!out_child || !out_token || !out_status || !out_flagged) return OR_BAD_ARG;
     if (B < 0 || N <= 0 || V <= 0 || n_rows < 0) return OR_BAD_ARG;
@@ -486,6 +486,10 @@ int32_t or_verify_tree_nodes(const void* target, const void* draft, int32_t dtyp
         out_token[i] = res.token;
         out_status[i] = res.status;
         out_flagged[i] = res.flagged;
+        if (out_margin) {
+            out_margin[i] = (res.min_accept_margin < res.sample_margin) ? res.min_accept_margin
+                                                                        : res.sample_margin;
+        }
     }
     free(p); free(q); free(kids); free(cand); free(ua);
     return rc;

@@ -126,7 +126,8 @@ int32_t or_verify_tree_walk(const void* target, const void* draft, int32_t dtype
 
 /* Tree batch, independent evaluation of selected nodes (rows[i] = b * N + n).
  * child[i]: accepted child node index or -1; token[i]: the node's emitted token
- * (accepted candidate's id, resampled id, bonus id, or -1); status/flagged per node. */
+ * (accepted candidate's id, resampled id, bonus id, or -1); status/flagged per node;
+ * margin: the smallest decision margin of the node (accept tests and the draw). */
 int32_t or_verify_tree_nodes(const void* target, const void* draft, int32_t dtype,
                              const int32_t* node_token, const int32_t* parent,
                              const float* u_accept, const float* u_resample,
@@ -134,7 +135,8 @@ int32_t or_verify_tree_nodes(const void* target, const void* draft, int32_t dtyp
                              int32_t mode, int32_t without_replacement, int32_t bonus,
                              const int64_t* rows, int64_t n_rows,
                              int32_t* out_child, int32_t* out_token, int32_t* out_status,
-                             int32_t* out_flagged, double* out_final_R /* n_rows*V or NULL */);
+                             int32_t* out_flagged, double* out_margin /* n_rows or NULL */,
+                             double* out_final_R /* n_rows*V or NULL */);
 
 #ifdef __cplusplus
 }

@@ -1,0 +1,136 @@
+"""The C ABI on the host: the library loads, exports every symbol the header declares,
+and its host-only entry points and argument checks behave as documented.  No device
+compute is launched here (every call below returns before any launch)."""
+import ctypes
+import os
+import re
+
+import numpy as np
+import pytest
+
+ROOT = os.path.dirname(os.path.dirname(os.path.abspath(__file__)))
+HEADER_DIR = os.path.join(ROOT, "include")
+
+
+def _declared_functions():
+    names = set()
+    for fn in os.listdir(HEADER_DIR):
+        if not fn.endswith(".h"):
+            continue
+        text = open(os.path.join(HEADER_DIR, fn)).read()
+        text = re.sub(r"/\*.*?\*/", "", text, flags=re.S)
+        for m in re.finditer(r"^[A-Za-z_][\w \t\*]*?\b(resispec_\w+)\s*\(", text, flags=re.M):
+            names.add(m.group(1))
+    return names
+
+
+@pytest.fixture(scope="module")
+def native():
+    from paper_2608_24411_amd import native
+    return native
+
+
+def test_library_exports_every_declared_symbol(native):
+    declared = _declared_functions()
+    assert declared, "no declarations found"
+    assert declared == set(native.EXPORTS)
+    for name in declared:
+        assert hasattr(native.lib, name), name
+        assert hasattr(native, name), name     # binding has the same names
+
+
+def test_abi_version_and_status_strings(native):
+    assert native.resispec_abi_version() == 1
+    for code in range(5):
+        s = native.resispec_status_string(code)
+        assert s.startswith("RS_")
+    assert "unknown" in native.resispec_status_string(99)
+
+
+def test_workspace_bytes(native):
+    assert native.resispec_workspace_bytes(0, 5) == 0
+    assert native.resispec_workspace_bytes(5, 0) == 0
+    for B, N in ((1, 1), (128, 33), (1024, 26), (3, 7)):
+        w = native.resispec_workspace_bytes(B, N)
+        assert w >= 3 * 4 * B * N
+        assert w % 256 == 0
+
+
+def test_validate_tree_host(native):
+    parent = np.array([[-1, 0, 0, 1, 1], [-1, 0, 1, 2, 3]], dtype=np.int32)
+    tok = np.array([[0, 1, 2, 3, 4], [0, 5, 6, 7, 8]], dtype=np.int32)
+    assert native.resispec_validate_tree_host(parent, tok, 16) == (native.RS_OK, -1)
+    bad = parent.copy()
+    bad[1, 3] = 3
+    assert native.resispec_validate_tree_host(bad, tok, 16) == (native.RS_ERR_INVALID_ARG, 8)
+    bad = parent.copy()
+    bad[0, 0] = 0
+    assert native.resispec_validate_tree_host(bad, tok, 16) == (native.RS_ERR_INVALID_ARG, 0)
+    badtok = tok.copy()
+    badtok[1, 4] = 16
+    assert native.resispec_validate_tree_host(parent, badtok, 16) == (native.RS_ERR_INVALID_ARG, 9)
+    star = np.zeros((1, 66), dtype=np.int32)
+    star[0, 0] = -1
+    assert native.resispec_validate_tree_host(star, np.zeros((1, 66), np.int32), 4)[0] == \
+        native.RS_ERR_INVALID_ARG
+    assert native.resispec_validate_tree_host(star[:, :65], np.zeros((1, 65), np.int32), 4)[0] == \
+        native.RS_OK
+
+
+def _prm(native, mode=0, dtype=0, T=1.0):
+    return native.RsParams(mode, dtype, T, 0, 1)
+
+
+def test_argument_errors_return_before_launch(native):
+    lib = native.lib
+    fake = ctypes.c_void_p(0x1000)   # never dereferenced: every call below fails validation
+    i32p = ctypes.c_void_p(0x2000)
+    ok = _prm(native)
+    # flat verify
+    assert lib.resispec_verify(fake, fake, i32p, fake, fake, 4, 100, 2, None, i32p, i32p, None,
+                               None) == native.RS_ERR_INVALID_ARG
+    for bad in (_prm(native, mode=7), _prm(native, dtype=5), _prm(native, T=0.0),
+                _prm(native, T=-1.0), _prm(native, T=float("inf"))):
+        assert lib.resispec_verify(fake, fake, i32p, fake, fake, 4, 100, 2, ctypes.byref(bad),
+                                   i32p, i32p, None, None) == native.RS_ERR_INVALID_ARG
+    assert lib.resispec_verify(None, fake, i32p, fake, fake, 4, 100, 2, ctypes.byref(ok), i32p,
+                               i32p, None, None) == native.RS_ERR_INVALID_ARG
+    assert lib.resispec_verify(fake, fake, i32p, fake, fake, 4, 0, 2, ctypes.byref(ok), i32p,
+                               i32p, None, None) == native.RS_ERR_INVALID_ARG
+    assert lib.resispec_verify(fake, fake, i32p, fake, fake, 4, 100, 65, ctypes.byref(ok), i32p,
+                               i32p, None, None) == native.RS_ERR_UNSUPPORTED
+    assert lib.resispec_verify(fake, fake, i32p, fake, fake, 4, (1 << 22) + 1, 2, ctypes.byref(ok),
+                               i32p, i32p, None, None) == native.RS_ERR_UNSUPPORTED
+    # B = 0 is a no-op
+    assert lib.resispec_verify(None, None, None, None, None, 0, 100, 2, ctypes.byref(ok), None,
+                               None, None, None) == native.RS_OK
+    # tree verify
+    args = [fake, fake, i32p, i32p, fake, fake]
+    assert lib.resispec_verify_tree(*args, 4, 5, 100, 2, ctypes.byref(ok), i32p, i32p, None,
+                                    None, 0, None) == native.RS_ERR_WORKSPACE
+    ws = native.resispec_workspace_bytes(4, 5)
+    assert lib.resispec_verify_tree(*args, 4, 5, 100, 2, ctypes.byref(ok), i32p, i32p, None,
+                                    ctypes.c_void_p(0x10000), ws - 1, None) == native.RS_ERR_WORKSPACE
+    assert lib.resispec_verify_tree(*args, 4, 0, 100, 2, ctypes.byref(ok), i32p, i32p, None,
+                                    fake, ws, None) == native.RS_ERR_INVALID_ARG
+    assert lib.resispec_verify_tree(*args, 4, 5, 100, -1, ctypes.byref(ok), i32p, i32p, None,
+                                    fake, ws, None) == native.RS_ERR_INVALID_ARG
+    assert lib.resispec_verify_tree(fake, None, i32p, i32p, fake, fake, 4, 5, 100, 2,
+                                    ctypes.byref(ok), i32p, i32p, None, fake, ws,
+                                    None) == native.RS_ERR_INVALID_ARG
+    assert lib.resispec_verify_tree(None, None, None, None, None, None, 0, 5, 100, 2,
+                                    ctypes.byref(ok), None, None, None, None, 0,
+                                    None) == native.RS_OK
+    assert lib.resispec_verify_tree_debug(*args, 4, 5, 100, 2, ctypes.byref(ok), i32p, i32p, None,
+                                          None, 0, None, None, None, None,
+                                          None) == native.RS_ERR_INVALID_ARG
+
+
+def test_product_path_has_no_oracle_dependency():
+    """The package and its native sources never reference the oracle."""
+    pkg = os.path.join(ROOT, "paper_2608_24411_amd")
+    for dirpath, _, files in os.walk(pkg):
+        for fn in files:
+            if fn.endswith((".py", ".hip", ".cpp", ".h")):
+                text = open(os.path.join(dirpath, fn)).read()
+                assert "oracle" not in text.lower(), os.path.join(dirpath, fn)
