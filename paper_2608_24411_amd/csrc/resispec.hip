@@ -6,7 +6,7 @@
 //   pass 1   online softmax statistics (max, sum of exp) of the target row and, for
 //            nodes with children, the draft row (Preliminary; temperature T);
 //   tests    candidate i is accepted iff u_i < R_i(x_i) / D_i(x_i) (Eq. 2 and
-//            Algorithm 1), evaluated in fp64 on gathered logits;
+//            Algorithm 1), evaluated in fp64 on the gathered candidate logits;
 //   pass i+1 after the i-th rejection one more pass over the row computes the sums the
 //            residual update needs:
 //              standard (Eq. 1/2):   S = sum_j max(R_j - D_j, 0)
@@ -16,15 +16,21 @@
 //            R_j - m_j gives, with a = Delta / (SR - M), the residual
 //              R'_j = ((1 - a) min(Z D_j, R_j) + a R_j) / Z   (j != x0),   R'_x0 = 0,
 //            i.e. norm(max(R - K, 0)) for the proxy K = R - r, K(x0) = D(x0).  So the
-//            residual is never materialised: every pass re-derives R_j from (p_j, q_j)
-//            through the chain of per-rejection scalars;
+//            residual is never materialised: every pass re-derives R_j from the two
+//            logits of token j through the chain of per-rejection scalars;
 //   draw     when every candidate is rejected (or the node is a leaf: bonus draw from
 //            p), the token is the smallest j whose running sum of the final residual in
 //            vocabulary order exceeds u * total.  The last pass records per-tile partial
 //            sums, so the draw re-reads a single tile.
 //
-// Precision: elements in fp32 (bf16 widened exactly), every sum accumulated in fp64,
-// the per-candidate probabilities and the scalar chain in fp64.
+// Numerics: elements in fp32 (bf16 widened exactly), every sum accumulated in fp64,
+// the candidates' probabilities and the scalar chain in fp64.  Exponents are taken as
+// exp2(l * c2 + K) with c2 = log2(e)/T split into two floats and K = -max * c2 rounded
+// once; the rounding of K is common to a whole row and cancels in the normalisation,
+// and the fp64 gathers use the same constants, so candidate probabilities agree with
+// the fp32 sums they are divided by.  Residual elements are carried in units of the
+// target row's unnormalised mass (the target normaliser is folded into the step
+// constants).
 //
 // A second kernel walks each tree from the root along accepted children.
 
@@ -42,7 +48,6 @@ constexpr int kBlock = 512;
 constexpr int kWaves = kBlock / 64;
 constexpr int kMaxCand = RS_MAX_CANDIDATES;
 constexpr int kMaxTiles = 64;
-constexpr float kLog2e = 1.4426950408889634f;
 
 // ------------------------------------------------------------------ loads ----
 
@@ -52,49 +57,72 @@ __device__ __forceinline__ float bf16_hi(uint32_t w) { return __uint_as_float(w 
 __device__ __forceinline__ float widen(float x) { return x; }
 __device__ __forceinline__ float widen(uint16_t h) { return __uint_as_float(((uint32_t)h) << 16); }
 
-// VEC consecutive elements starting at element idx; elements at or beyond V read as
-// -inf, which makes them contribute exactly zero to every sum below.
+// VEC consecutive elements starting at element idx, kept as raw words until used;
+// elements at or beyond V read as -inf, which makes them contribute exactly zero to
+// every sum below.
 template <typename In, int VEC>
-struct Loader;
+struct Vec;
 
 template <>
-struct Loader<float, 4> {
-    static __device__ __forceinline__ void load(const float* __restrict__ row, int64_t idx,
-                                                int64_t V, float (&v)[4]) {
-        if (idx < V) {
-            const float4 t = *reinterpret_cast<const float4*>(row + idx);
-            v[0] = t.x; v[1] = t.y; v[2] = t.z; v[3] = t.w;
-        } else {
-#pragma unroll
-            for (int e = 0; e < 4; ++e) v[e] = -INFINITY;
-        }
+struct Vec<float, 4> {
+    using raw = uint4;
+    static __device__ __forceinline__ raw load(const float* __restrict__ row, int idx, int V) {
+        if (idx < V) return *reinterpret_cast<const uint4*>(row + idx);
+        return make_uint4(0xff800000u, 0xff800000u, 0xff800000u, 0xff800000u);
+    }
+    static __device__ __forceinline__ void unpack(const raw& r, float (&v)[4]) {
+        v[0] = __uint_as_float(r.x); v[1] = __uint_as_float(r.y);
+        v[2] = __uint_as_float(r.z); v[3] = __uint_as_float(r.w);
     }
 };
 
 template <>
-struct Loader<uint16_t, 8> {
-    static __device__ __forceinline__ void load(const uint16_t* __restrict__ row, int64_t idx,
-                                                int64_t V, float (&v)[8]) {
-        if (idx < V) {
-            const uint4 t = *reinterpret_cast<const uint4*>(row + idx);
-            v[0] = bf16_lo(t.x); v[1] = bf16_hi(t.x);
-            v[2] = bf16_lo(t.y); v[3] = bf16_hi(t.y);
-            v[4] = bf16_lo(t.z); v[5] = bf16_hi(t.z);
-            v[6] = bf16_lo(t.w); v[7] = bf16_hi(t.w);
-        } else {
-#pragma unroll
-            for (int e = 0; e < 8; ++e) v[e] = -INFINITY;
-        }
+struct Vec<uint16_t, 8> {
+    using raw = uint4;
+    static __device__ __forceinline__ raw load(const uint16_t* __restrict__ row, int idx, int V) {
+        if (idx < V) return *reinterpret_cast<const uint4*>(row + idx);
+        return make_uint4(0xff80ff80u, 0xff80ff80u, 0xff80ff80u, 0xff80ff80u);
+    }
+    static __device__ __forceinline__ void unpack(const raw& r, float (&v)[8]) {
+        v[0] = bf16_lo(r.x); v[1] = bf16_hi(r.x);
+        v[2] = bf16_lo(r.y); v[3] = bf16_hi(r.y);
+        v[4] = bf16_lo(r.z); v[5] = bf16_hi(r.z);
+        v[6] = bf16_lo(r.w); v[7] = bf16_hi(r.w);
     }
 };
 
-template <typename In>
-struct Loader<In, 1> {
-    static __device__ __forceinline__ void load(const In* __restrict__ row, int64_t idx,
-                                                int64_t V, float (&v)[1]) {
-        v[0] = (idx < V) ? widen(row[idx]) : -INFINITY;
+template <>
+struct Vec<float, 1> {
+    using raw = uint32_t;
+    static __device__ __forceinline__ raw load(const float* __restrict__ row, int idx, int V) {
+        return idx < V ? __float_as_uint(row[idx]) : 0xff800000u;
     }
+    static __device__ __forceinline__ void unpack(const raw& r, float (&v)[1]) { v[0] = __uint_as_float(r); }
 };
+
+template <>
+struct Vec<uint16_t, 1> {
+    using raw = uint32_t;
+    static __device__ __forceinline__ raw load(const uint16_t* __restrict__ row, int idx, int V) {
+        return idx < V ? ((uint32_t)row[idx]) << 16 : 0xff800000u;
+    }
+    static __device__ __forceinline__ void unpack(const raw& r, float (&v)[1]) { v[0] = __uint_as_float(r); }
+};
+
+// Unpacked elements of one vector (used outside the streaming passes).
+template <typename In, int VEC>
+__device__ __forceinline__ void load_vec(const In* __restrict__ row, int idx, int V, float (&v)[VEC]) {
+    Vec<In, VEC>::unpack(Vec<In, VEC>::load(row, idx, V), v);
+}
+
+// v_exp_f32: 2^x; results below the normal range flush to zero (they are more than
+// 2^-126 below the row maximum and carry no mass at fp32 resolution).
+__device__ __forceinline__ float exp2_fast(float x) { return __builtin_amdgcn_exp2f(x); }
+
+// exponent l * c2 + K with c2 = c2h + c2l (both > 0; see base_params)
+__device__ __forceinline__ float expo(float l, float c2h, float c2l, float K) {
+    return fmaf(l, c2l, fmaf(l, c2h, K));
+}
 
 // ------------------------------------------------------------- wave ops ----
 
@@ -121,35 +149,37 @@ __device__ __forceinline__ double wave_incl_scan(double v, int lane) {
 
 // ------------------------------------------------------------ row state ----
 
-struct StepConst {      // one rejection, in the order the candidates were tested
-    int32_t x;          // rejected token
-    float zf, af, invf; // ResiSpec: Z, a, 1/Z.  Standard: invf = 1/S
-    float dscalef;      // draft scale of this step (without replacement)
-    double z, a, inv, dscale;
-};
-
 struct Smem {
     int32_t status;
     int32_t nc;
     int32_t decision;     // -1 continue, >= 0 accepted candidate, -2 fault
-    int32_t nrej;
     float ur;
-    float mt, md;         // raw-logit row maxima
-    double St, Sd;        // sums of exp((l - max)/T)
+    float Kt, Kd;         // exponent offsets -max * c2 of target / draft
+    double St, Sd;        // sums of exp2(l c2 + K)
     int32_t cand_tok[kMaxCand];
     int32_t cand_node[kMaxCand];
     float cand_u[kMaxCand];
+    float cand_lt[kMaxCand];
+    float cand_ld[kMaxCand];
     double cand_p[kMaxCand];
     double cand_q[kMaxCand];
-    StepConst step[kMaxCand + 1];
+    // rejection steps, in test order; fp32 copies are in target-mass units
+    int32_t st_x[kMaxCand + 1];
+    int32_t st_iter[kMaxCand + 1];  // loop iteration that holds token x
+    float st_c[kMaxCand + 1];       // ResiSpec: Z * dscale * St/Sd.  Standard: dscale * St/Sd
+    float st_a[kMaxCand + 1];       // ResiSpec: a
+    float st_i[kMaxCand + 1];       // ResiSpec: 1/Z.  Standard: 1/S
+    double st_zd[kMaxCand + 1], st_ad[kMaxCand + 1], st_id[kMaxCand + 1];
+    double st_ds[kMaxCand + 1];     // draft scale (without replacement)
     // per-tile partials written by one wave each
     double tpA[kMaxTiles][kWaves];
     double tpB[kMaxTiles][kWaves];
-    float tpM[kMaxTiles][kWaves];
+    float tpK[kMaxTiles][kWaves];
     double tileT[kMaxTiles];
     // cross-wave reductions
-    float redf[2][kWaves];
-    double redd[2][kWaves];
+    float redm[2][kWaves];
+    float redk[2][kWaves];
+    double reds[2][kWaves];
     double scan_w[kWaves];
     int32_t first_w[kWaves + 1];
     // draw
@@ -179,85 +209,17 @@ struct KParams {
     int32_t* node_status;
     float* residual_out;
     int32_t B, N;
-    int64_t V;
+    int32_t V;
     float T;
-    float c2;          // log2(e) / T
+    float c2h, c2l;      // log2(e) / T = c2h + c2l
     int32_t worep, bonus, flat;
-    int32_t tile_iters; // loop iterations per tile
+    int32_t niters;      // loop iterations per pass
+    int32_t tile_iters;  // loop iterations per tile
     int32_t ntiles;
 };
 
-// Per-element state of the residual chain after `nsteps` rejections, starting from
-// p_j = exp2((lt - mt) c2) / St and q_j likewise (fp32).
-template <int MODE>
-__device__ __forceinline__ void apply_chain(float& R, float& D, bool& removed, int64_t j,
-                                            float q, const StepConst* __restrict__ st,
-                                            int nsteps, bool worep) {
-    for (int t = 0; t < nsteps; ++t) {
-        const StepConst& s = st[t];
-        const float Dt = removed ? 0.0f : q * s.dscalef;
-        if (MODE == RS_MODE_SPECINFER) {
-            R = fmaxf(R - Dt, 0.0f) * s.invf;
-        } else {
-            if (j == (int64_t)s.x) {
-                R = 0.0f;
-            } else {
-                const float m = fminf(s.zf * Dt, R);
-                R = ((1.0f - s.af) * m + s.af * R) * s.invf;
-            }
-        }
-        if (worep && j == (int64_t)s.x) removed = true;
-    }
-    D = removed ? 0.0f : q * st[nsteps].dscalef;
-}
-
-// Quantities of rejection step `i` for one element (chain over steps 0..i-1 first):
-//   standard: A = max(R - D, 0), B unused
-//   ResiSpec: A = min(Z D, R), B = R, both zero at the rejected token.
-template <int MODE>
-__device__ __forceinline__ void step_terms(float lt, float ld, int64_t j, const Smem& sm, float c2,
-                                           float invSt, float invSd, int i, bool worep,
-                                           float& A, float& Bv) {
-    const float p = exp2f((lt - sm.mt) * c2) * invSt;
-    const float q = exp2f((ld - sm.md) * c2) * invSd;
-    float R = p, D;
-    bool removed = false;
-    apply_chain<MODE>(R, D, removed, j, q, sm.step, i, worep);
-    if (MODE == RS_MODE_SPECINFER) {
-        A = fmaxf(R - D, 0.0f);
-        Bv = 0.0f;
-    } else {
-        const bool x0 = (j == (int64_t)sm.step[i].x);
-        A = x0 ? 0.0f : fminf(sm.step[i].zf * D, R);
-        Bv = x0 ? 0.0f : R;
-    }
-}
-
-// Scalar chain for the accept test of candidate i (fp64).
-template <int MODE>
-__device__ double scalar_residual(const Smem& sm, int i, double p, double q, int32_t x,
-                                  bool worep, double& Dout) {
-    double R = p;
-    bool removed = false;
-    for (int t = 0; t < i; ++t) {
-        const StepConst& s = sm.step[t];
-        const double Dt = removed ? 0.0 : q * s.dscale;
-        if (MODE == RS_MODE_SPECINFER) {
-            const double w = R - Dt;
-            R = (w > 0.0 ? w : 0.0) * s.inv;
-        } else {
-            if (x == s.x) {
-                R = 0.0;
-            } else {
-                const double zd = s.z * Dt;
-                const double m = zd < R ? zd : R;
-                R = ((1.0 - s.a) * m + s.a * R) / s.z;
-            }
-        }
-        if (worep && x == s.x) removed = true;
-    }
-    Dout = removed ? 0.0 : q * sm.step[i].dscale;
-    return R;
+__device__ __forceinline__ float kref(float m, float c2h) {
+    return m > -FLT_MAX ? -(m * c2h) : 0.0f;
 }
 
 __device__ __forceinline__ void write_outcome(const KParams& P, int64_t row, int32_t child,
@@ -274,11 +236,118 @@ __device__ __forceinline__ void write_outcome(const KParams& P, int64_t row, int
     }
 }
 
-template <typename In, int VEC>
 __device__ void zero_residual_row(const KParams& P, int64_t row) {
     if (!P.residual_out) return;
     float* out = P.residual_out + row * P.V;
-    for (int64_t j = threadIdx.x; j < P.V; j += kBlock) out[j] = 0.0f;
+    for (int j = threadIdx.x; j < P.V; j += kBlock) out[j] = 0.0f;
+}
+
+// Rejection-step terms of one element, given its target mass R (target units) and
+// unnormalised draft mass Q.  The chain over the earlier steps 0..i-1 first.
+//   standard: A = max(R - c_i Q, 0)                    (c_i = dscale_i St/Sd)
+//   ResiSpec: A = min(c_i Q, R), B = R, both 0 at x_i   (c_i = Z_i dscale_i St/Sd)
+// CHECK = false skips the token comparisons (no rejected token in this element's
+// loop iteration); the standard update needs none: R < D at every rejected token.
+template <int MODE, bool CHECK>
+__device__ __forceinline__ void chain_terms(float R, float Q, int j, const Smem& sm, int i,
+                                            float& A, float& Bv) {
+    for (int t = 0; t < i; ++t) {
+        const float c = sm.st_c[t];
+        if (MODE == RS_MODE_SPECINFER) {
+            R = fmaxf(fmaf(-c, Q, R), 0.0f) * sm.st_i[t];
+        } else {
+            const float m = fminf(c * Q, R);
+            R = fmaf(sm.st_a[t], R - m, m) * sm.st_i[t];
+            if (CHECK && j == sm.st_x[t]) R = 0.0f;
+        }
+    }
+    const float c = sm.st_c[i];
+    if (MODE == RS_MODE_SPECINFER) {
+        A = fmaxf(fmaf(-c, Q, R), 0.0f);
+        Bv = 0.0f;
+    } else {
+        const bool x0 = CHECK && j == sm.st_x[i];
+        A = x0 ? 0.0f : fminf(c * Q, R);
+        Bv = x0 ? 0.0f : R;
+    }
+}
+
+// Scalar chain for the accept test of candidate i (fp64, normalised units).
+template <int MODE>
+__device__ double scalar_residual(const Smem& sm, int i, double p, double q, int32_t x,
+                                  bool worep, double& Dout) {
+    double R = p;
+    bool removed = false;
+    for (int t = 0; t < i; ++t) {
+        const double Dt = removed ? 0.0 : q * sm.st_ds[t];
+        if (MODE == RS_MODE_SPECINFER) {
+            const double w = R - Dt;
+            R = (w > 0.0 ? w : 0.0) * sm.st_id[t];
+        } else {
+            if (x == sm.st_x[t]) {
+                R = 0.0;
+            } else {
+                const double zd = sm.st_zd[t] * Dt;
+                const double m = zd < R ? zd : R;
+                R = ((1.0 - sm.st_ad[t]) * m + sm.st_ad[t] * R) / sm.st_zd[t];
+            }
+        }
+        if (worep && x == sm.st_x[t]) removed = true;
+    }
+    Dout = removed ? 0.0 : q * sm.st_ds[i];
+    return R;
+}
+
+// One sweep over the row with register prefetch of the next iteration.  body(t, d,
+// idx0, it) gets the UNR x VEC unpacked elements of iteration `it`; element (u, e)
+// has index idx0 + u * kBlock * VEC + e.  flush(tile) runs after the last iteration
+// of a tile.
+template <typename In, int VEC, int UNR, bool PAIR, typename Body, typename Flush>
+__device__ __forceinline__ void sweep(const In* __restrict__ tg, const In* __restrict__ dg,
+                                      int V, int niters, int ti, bool reverse, Body&& body,
+                                      Flush&& flush) {
+    using W = Vec<In, VEC>;
+    using raw = typename W::raw;
+    constexpr int ITER = kBlock * VEC * UNR;
+    const int lane0 = threadIdx.x * VEC;
+    raw ct[UNR], cd[UNR];
+    int it = reverse ? niters - 1 : 0;
+#pragma unroll
+    for (int u = 0; u < UNR; ++u) {
+        ct[u] = W::load(tg, it * ITER + u * kBlock * VEC + lane0, V);
+        if (PAIR) cd[u] = W::load(dg, it * ITER + u * kBlock * VEC + lane0, V);
+    }
+    int tile = it / ti;
+    int edge = reverse ? tile * ti : min((tile + 1) * ti, niters) - 1;
+    for (int k = 0; k < niters; ++k) {
+        const int nit = reverse ? it - 1 : it + 1;
+        raw nt[UNR], nd[UNR];
+        if (k + 1 < niters) {
+#pragma unroll
+            for (int u = 0; u < UNR; ++u) {
+                nt[u] = W::load(tg, nit * ITER + u * kBlock * VEC + lane0, V);
+                if (PAIR) nd[u] = W::load(dg, nit * ITER + u * kBlock * VEC + lane0, V);
+            }
+        }
+        float t[UNR][VEC], d[UNR][VEC];
+#pragma unroll
+        for (int u = 0; u < UNR; ++u) {
+            W::unpack(ct[u], t[u]);
+            if (PAIR) W::unpack(cd[u], d[u]);
+        }
+        body(t, d, it * ITER + lane0, it);
+        if (it == edge) {
+            flush(tile);
+            tile += reverse ? -1 : 1;
+            edge = reverse ? tile * ti : min((tile + 1) * ti, niters) - 1;
+        }
+#pragma unroll
+        for (int u = 0; u < UNR; ++u) {
+            ct[u] = nt[u];
+            if (PAIR) cd[u] = nd[u];
+        }
+        it = nit;
+    }
 }
 
 // ------------------------------------------------------------ row kernel ----
@@ -289,8 +358,8 @@ __global__ void __launch_bounds__(kBlock) rs_row_kernel(const KParams P) {
     const int tid = threadIdx.x;
     const int lane = tid & 63;
     const int wid = tid >> 6;
-    const int64_t V = P.V;
-    constexpr int64_t ITER = (int64_t)kBlock * VEC * UNR;
+    const int V = P.V;
+    constexpr int ITER = kBlock * VEC * UNR;
 
     int64_t row;
     int32_t b, n;
@@ -306,20 +375,25 @@ __global__ void __launch_bounds__(kBlock) rs_row_kernel(const KParams P) {
         b = g - n * P.B;
         row = (int64_t)b * P.N + n;
     }
+    const In* __restrict__ tg = reinterpret_cast<const In*>(P.tgt) + row * V;
+    const In* __restrict__ dg = reinterpret_cast<const In*>(P.dft) + row * V;
 
-    // ---- row description: candidates, their uniforms, structural checks
+    // ---- row description: candidates, their uniforms and logits, structural checks
     if (tid == 0) {
         sm.status = RS_SEQ_OK;
         sm.nc = 0;
         sm.decision = -1;
-        sm.nrej = 0;
     }
     __syncthreads();
     if (P.flat) {
         if (tid < P.k) {
-            sm.cand_tok[tid] = P.cand_ids[row * P.k + tid];
+            const int32_t x = P.cand_ids[row * P.k + tid];
+            sm.cand_tok[tid] = x;
             sm.cand_u[tid] = P.ua_flat[row * P.k + tid];
             sm.cand_node[tid] = tid;
+            const bool ok = x >= 0 && x < V;
+            sm.cand_lt[tid] = ok ? widen(tg[x]) : 0.0f;
+            sm.cand_ld[tid] = ok ? widen(dg[x]) : 0.0f;
         }
         if (tid == 0) {
             sm.nc = P.k;
@@ -343,9 +417,13 @@ __global__ void __launch_bounds__(kBlock) rs_row_kernel(const KParams P) {
                 if (is_child) {
                     const int idx = count + __popcll(mask & __lanemask_lt());
                     if (idx < kMaxCand) {
-                        sm.cand_tok[idx] = P.node_token[(int64_t)b * P.N + m];
+                        const int32_t x = P.node_token[(int64_t)b * P.N + m];
+                        sm.cand_tok[idx] = x;
                         sm.cand_u[idx] = P.ua[(int64_t)b * P.N + m];
                         sm.cand_node[idx] = m;
+                        const bool ok = x >= 0 && x < V;
+                        sm.cand_lt[idx] = ok ? widen(tg[x]) : 0.0f;
+                        sm.cand_ld[idx] = ok ? widen(dg[x]) : 0.0f;
                     }
                 }
                 count += __popcll(mask);
@@ -362,145 +440,165 @@ __global__ void __launch_bounds__(kBlock) rs_row_kernel(const KParams P) {
     const int nc = sm.nc;
     if (sm.status != RS_SEQ_OK) {
         if (tid == 0) write_outcome(P, row, -1, -1, sm.status);
-        zero_residual_row<In, VEC>(P, row);
+        zero_residual_row(P, row);
         return;
     }
     if (nc == 0 && !P.flat && !P.bonus) {
         if (tid == 0) write_outcome(P, row, -1, -1, RS_SEQ_OK);
-        zero_residual_row<In, VEC>(P, row);
+        zero_residual_row(P, row);
         return;
     }
 
     const bool internal = nc > 0;
-    const In* __restrict__ tg = reinterpret_cast<const In*>(P.tgt) + row * V;
-    const In* __restrict__ dg = reinterpret_cast<const In*>(P.dft) + row * V;
-    const float c2 = P.c2;
-    const double c2d = (double)kLog2e / (double)P.T;
-    const int tile_iters = P.tile_iters;
+    const float c2h = P.c2h, c2l = P.c2l;
+    const int niters = P.niters, ti = P.tile_iters;
 
-    // ---- pass 1: softmax statistics (per-lane running max, rescaled sums)
+    // ---- pass 1: softmax statistics (per-lane running max; sums rescaled exactly
+    // when the reference K = -max * c2 moves)
     {
-        float mt = -FLT_MAX, md = -FLT_MAX;
+        float mt = -FLT_MAX, kt = 0.0f, md = -FLT_MAX, kd = 0.0f;
         double st = 0.0, sd = 0.0;
-        float stile = 0.0f;   // leaf rows: this tile's share of st (same reference mt)
-        int64_t it = 0;
-        for (int64_t base = 0; base < V; base += ITER, ++it) {
-            float tv[UNR][VEC], dv[UNR][VEC];
-#pragma unroll
-            for (int u = 0; u < UNR; ++u)
-                Loader<In, VEC>::load(tg, base + ((int64_t)u * kBlock + tid) * VEC, V, tv[u]);
-            if (internal) {
-#pragma unroll
-                for (int u = 0; u < UNR; ++u)
-                    Loader<In, VEC>::load(dg, base + ((int64_t)u * kBlock + tid) * VEC, V, dv[u]);
+        float stile = 0.0f;   // leaf rows: this tile's share of st (reference kt)
+        auto flush = [&](int tile) {
+            if (internal) return;
+            const float mw = wave_max(mt);
+            const float kw = kref(mw, c2h);
+            const double sw = wave_sum(stile > 0.0f ? (double)stile * exp2((double)kw - (double)kt) : 0.0);
+            if (lane == 0) {
+                sm.tpK[tile][wid] = kw;
+                sm.tpA[tile][wid] = sw;
             }
-            float mx = -FLT_MAX;
-#pragma unroll
-            for (int u = 0; u < UNR; ++u)
-#pragma unroll
-                for (int e = 0; e < VEC; ++e) mx = fmaxf(mx, tv[u][e]);
-            if (mx > mt) {
-                const double f = exp2(((double)mt - (double)mx) * c2d);
-                st *= f;
-                stile = (float)(stile * f);
-                mt = mx;
-            }
-            float acc = 0.0f;
-#pragma unroll
-            for (int u = 0; u < UNR; ++u)
-#pragma unroll
-                for (int e = 0; e < VEC; ++e) acc += exp2f((tv[u][e] - mt) * c2);
-            st += (double)acc;
-            stile += acc;
-            if (internal) {
-                float my = -FLT_MAX;
-#pragma unroll
-                for (int u = 0; u < UNR; ++u)
-#pragma unroll
-                    for (int e = 0; e < VEC; ++e) my = fmaxf(my, dv[u][e]);
-                if (my > md) {
-                    sd *= exp2(((double)md - (double)my) * c2d);
-                    md = my;
-                }
-                float accd = 0.0f;
-#pragma unroll
-                for (int u = 0; u < UNR; ++u)
-#pragma unroll
-                    for (int e = 0; e < VEC; ++e) accd += exp2f((dv[u][e] - md) * c2);
-                sd += (double)accd;
-            } else {
-                const bool tile_end = ((it + 1) % tile_iters == 0) || (base + ITER >= V);
-                if (tile_end) {
-                    const int tile = (int)(it / tile_iters);
-                    const float mw = wave_max(mt);
-                    const double sw = wave_sum((double)stile * exp2(((double)mt - (double)mw) * c2d));
-                    if (lane == 0) {
-                        sm.tpM[tile][wid] = mw;
-                        sm.tpA[tile][wid] = sw;
-                    }
-                    stile = 0.0f;
-                }
-            }
-        }
-        // block combine
-        const float mwt = wave_max(mt);
-        const double swt = wave_sum(st * exp2(((double)mt - (double)mwt) * c2d));
-        float mwd = -FLT_MAX;
-        double swd = 0.0;
+            stile = 0.0f;
+        };
         if (internal) {
-            mwd = wave_max(md);
-            swd = wave_sum(sd * exp2(((double)md - (double)mwd) * c2d));
+            sweep<In, VEC, UNR, true>(tg, dg, V, niters, ti, false,
+                [&](const float (&t)[UNR][VEC], const float (&d)[UNR][VEC], int, int) {
+                    float mx = -FLT_MAX, my = -FLT_MAX;
+#pragma unroll
+                    for (int u = 0; u < UNR; ++u)
+#pragma unroll
+                        for (int e = 0; e < VEC; ++e) {
+                            mx = fmaxf(mx, t[u][e]);
+                            my = fmaxf(my, d[u][e]);
+                        }
+                    if (mx > mt) {
+                        const float nk = -(mx * c2h);
+                        st *= exp2((double)nk - (double)kt);
+                        mt = mx;
+                        kt = nk;
+                    }
+                    if (my > md) {
+                        const float nk = -(my * c2h);
+                        sd *= exp2((double)nk - (double)kd);
+                        md = my;
+                        kd = nk;
+                    }
+                    float a = 0.0f, c = 0.0f;
+#pragma unroll
+                    for (int u = 0; u < UNR; ++u)
+#pragma unroll
+                        for (int e = 0; e < VEC; ++e) {
+                            a += exp2_fast(expo(t[u][e], c2h, c2l, kt));
+                            c += exp2_fast(expo(d[u][e], c2h, c2l, kd));
+                        }
+                    st += (double)a;
+                    sd += (double)c;
+                },
+                flush);
+        } else {
+            sweep<In, VEC, UNR, false>(tg, dg, V, niters, ti, false,
+                [&](const float (&t)[UNR][VEC], const float (&)[UNR][VEC], int, int) {
+                    float mx = -FLT_MAX;
+#pragma unroll
+                    for (int u = 0; u < UNR; ++u)
+#pragma unroll
+                        for (int e = 0; e < VEC; ++e) mx = fmaxf(mx, t[u][e]);
+                    if (mx > mt) {
+                        const float nk = -(mx * c2h);
+                        const double f = exp2((double)nk - (double)kt);
+                        st *= f;
+                        stile = (float)(stile * f);
+                        mt = mx;
+                        kt = nk;
+                    }
+                    float a = 0.0f;
+#pragma unroll
+                    for (int u = 0; u < UNR; ++u)
+#pragma unroll
+                        for (int e = 0; e < VEC; ++e) a += exp2_fast(expo(t[u][e], c2h, c2l, kt));
+                    st += (double)a;
+                    stile += a;
+                },
+                flush);
         }
-        if (lane == 0) {
-            sm.redf[0][wid] = mwt;
-            sm.redd[0][wid] = swt;
-            sm.redf[1][wid] = mwd;
-            sm.redd[1][wid] = swd;
+        // combine lanes, then waves (wave 0)
+        {
+            const float mw = wave_max(mt);
+            const float kw = kref(mw, c2h);
+            const double sw = wave_sum(st > 0.0 ? st * exp2((double)kw - (double)kt) : 0.0);
+            float mw2 = -FLT_MAX, kw2 = 0.0f;
+            double sw2 = 0.0;
+            if (internal) {
+                mw2 = wave_max(md);
+                kw2 = kref(mw2, c2h);
+                sw2 = wave_sum(sd > 0.0 ? sd * exp2((double)kw2 - (double)kd) : 0.0);
+            }
+            if (lane == 0) {
+                sm.redm[0][wid] = mw;
+                sm.redk[0][wid] = kw;
+                sm.reds[0][wid] = sw;
+                sm.redm[1][wid] = mw2;
+                sm.redk[1][wid] = kw2;
+                sm.reds[1][wid] = sw2;
+            }
         }
         __syncthreads();
-        if (tid == 0) {
-            float m0 = -FLT_MAX, m1 = -FLT_MAX;
-            for (int w = 0; w < kWaves; ++w) {
-                m0 = fmaxf(m0, sm.redf[0][w]);
-                m1 = fmaxf(m1, sm.redf[1][w]);
+        if (wid == 0) {
+            const bool in = lane < kWaves;
+            const int w = in ? lane : 0;
+            const float m0 = wave_max(in ? sm.redm[0][w] : -FLT_MAX);
+            const float m1 = wave_max(in ? sm.redm[1][w] : -FLT_MAX);
+            const float k0 = kref(m0, c2h), k1 = kref(m1, c2h);
+            const double s0 = wave_sum(in && sm.reds[0][w] > 0.0
+                                           ? sm.reds[0][w] * exp2((double)k0 - (double)sm.redk[0][w]) : 0.0);
+            const double s1 = wave_sum(in && sm.reds[1][w] > 0.0
+                                           ? sm.reds[1][w] * exp2((double)k1 - (double)sm.redk[1][w]) : 0.0);
+            if (lane == 0) {
+                sm.Kt = k0;
+                sm.Kd = k1;
+                sm.St = s0;
+                sm.Sd = s1;
+                if (!(s0 > 0.0) || (internal && !(s1 > 0.0))) sm.status = RS_SEQ_UNDERFLOW;
+                sm.st_ds[0] = 1.0;
             }
-            double s0 = 0.0, s1 = 0.0;
-            for (int w = 0; w < kWaves; ++w) {
-                s0 += sm.redd[0][w] * exp2(((double)sm.redf[0][w] - (double)m0) * c2d);
-                if (internal) s1 += sm.redd[1][w] * exp2(((double)sm.redf[1][w] - (double)m1) * c2d);
-            }
-            sm.mt = m0;
-            sm.md = m1;
-            sm.St = s0;
-            sm.Sd = s1;
-            if (!(s0 > 0.0) || (internal && !(s1 > 0.0))) sm.status = RS_SEQ_UNDERFLOW;
-            sm.step[0].dscale = 1.0;
-            sm.step[0].dscalef = 1.0f;
         }
         __syncthreads();
         if (sm.status != RS_SEQ_OK) {
             if (tid == 0) write_outcome(P, row, -1, -1, sm.status);
-            zero_residual_row<In, VEC>(P, row);
+            zero_residual_row(P, row);
             return;
         }
     }
 
-    // ---- candidate probabilities in fp64 (gathers)
+    const double c2d = (double)c2h + (double)c2l;
+    const float Kt = sm.Kt, Kd = sm.Kd;
+    const double St = sm.St, Sd = sm.Sd;
+    // draft mass in target units: q St / Sd, folded into the step constants
+    const double q2t = internal ? St / Sd : 0.0;
+
+    // ---- candidate probabilities in fp64, with the same exponent constants
     if (tid < nc) {
         const int32_t x = sm.cand_tok[tid];
         double pc = 0.0, qc = 0.0;
-        if (x >= 0 && (int64_t)x < V) {
-            const double T = (double)P.T;
-            pc = exp(((double)widen(tg[x]) - (double)sm.mt) / T) / sm.St;
-            qc = exp(((double)widen(dg[x]) - (double)sm.md) / T) / sm.Sd;
+        if (x >= 0 && x < V) {
+            pc = exp2((double)sm.cand_lt[tid] * c2d + (double)Kt) / St;
+            qc = exp2((double)sm.cand_ld[tid] * c2d + (double)Kd) / Sd;
         }
         sm.cand_p[tid] = pc;
         sm.cand_q[tid] = qc;
     }
     __syncthreads();
 
-    const float invSt = (float)(1.0 / sm.St);
-    const float invSd = internal ? (float)(1.0 / sm.Sd) : 0.0f;
     const bool worep = P.worep != 0;
 
     // ---- sequential accept / reject
@@ -510,7 +608,7 @@ __global__ void __launch_bounds__(kBlock) rs_row_kernel(const KParams P) {
             const int32_t x = sm.cand_tok[i];
             const float u = sm.cand_u[i];
             int dec = -1;
-            if (x < 0 || (int64_t)x >= V) {
+            if (x < 0 || x >= V) {
                 sm.status = RS_SEQ_BAD_TOKEN;
                 dec = -2;
             } else if (!(u >= 0.0f && u < 1.0f)) {
@@ -525,10 +623,11 @@ __global__ void __launch_bounds__(kBlock) rs_row_kernel(const KParams P) {
                 } else if ((double)u < Rx / Dx) {
                     dec = i;
                 } else {
-                    StepConst& s = sm.step[i];
-                    s.x = x;
-                    s.z = Dx - Rx;   // ResiSpec budget; unused by the standard update
-                    s.zf = (float)s.z;
+                    const double z = Dx - Rx;   // ResiSpec budget
+                    sm.st_x[i] = x;
+                    sm.st_iter[i] = x / ITER;
+                    sm.st_zd[i] = z;
+                    sm.st_c[i] = (float)((MODE == RS_MODE_SPECINFER ? 1.0 : z) * sm.st_ds[i] * q2t);
                 }
             }
             sm.decision = dec;
@@ -539,40 +638,53 @@ __global__ void __launch_bounds__(kBlock) rs_row_kernel(const KParams P) {
         // rejection pass: sums of step i with per-tile partials
         {
             double accA = 0.0, accB = 0.0;   // this tile's lane partials
-            int64_t it = 0;
-            for (int64_t base = 0; base < V; base += ITER, ++it) {
-                float tv[UNR][VEC], dv[UNR][VEC];
-#pragma unroll
-                for (int u = 0; u < UNR; ++u) {
-                    Loader<In, VEC>::load(tg, base + ((int64_t)u * kBlock + tid) * VEC, V, tv[u]);
-                    Loader<In, VEC>::load(dg, base + ((int64_t)u * kBlock + tid) * VEC, V, dv[u]);
+            auto flush = [&](int tile) {
+                const double wa = wave_sum(accA);
+                const double wb = (MODE == RS_MODE_RESISPEC) ? wave_sum(accB) : 0.0;
+                if (lane == 0) {
+                    sm.tpA[tile][wid] = wa;
+                    sm.tpB[tile][wid] = wb;
                 }
-                float fa = 0.0f, fb = 0.0f;
-#pragma unroll
-                for (int u = 0; u < UNR; ++u) {
-#pragma unroll
-                    for (int e = 0; e < VEC; ++e) {
-                        const int64_t j = base + ((int64_t)u * kBlock + tid) * VEC + e;
-                        float A, Bv;
-                        step_terms<MODE>(tv[u][e], dv[u][e], j, sm, c2, invSt, invSd, i, worep, A, Bv);
-                        fa += A;
-                        fb += Bv;
+                accA = accB = 0.0;
+            };
+            const bool reverse = (i & 1) == 0;   // re-read the most recently fetched end first
+            const int ii = i;
+            sweep<In, VEC, UNR, true>(tg, dg, V, niters, ti, reverse,
+                [&](const float (&t)[UNR][VEC], const float (&d)[UNR][VEC], int idx0, int it) {
+                    bool hit = false;
+                    if (MODE == RS_MODE_RESISPEC) {
+                        for (int s = 0; s <= ii; ++s) hit |= (sm.st_iter[s] == it);
                     }
-                }
-                accA += (double)fa;
-                accB += (double)fb;
-                const bool tile_end = ((it + 1) % tile_iters == 0) || (base + ITER >= V);
-                if (tile_end) {
-                    const int tile = (int)(it / tile_iters);
-                    const double wa = wave_sum(accA);
-                    const double wb = (MODE == RS_MODE_RESISPEC) ? wave_sum(accB) : 0.0;
-                    if (lane == 0) {
-                        sm.tpA[tile][wid] = wa;
-                        sm.tpB[tile][wid] = wb;
+                    float fa = 0.0f, fb = 0.0f;
+                    if (!hit) {
+#pragma unroll
+                        for (int u = 0; u < UNR; ++u)
+#pragma unroll
+                            for (int e = 0; e < VEC; ++e) {
+                                const float R = exp2_fast(expo(t[u][e], c2h, c2l, Kt));
+                                const float Q = exp2_fast(expo(d[u][e], c2h, c2l, Kd));
+                                float A, Bv;
+                                chain_terms<MODE, false>(R, Q, 0, sm, ii, A, Bv);
+                                fa += A;
+                                fb += Bv;
+                            }
+                    } else {
+#pragma unroll
+                        for (int u = 0; u < UNR; ++u)
+#pragma unroll
+                            for (int e = 0; e < VEC; ++e) {
+                                const float R = exp2_fast(expo(t[u][e], c2h, c2l, Kt));
+                                const float Q = exp2_fast(expo(d[u][e], c2h, c2l, Kd));
+                                float A, Bv;
+                                chain_terms<MODE, true>(R, Q, idx0 + u * kBlock * VEC + e, sm, ii, A, Bv);
+                                fa += A;
+                                fb += Bv;
+                            }
                     }
-                    accA = accB = 0.0;
-                }
-            }
+                    accA += (double)fa;
+                    accB += (double)fb;
+                },
+                flush);
         }
         __syncthreads();
         if (wid == 0) {
@@ -584,9 +696,9 @@ __global__ void __launch_bounds__(kBlock) rs_row_kernel(const KParams P) {
                 }
             }
             // lane 0's sums, so that every lane derives identical constants
-            const double totA = __shfl(wave_sum(A), 0, 64);
-            const double totB = __shfl(wave_sum(Bv), 0, 64);
-            const double z = sm.step[i].z;
+            const double totA = __shfl(wave_sum(A), 0, 64) / St;   // normalised units
+            const double totB = __shfl(wave_sum(Bv), 0, 64) / St;
+            const double z = sm.st_zd[i];
             double a = 0.0, inv;
             if (MODE == RS_MODE_SPECINFER) {
                 inv = 1.0 / totA;
@@ -601,24 +713,20 @@ __global__ void __launch_bounds__(kBlock) rs_row_kernel(const KParams P) {
                 sm.tileT[lane] = (MODE == RS_MODE_SPECINFER) ? A : (1.0 - a) * A + a * Bv;
             }
             if (lane == 0) {
-                StepConst& s = sm.step[i];
                 if (MODE == RS_MODE_SPECINFER && !(totA > 0.0)) {
                     sm.status = RS_SEQ_UNDERFLOW;
                     sm.decision = -2;
                 }
-                s.a = a;
-                s.af = (float)a;
-                s.inv = inv;
-                s.invf = (float)inv;
-                StepConst& nx = sm.step[i + 1];
+                sm.st_ad[i] = a;
+                sm.st_a[i] = (float)a;
+                sm.st_id[i] = inv;
+                sm.st_i[i] = (float)inv;
                 if (worep) {
-                    const double rest = 1.0 - sm.cand_q[i] * s.dscale;
-                    nx.dscale = rest > 0.0 ? s.dscale / rest : 0.0;
+                    const double rest = 1.0 - sm.cand_q[i] * sm.st_ds[i];
+                    sm.st_ds[i + 1] = rest > 0.0 ? sm.st_ds[i] / rest : 0.0;
                 } else {
-                    nx.dscale = 1.0;
+                    sm.st_ds[i + 1] = 1.0;
                 }
-                nx.dscalef = (float)nx.dscale;
-                sm.nrej = i + 1;
             }
         }
         __syncthreads();
@@ -627,7 +735,7 @@ __global__ void __launch_bounds__(kBlock) rs_row_kernel(const KParams P) {
 
     if (sm.decision == -2) {
         if (tid == 0) write_outcome(P, row, -1, -1, sm.status);
-        zero_residual_row<In, VEC>(P, row);
+        zero_residual_row(P, row);
         return;
     }
     if (sm.decision >= 0) {
@@ -635,7 +743,7 @@ __global__ void __launch_bounds__(kBlock) rs_row_kernel(const KParams P) {
             const int d = sm.decision;
             write_outcome(P, row, sm.cand_node[d], sm.cand_tok[d], RS_SEQ_OK);
         }
-        zero_residual_row<In, VEC>(P, row);
+        zero_residual_row(P, row);
         return;
     }
 
@@ -643,7 +751,7 @@ __global__ void __launch_bounds__(kBlock) rs_row_kernel(const KParams P) {
     const float u = sm.ur;
     if (!(u >= 0.0f && u < 1.0f)) {
         if (tid == 0) write_outcome(P, row, -1, -1, RS_SEQ_BAD_UNIFORM);
-        zero_residual_row<In, VEC>(P, row);
+        zero_residual_row(P, row);
         return;
     }
     const int last = nc - 1;   // index of the last rejection step (internal rows)
@@ -653,8 +761,10 @@ __global__ void __launch_bounds__(kBlock) rs_row_kernel(const KParams P) {
             if (internal) {
                 T = sm.tileT[lane];
             } else {
-                for (int w = 0; w < kWaves; ++w)
-                    T += sm.tpA[lane][w] * exp2(((double)sm.tpM[lane][w] - (double)sm.mt) * c2d);
+                for (int w = 0; w < kWaves; ++w) {
+                    const double s = sm.tpA[lane][w];
+                    if (s > 0.0) T += s * exp2((double)Kt - (double)sm.tpK[lane][w]);
+                }
             }
         }
         const double cum = wave_incl_scan(T, lane);
@@ -679,32 +789,33 @@ __global__ void __launch_bounds__(kBlock) rs_row_kernel(const KParams P) {
     __syncthreads();
     if (sm.status != RS_SEQ_OK) {
         if (tid == 0) write_outcome(P, row, -1, -1, sm.status);
-        zero_residual_row<In, VEC>(P, row);
+        zero_residual_row(P, row);
         return;
     }
 
-    // element values of the final distribution (unnormalised)
-    const double a_last = (internal && MODE == RS_MODE_RESISPEC) ? sm.step[last].a : 0.0;
-    auto final_value = [&](float lt, float ld, int64_t j) -> float {
-        if (!internal) return exp2f((lt - sm.mt) * c2);
+    // element values of the final distribution (unnormalised, target units)
+    const float a_last = (internal && MODE == RS_MODE_RESISPEC) ? sm.st_a[last] : 0.0f;
+    auto final_value = [&](float lt, float ld, int j) -> float {
+        const float R = exp2_fast(expo(lt, c2h, c2l, Kt));
+        if (!internal) return R;
+        const float Q = exp2_fast(expo(ld, c2h, c2l, Kd));
         float A, Bv;
-        step_terms<MODE>(lt, ld, j, sm, c2, invSt, invSd, last, worep, A, Bv);
+        chain_terms<MODE, true>(R, Q, j, sm, last, A, Bv);
         if (MODE == RS_MODE_SPECINFER) return A;
-        const float af = (float)a_last;
-        return (1.0f - af) * A + af * Bv;
+        return fmaf(a_last, Bv - A, A);
     };
 
-    const int64_t tile_elems = (int64_t)tile_iters * ITER;
-    const int64_t CH = tile_elems / kBlock;           // contiguous elements per thread
-    const int64_t t0 = (int64_t)sm.ksel * tile_elems + (int64_t)tid * CH;
+    const int tile_elems = ti * ITER;
+    const int CH = tile_elems / kBlock;           // contiguous elements per thread
+    const int t0 = sm.ksel * tile_elems + tid * CH;
     double own = 0.0;
-    for (int64_t c = 0; c < CH; c += VEC) {
+    for (int c = 0; c < CH; c += VEC) {
         float tv[VEC], dv[VEC];
-        Loader<In, VEC>::load(tg, t0 + c, V, tv);
-        if (internal) Loader<In, VEC>::load(dg, t0 + c, V, dv);
+        load_vec<In, VEC>(tg, t0 + c, V, tv);
+        if (internal) load_vec<In, VEC>(dg, t0 + c, V, dv);
 #pragma unroll
         for (int e = 0; e < VEC; ++e) {
-            const int64_t j = t0 + c + e;
+            const int j = t0 + c + e;
             if (j < V) own += (double)final_value(tv[e], internal ? dv[e] : 0.0f, j);
         }
     }
@@ -745,13 +856,13 @@ __global__ void __launch_bounds__(kBlock) rs_row_kernel(const KParams P) {
     }
     if (tid == chosen) {
         double acc = tbase + excl;
-        int64_t tok = -1, lastpos = -1;
-        for (int64_t c = 0; c < CH && tok < 0; c += VEC) {
+        int tok = -1, lastpos = -1;
+        for (int c = 0; c < CH && tok < 0; c += VEC) {
             float tv[VEC], dv[VEC];
-            Loader<In, VEC>::load(tg, t0 + c, V, tv);
-            if (internal) Loader<In, VEC>::load(dg, t0 + c, V, dv);
+            load_vec<In, VEC>(tg, t0 + c, V, tv);
+            if (internal) load_vec<In, VEC>(dg, t0 + c, V, dv);
             for (int e = 0; e < VEC; ++e) {
-                const int64_t j = t0 + c + e;
+                const int j = t0 + c + e;
                 if (j >= V) break;
                 const float v = final_value(tv[e], internal ? dv[e] : 0.0f, j);
                 if (v > 0.0f) lastpos = j;
@@ -763,7 +874,7 @@ __global__ void __launch_bounds__(kBlock) rs_row_kernel(const KParams P) {
             }
         }
         if (tok < 0) tok = lastpos;
-        sm.token = (int32_t)tok;
+        sm.token = tok;
     }
     __syncthreads();
     const int32_t tok = sm.token;
@@ -776,7 +887,7 @@ __global__ void __launch_bounds__(kBlock) rs_row_kernel(const KParams P) {
     if (P.residual_out) {
         float* out = P.residual_out + row * V;
         const double inv_total = 1.0 / sm.total;
-        for (int64_t j = tid; j < V; j += kBlock) {
+        for (int j = tid; j < V; j += kBlock) {
             const float lt = widen(tg[j]);
             const float ld = internal ? widen(dg[j]) : 0.0f;
             out[j] = (float)((double)final_value(lt, ld, j) * inv_total);
@@ -852,8 +963,9 @@ rs_status check_params(const rs_params* prm) {
 template <typename In, int VEC, int UNR, int MODE>
 hipError_t launch_rows_t(KParams P, int64_t nrows, hipStream_t s) {
     constexpr int64_t ITER = (int64_t)kBlock * VEC * UNR;
-    const int64_t niters = (P.V + ITER - 1) / ITER;
+    const int64_t niters = ((int64_t)P.V + ITER - 1) / ITER;
     const int64_t tile_iters = (niters + kMaxTiles - 1) / kMaxTiles;
+    P.niters = (int32_t)niters;
     P.tile_iters = (int32_t)tile_iters;
     P.ntiles = (int32_t)((niters + tile_iters - 1) / tile_iters);
     hipLaunchKernelGGL((rs_row_kernel<In, VEC, UNR, MODE>), dim3((unsigned)nrows), dim3(kBlock), 0, s, P);
@@ -866,7 +978,7 @@ hipError_t launch_rows_m(const KParams& P, int dtype, bool vec, int64_t nrows, h
         return vec ? launch_rows_t<uint16_t, 8, 2, MODE>(P, nrows, s)
                    : launch_rows_t<uint16_t, 1, 4, MODE>(P, nrows, s);
     }
-    return vec ? launch_rows_t<float, 4, 4, MODE>(P, nrows, s)
+    return vec ? launch_rows_t<float, 4, 2, MODE>(P, nrows, s)
                : launch_rows_t<float, 1, 4, MODE>(P, nrows, s);
 }
 
@@ -884,9 +996,15 @@ KParams base_params(const void* t, const void* d, int64_t V, const rs_params* pr
     KParams P{};
     P.tgt = t;
     P.dft = d;
-    P.V = V;
+    P.V = (int32_t)V;
     P.T = prm->temperature;
-    P.c2 = (float)(1.4426950408889634 / (double)prm->temperature);
+    // c2 = c2h + c2l with c2h strictly below c2, so c2l > 0: then a -inf logit gives
+    // the exponent -inf (never -inf + inf) and contributes exactly zero.
+    const double c2 = 1.4426950408889634 / (double)prm->temperature;
+    float c2h = (float)c2;
+    if ((double)c2h >= c2) c2h = std::nextafter(c2h, 0.0f);
+    P.c2h = c2h;
+    P.c2l = (float)(c2 - (double)c2h);
     P.worep = prm->without_replacement ? 1 : 0;
     P.bonus = prm->bonus ? 1 : 0;
     return P;

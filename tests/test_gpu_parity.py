@@ -192,6 +192,31 @@ def test_tree_edges(gpu_lib):
     assert t.numel() == 0
 
 
+@pytest.mark.parametrize("cfg,over", [(2, dict(B=3, V=20000)), (4, dict(B=3, V=30000)),
+                                      (3, dict(B=2, V=30001))])
+def test_masked_logits(gpu_lib, cfg, over):
+    """Rows with -inf entries (masked vocabulary, as after top-k filtering) at every
+    temperature of the recipes; candidate tokens keep finite logits."""
+    w = synth.make_workload(cfg, device="cuda", **over)
+    g = torch.Generator(device="cuda").manual_seed(7)
+    for key in ("target", "draft"):
+        mask = torch.rand(w[key].shape, generator=g, device="cuda") < 0.3
+        B, N = w["node_token"].shape
+        keep = torch.zeros_like(mask)
+        for b in range(B):   # keep every candidate's own entries finite
+            par = w["parent"][b].cpu().numpy()
+            tok = w["node_token"][b].cpu().numpy()
+            for m in range(1, N):
+                keep[b, par[m], tok[m]] = True
+        w[key] = w[key].masked_fill(mask & ~keep, float("-inf"))
+    h = host_tree(w)
+    for mode in MODES:
+        gpu = gpu_tree(gpu_lib, w, mode, debug=True)
+        compare_walk(gpu, oracle_walk(h, w, mode))
+        compare_nodes(gpu, h, w, mode)
+        assert (gpu["status"].cpu().numpy() == 0).all()
+
+
 def test_max_children(gpu_lib):
     """A node with RS_MAX_CANDIDATES children, and one with one more (device status 7)."""
     for n_kids, expect_status in ((64, 0), (65, 7)):
