@@ -111,6 +111,8 @@ def main():
     ap.add_argument("--cpu-seconds", type=float, default=15.0)
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--no-other-mode", action="store_true")
+    ap.add_argument("--copy-probe", type=int, default=0, metavar="MIB",
+                    help="only run a plain device copy of MIB MiB (counter calibration)")
     args = ap.parse_args()
 
     world = int(os.environ.get("WORLD_SIZE", "1"))
@@ -125,6 +127,17 @@ def main():
     from paper_2608_24411_amd import native, synth
 
     torch.cuda.set_device(0)
+    if args.copy_probe:
+        # A plain copy of known size: FETCH_SIZE / WRITE_SIZE of this kernel divided by
+        # its bytes is the scale applied to the row kernel's counters.
+        n = args.copy_probe * (1 << 20) // 4
+        src = torch.ones(n, dtype=torch.float32, device="cuda")
+        dst = torch.empty_like(src)
+        for _ in range(max(1, args.steps)):
+            dst.copy_(src)
+        torch.cuda.synchronize()
+        print(json.dumps({"copy_probe_bytes_each_way": 4 * n, "launches": max(1, args.steps)}))
+        return
     w = synth.make_workload(args.config, device="cuda")
     B, N, V = w["B"], w["N"], w["V"]
     esz = 2 if w["target"].dtype == torch.bfloat16 else 4

@@ -20,8 +20,9 @@
 //            logits of token j through the chain of per-rejection scalars;
 //   draw     when every candidate is rejected (or the node is a leaf: bonus draw from
 //            p), the token is the smallest j whose running sum of the final residual in
-//            vocabulary order exceeds u * total.  The last pass records per-tile partial
-//            sums, so the draw re-reads a single tile.
+//            vocabulary order exceeds u * total.  The last pass records partial sums
+//            per slot (a run of 64 * 16 elements for bf16), so the draw re-reads one
+//            slot.
 //
 // Numerics: elements in fp32 (bf16 widened exactly), every sum accumulated in fp64,
 // the candidates' probabilities and the scalar chain in fp64.  Exponents are taken as
@@ -44,10 +45,28 @@
 
 namespace {
 
-constexpr int kBlock = 512;
+#ifndef RS_BLOCK
+#define RS_BLOCK 512
+#endif
+constexpr int kBlock = RS_BLOCK;
 constexpr int kWaves = kBlock / 64;
 constexpr int kMaxCand = RS_MAX_CANDIDATES;
-constexpr int kMaxTiles = 64;
+#ifndef RS_MAX_SLOTS
+#define RS_MAX_SLOTS 128
+#endif
+#ifndef RS_LANE_PARTIALS
+#define RS_LANE_PARTIALS 1
+#endif
+#ifndef RS_UNR16
+#define RS_UNR16 2
+#endif
+#ifndef RS_UNR32
+#define RS_UNR32 2
+#endif
+constexpr int kMaxSlots = RS_MAX_SLOTS;   // per-row slots (runs of chunks) with partial sums
+// A row's exponent reference is fixed before pass 1; sums outside [2^-kLow, inf) send the
+// row through an exact-maximum pass and a second pass 1.
+constexpr double kLowSum = 1.0 / 1048576.0;
 
 // ------------------------------------------------------------------ loads ----
 
@@ -126,16 +145,47 @@ __device__ __forceinline__ float expo(float l, float c2h, float c2l, float K) {
 
 // ------------------------------------------------------------- wave ops ----
 
+// Wave-wide reductions with DPP lane moves inside each 16-lane row (xor 1, xor 2,
+// half-row mirror, row mirror), then the four row results combined in a fixed order
+// from lanes 0, 16, 32, 48.  Every lane returns the same value.
+template <int CTRL>
+__device__ __forceinline__ int dpp_i(int v) {
+    return __builtin_amdgcn_update_dpp(0, v, CTRL, 0xF, 0xF, false);
+}
+template <int CTRL>
+__device__ __forceinline__ float dpp_f(float v) {
+    return __int_as_float(dpp_i<CTRL>(__float_as_int(v)));
+}
+template <int CTRL>
+__device__ __forceinline__ double dpp_d(double v) {
+    const int lo = dpp_i<CTRL>(__double2loint(v));
+    const int hi = dpp_i<CTRL>(__double2hiint(v));
+    return __hiloint2double(hi, lo);
+}
+constexpr int kDppXor1 = 0xB1, kDppXor2 = 0x4E, kDppHalfMirror = 0x141, kDppMirror = 0x140;
+
+__device__ __forceinline__ float readlane_f(float v, int l) {
+    return __int_as_float(__builtin_amdgcn_readlane(__float_as_int(v), l));
+}
+__device__ __forceinline__ double readlane_d(double v, int l) {
+    return __hiloint2double(__builtin_amdgcn_readlane(__double2hiint(v), l),
+                            __builtin_amdgcn_readlane(__double2loint(v), l));
+}
+
 __device__ __forceinline__ float wave_max(float v) {
-#pragma unroll
-    for (int o = 32; o > 0; o >>= 1) v = fmaxf(v, __shfl_xor(v, o, 64));
-    return v;
+    v = fmaxf(v, dpp_f<kDppXor1>(v));
+    v = fmaxf(v, dpp_f<kDppXor2>(v));
+    v = fmaxf(v, dpp_f<kDppHalfMirror>(v));
+    v = fmaxf(v, dpp_f<kDppMirror>(v));
+    return fmaxf(fmaxf(readlane_f(v, 0), readlane_f(v, 16)), fmaxf(readlane_f(v, 32), readlane_f(v, 48)));
 }
 
 __device__ __forceinline__ double wave_sum(double v) {
-#pragma unroll
-    for (int o = 32; o > 0; o >>= 1) v += __shfl_xor(v, o, 64);
-    return v;
+    v += dpp_d<kDppXor1>(v);
+    v += dpp_d<kDppXor2>(v);
+    v += dpp_d<kDppHalfMirror>(v);
+    v += dpp_d<kDppMirror>(v);
+    return (readlane_d(v, 0) + readlane_d(v, 16)) + (readlane_d(v, 32) + readlane_d(v, 48));
 }
 
 __device__ __forceinline__ double wave_incl_scan(double v, int lane) {
@@ -151,11 +201,13 @@ __device__ __forceinline__ double wave_incl_scan(double v, int lane) {
 
 struct Smem {
     int32_t status;
-    int32_t nc;
     int32_t decision;     // -1 continue, >= 0 accepted candidate, -2 fault
+    int32_t next_slot;    // slot counter of the running sweep
+    int32_t nc;           // rows with more nodes than threads only
     float ur;
-    float Kt, Kd;         // exponent offsets -max * c2 of target / draft
     double St, Sd;        // sums of exp2(l c2 + K)
+    int32_t wcount[kWaves];
+    int32_t wbad[kWaves];
     int32_t cand_tok[kMaxCand];
     int32_t cand_node[kMaxCand];
     float cand_u[kMaxCand];
@@ -165,27 +217,25 @@ struct Smem {
     double cand_q[kMaxCand];
     // rejection steps, in test order; fp32 copies are in target-mass units
     int32_t st_x[kMaxCand + 1];
-    int32_t st_iter[kMaxCand + 1];  // loop iteration that holds token x
     float st_c[kMaxCand + 1];       // ResiSpec: Z * dscale * St/Sd.  Standard: dscale * St/Sd
     float st_a[kMaxCand + 1];       // ResiSpec: a
     float st_i[kMaxCand + 1];       // ResiSpec: 1/Z.  Standard: 1/S
     double st_zd[kMaxCand + 1], st_ad[kMaxCand + 1], st_id[kMaxCand + 1];
     double st_ds[kMaxCand + 1];     // draft scale (without replacement)
-    // per-tile partials written by one wave each
-    double tpA[kMaxTiles][kWaves];
-    double tpB[kMaxTiles][kWaves];
-    float tpK[kMaxTiles][kWaves];
-    double tileT[kMaxTiles];
-    // cross-wave reductions
-    float redm[2][kWaves];
-    float redk[2][kWaves];
-    double reds[2][kWaves];
-    double scan_w[kWaves];
-    int32_t first_w[kWaves + 1];
+    uint32_t hit_slots[kMaxSlots / 32];  // slots that hold a rejected token
+    // per-lane partials of every slot of the running pass ([lane][slot], padded so a
+    // wave's 64 stores hit 64 distinct banks), reduced after the pass in a fixed order
+#if RS_LANE_PARTIALS
+    float partA[64][kMaxSlots + 1];
+    float partB[64][kMaxSlots + 1];
+#endif
+    double slotA[kMaxSlots];
+    double slotB[kMaxSlots];
+    double slotT[kMaxSlots];
+    float wmax[2][kWaves];
     // draw
-    int32_t ksel;
-    double base, thr, total;
     int32_t token;
+    double total;
 };
 
 struct KParams {
@@ -213,13 +263,32 @@ struct KParams {
     float T;
     float c2h, c2l;      // log2(e) / T = c2h + c2l
     int32_t worep, bonus, flat;
-    int32_t niters;      // loop iterations per pass
-    int32_t tile_iters;  // loop iterations per tile
-    int32_t ntiles;
+    int32_t G;           // chunks per slot
+    int32_t nslots;      // slots per row
 };
 
+#ifdef RS_TIMING
+// Phase timestamps (s_memrealtime, 100 MHz) per row, for profiling builds only.
+__device__ long long* g_timing = nullptr;
+#define RS_STAMP(row, k)                                                               \
+    do {                                                                               \
+        if (threadIdx.x == 0 && g_timing) g_timing[(row) * 16 + (k)] = wall_clock64(); \
+    } while (0)
+#else
+#define RS_STAMP(row, k) \
+    do {                 \
+    } while (0)
+#endif
+
+// Exponent reference for a maximum m: an integer-valued float near -m * c2, so that
+// moving between references rescales sums by an exact power of two (ldexp).
 __device__ __forceinline__ float kref(float m, float c2h) {
-    return m > -FLT_MAX ? -(m * c2h) : 0.0f;
+    return m > -FLT_MAX ? -ceilf(m * c2h) : 0.0f;
+}
+
+// acc * 2^(to - from) for integer-valued references
+__device__ __forceinline__ double rescale(double acc, float to, float from) {
+    return ldexp(acc, (int)(to - from));
 }
 
 __device__ __forceinline__ void write_outcome(const KParams& P, int64_t row, int32_t child,
@@ -242,13 +311,12 @@ __device__ void zero_residual_row(const KParams& P, int64_t row) {
     for (int j = threadIdx.x; j < P.V; j += kBlock) out[j] = 0.0f;
 }
 
-// Rejection-step terms of one element, given its target mass R (target units) and
-// unnormalised draft mass Q.  The chain over the earlier steps 0..i-1 first.
+// Rejection-step terms of one element (exact token comparisons), given its target
+// mass R (target units) and unnormalised draft mass Q; the chain over the earlier
+// steps 0..i-1 first.
 //   standard: A = max(R - c_i Q, 0)                    (c_i = dscale_i St/Sd)
 //   ResiSpec: A = min(c_i Q, R), B = R, both 0 at x_i   (c_i = Z_i dscale_i St/Sd)
-// CHECK = false skips the token comparisons (no rejected token in this element's
-// loop iteration); the standard update needs none: R < D at every rejected token.
-template <int MODE, bool CHECK>
+template <int MODE>
 __device__ __forceinline__ void chain_terms(float R, float Q, int j, const Smem& sm, int i,
                                             float& A, float& Bv) {
     for (int t = 0; t < i; ++t) {
@@ -258,7 +326,7 @@ __device__ __forceinline__ void chain_terms(float R, float Q, int j, const Smem&
         } else {
             const float m = fminf(c * Q, R);
             R = fmaf(sm.st_a[t], R - m, m) * sm.st_i[t];
-            if (CHECK && j == sm.st_x[t]) R = 0.0f;
+            if (j == sm.st_x[t]) R = 0.0f;
         }
     }
     const float c = sm.st_c[i];
@@ -266,7 +334,7 @@ __device__ __forceinline__ void chain_terms(float R, float Q, int j, const Smem&
         A = fmaxf(fmaf(-c, Q, R), 0.0f);
         Bv = 0.0f;
     } else {
-        const bool x0 = CHECK && j == sm.st_x[i];
+        const bool x0 = j == sm.st_x[i];
         A = x0 ? 0.0f : fminf(c * Q, R);
         Bv = x0 ? 0.0f : R;
     }
@@ -298,35 +366,62 @@ __device__ double scalar_residual(const Smem& sm, int i, double p, double q, int
     return R;
 }
 
-// One sweep over the row with register prefetch of the next iteration.  body(t, d,
-// idx0, it) gets the UNR x VEC unpacked elements of iteration `it`; element (u, e)
-// has index idx0 + u * kBlock * VEC + e.  flush(tile) runs after the last iteration
-// of a tile.
-template <typename In, int VEC, int UNR, bool PAIR, typename Body, typename Flush>
-__device__ __forceinline__ void sweep(const In* __restrict__ tg, const In* __restrict__ dg,
-                                      int V, int niters, int ti, bool reverse, Body&& body,
-                                      Flush&& flush) {
+// One pass over the row.  The row is cut into chunks of 64 * VEC * UNR elements (one
+// 128-bit load per lane and UNR) and runs of G chunks form slots.  Waves take slots
+// from a shared counter, so the eight waves of the block finish within about one chunk
+// of each other; a wave's first slot is its own index, so its first loads can be
+// issued before the counter is set.  The next chunk is loaded while the current one is
+// processed.  body(t, d, idx0, slot) gets the unpacked elements of a chunk (element
+// (u, e) has index idx0 + u * 64 * VEC + e); flush(slot) runs after a slot's last
+// chunk.  reverse: slots in descending order, chunks descending inside a slot.
+template <typename In, int VEC, int UNR, bool PAIR, bool PRE, typename Body, typename Flush>
+__device__ __forceinline__ void wave_sweep(const In* __restrict__ tg, const In* __restrict__ dg,
+                                           int V, int G, int nslots, bool reverse,
+                                           const typename Vec<In, VEC>::raw (&pre)[UNR],
+                                           int* counter, Body&& body, Flush&& flush) {
     using W = Vec<In, VEC>;
     using raw = typename W::raw;
-    constexpr int ITER = kBlock * VEC * UNR;
-    const int lane0 = threadIdx.x * VEC;
+    constexpr int CHUNK = 64 * VEC * UNR;
+    const int lane = threadIdx.x & 63;
+    const int wid = threadIdx.x >> 6;
+    const int lane0 = lane * VEC;
+    auto chunk_base = [&](int slot, int j) -> int {
+        return (slot * G + (reverse ? G - 1 - j : j)) * CHUNK + lane0;
+    };
+    int slot = wid < nslots ? (reverse ? nslots - 1 - wid : wid) : -1;
+    if (slot < 0) return;
+    // the counter is read one slot ahead, so its latency overlaps a chunk's work
+    auto take = [&]() -> int {
+        int v = 0;
+        if (lane == 0) v = atomicAdd(counter, 1);
+        v = __builtin_amdgcn_readfirstlane(v);
+        return v < nslots ? (reverse ? nslots - 1 - v : v) : -1;
+    };
+    int ahead = take();
     raw ct[UNR], cd[UNR];
-    int it = reverse ? niters - 1 : 0;
+    {
+        const int base = chunk_base(slot, 0);
 #pragma unroll
-    for (int u = 0; u < UNR; ++u) {
-        ct[u] = W::load(tg, it * ITER + u * kBlock * VEC + lane0, V);
-        if (PAIR) cd[u] = W::load(dg, it * ITER + u * kBlock * VEC + lane0, V);
+        for (int u = 0; u < UNR; ++u) {
+            ct[u] = PRE ? pre[u] : W::load(tg, base + u * 64 * VEC, V);
+            if (PAIR) cd[u] = W::load(dg, base + u * 64 * VEC, V);
+        }
     }
-    int tile = it / ti;
-    int edge = reverse ? tile * ti : min((tile + 1) * ti, niters) - 1;
-    for (int k = 0; k < niters; ++k) {
-        const int nit = reverse ? it - 1 : it + 1;
+    int j = 0;
+    for (;;) {
+        int nslot = slot, nj = j + 1;
+        if (nj == G) {
+            nslot = ahead;
+            nj = 0;
+            if (nslot >= 0) ahead = take();
+        }
         raw nt[UNR], nd[UNR];
-        if (k + 1 < niters) {
+        if (nslot >= 0) {
+            const int base = chunk_base(nslot, nj);
 #pragma unroll
             for (int u = 0; u < UNR; ++u) {
-                nt[u] = W::load(tg, nit * ITER + u * kBlock * VEC + lane0, V);
-                if (PAIR) nd[u] = W::load(dg, nit * ITER + u * kBlock * VEC + lane0, V);
+                nt[u] = W::load(tg, base + u * 64 * VEC, V);
+                if (PAIR) nd[u] = W::load(dg, base + u * 64 * VEC, V);
             }
         }
         float t[UNR][VEC], d[UNR][VEC];
@@ -335,18 +430,16 @@ __device__ __forceinline__ void sweep(const In* __restrict__ tg, const In* __res
             W::unpack(ct[u], t[u]);
             if (PAIR) W::unpack(cd[u], d[u]);
         }
-        body(t, d, it * ITER + lane0, it);
-        if (it == edge) {
-            flush(tile);
-            tile += reverse ? -1 : 1;
-            edge = reverse ? tile * ti : min((tile + 1) * ti, niters) - 1;
-        }
+        body(t, d, chunk_base(slot, j), slot);
+        if (j == G - 1) flush(slot);
+        if (nslot < 0) break;
+        slot = nslot;
+        j = nj;
 #pragma unroll
         for (int u = 0; u < UNR; ++u) {
             ct[u] = nt[u];
             if (PAIR) cd[u] = nd[u];
         }
-        it = nit;
     }
 }
 
@@ -359,7 +452,8 @@ __global__ void __launch_bounds__(kBlock) rs_row_kernel(const KParams P) {
     const int lane = tid & 63;
     const int wid = tid >> 6;
     const int V = P.V;
-    constexpr int ITER = kBlock * VEC * UNR;
+    constexpr int CHUNK = 64 * VEC * UNR;
+    const int G = P.G, nslots = P.nslots;
 
     int64_t row;
     int32_t b, n;
@@ -378,29 +472,85 @@ __global__ void __launch_bounds__(kBlock) rs_row_kernel(const KParams P) {
     const In* __restrict__ tg = reinterpret_cast<const In*>(P.tgt) + row * V;
     const In* __restrict__ dg = reinterpret_cast<const In*>(P.dft) + row * V;
 
-    // ---- row description: candidates, their uniforms and logits, structural checks
+    RS_STAMP(row, 0);
+    using W = Vec<In, VEC>;
+    // This wave's first target chunk is requested before anything else, so its latency
+    // overlaps the row description below (the first slot of wave w is slot w).
+    typename W::raw pre[UNR];
+#pragma unroll
+    for (int u = 0; u < UNR; ++u) pre[u] = W::load(tg, wid * G * CHUNK + lane * VEC + u * 64 * VEC, V);
+
+    // ---- row description.  "Holder" threads own one candidate each: node, token and
+    // uniform now; the two logits of its token are gathered while pass 1 streams and
+    // written to shared memory after it.
     if (tid == 0) {
-        sm.status = RS_SEQ_OK;
-        sm.nc = 0;
         sm.decision = -1;
+        sm.next_slot = kWaves;
+        sm.ur = P.flat ? P.ur_flat[row] : P.ur[row];
     }
-    __syncthreads();
+    for (int w = tid; w < kMaxSlots / 32; w += kBlock) sm.hit_slots[w] = 0u;
+    // maxima of the chunks just requested: they fix the row's exponent reference
+    auto publish_premax = [&]() {
+        float mx = -FLT_MAX;
+#pragma unroll
+        for (int u = 0; u < UNR; ++u) {
+            float v[VEC];
+            W::unpack(pre[u], v);
+#pragma unroll
+            for (int e = 0; e < VEC; ++e) mx = fmaxf(mx, v[e]);
+        }
+        mx = wave_max(mx);
+        if (lane == 0) sm.wmax[0][wid] = mx;
+    };
+    bool holder = false;
+    int32_t hx = 0, hnode = 0, hrank = 0;
+    float hu = 0.0f;
+    int nc = 0;
+    int status = RS_SEQ_OK;
     if (P.flat) {
-        if (tid < P.k) {
-            const int32_t x = P.cand_ids[row * P.k + tid];
-            sm.cand_tok[tid] = x;
-            sm.cand_u[tid] = P.ua_flat[row * P.k + tid];
-            sm.cand_node[tid] = tid;
-            const bool ok = x >= 0 && x < V;
-            sm.cand_lt[tid] = ok ? widen(tg[x]) : 0.0f;
-            sm.cand_ld[tid] = ok ? widen(dg[x]) : 0.0f;
+        holder = tid < P.k;
+        if (holder) {
+            hx = P.cand_ids[row * P.k + tid];
+            hu = P.ua_flat[row * P.k + tid];
+            hnode = tid;
+            hrank = tid;
         }
-        if (tid == 0) {
-            sm.nc = P.k;
-            sm.ur = P.ur_flat[row];
-        }
+        nc = P.k;
+        publish_premax();
         __syncthreads();
+    } else if (P.N <= kBlock) {
+        const int64_t sb = (int64_t)b * P.N;
+        int bad = 0;
+        if (tid < P.N) {
+            const int32_t pm = P.parent[sb + tid];
+            hx = P.node_token[sb + tid];
+            hu = P.ua[sb + tid];
+            hnode = tid;
+            bad = (tid == 0) ? (pm != -1) : (pm < 0 || pm >= tid);
+            holder = tid > n && pm == n;
+        }
+        const uint64_t cm = __ballot(holder);
+        const uint64_t bm = __ballot(bad);
+        hrank = __popcll(cm & __lanemask_lt());
+        if (lane == 0) {
+            sm.wcount[wid] = __popcll(cm);
+            sm.wbad[wid] = bm != 0;
+        }
+        publish_premax();
+        __syncthreads();
+        int anybad = 0;
+        for (int w = 0; w < kWaves; ++w) {
+            const int c = sm.wcount[w];
+            nc += c;
+            hrank += (w < wid) ? c : 0;
+            anybad |= sm.wbad[w];
+        }
+        if (anybad) status = RS_SEQ_BAD_TREE;
+        else if (nc > kMaxCand) status = RS_SEQ_TOO_MANY_CHILDREN;
     } else {
+        // more nodes than threads: describe the row directly in shared memory
+        if (tid == 0) sm.status = RS_SEQ_OK;
+        publish_premax();
         const int32_t* par = P.parent + (int64_t)b * P.N;
         int bad = 0;
         for (int m = tid; m < P.N; m += kBlock) {
@@ -430,16 +580,16 @@ __global__ void __launch_bounds__(kBlock) rs_row_kernel(const KParams P) {
             }
             if (lane == 0) {
                 sm.nc = count;
-                sm.ur = P.ur[row];
                 if (bad) sm.status = RS_SEQ_BAD_TREE;
                 else if (count > kMaxCand) sm.status = RS_SEQ_TOO_MANY_CHILDREN;
             }
         }
         __syncthreads();
+        nc = sm.nc;
+        status = sm.status;
     }
-    const int nc = sm.nc;
-    if (sm.status != RS_SEQ_OK) {
-        if (tid == 0) write_outcome(P, row, -1, -1, sm.status);
+    if (status != RS_SEQ_OK) {
+        if (tid == 0) write_outcome(P, row, -1, -1, status);
         zero_residual_row(P, row);
         return;
     }
@@ -448,140 +598,156 @@ __global__ void __launch_bounds__(kBlock) rs_row_kernel(const KParams P) {
         zero_residual_row(P, row);
         return;
     }
+    if (tid == 0) sm.status = RS_SEQ_OK;
+    // candidate logits: requested now, consumed after pass 1
+    float hlt = 0.0f, hld = 0.0f;
+    if (holder && hrank < kMaxCand && hx >= 0 && hx < V) {
+        hlt = widen(tg[hx]);
+        hld = widen(dg[hx]);
+    }
 
+    RS_STAMP(row, 1);
     const bool internal = nc > 0;
     const float c2h = P.c2h, c2l = P.c2l;
-    const int niters = P.niters, ti = P.tile_iters;
 
-    // ---- pass 1: softmax statistics (per-lane running max; sums rescaled exactly
-    // when the reference K = -max * c2 moves)
+    // ---- pass 1: softmax statistics.  Both rows are summed against one exponent
+    // reference K, fixed from the maxima of the first chunks, so element values do not
+    // depend on which wave read which chunk; per-lane partials of every slot go to shared
+    // memory and are reduced in a fixed order.  A row whose sums overflow, or come out
+    // below kLowSum, takes an exact-maximum pass and is summed again.
+    float Kt, Kd;
     {
-        float mt = -FLT_MAX, kt = 0.0f, md = -FLT_MAX, kd = 0.0f;
-        double st = 0.0, sd = 0.0;
-        float stile = 0.0f;   // leaf rows: this tile's share of st (reference kt)
-        auto flush = [&](int tile) {
-            if (internal) return;
-            const float mw = wave_max(mt);
-            const float kw = kref(mw, c2h);
-            const double sw = wave_sum(stile > 0.0f ? (double)stile * exp2((double)kw - (double)kt) : 0.0);
+        float m0 = -FLT_MAX;
+        for (int w = 0; w < kWaves; ++w) m0 = fmaxf(m0, sm.wmax[0][w]);
+        Kt = Kd = kref(m0, c2h);
+    }
+    for (int attempt = 0;; ++attempt) {
+        float fa = 0.0f, fc = 0.0f;   // this slot's lane partials
+        auto flush = [&](int slot) {
+#if RS_LANE_PARTIALS
+            sm.partA[lane][slot] = fa;
+            if (internal) sm.partB[lane][slot] = fc;
+#else
+            const double a = wave_sum((double)fa);
+            const double c = internal ? wave_sum((double)fc) : 0.0;
             if (lane == 0) {
-                sm.tpK[tile][wid] = kw;
-                sm.tpA[tile][wid] = sw;
+                sm.slotA[slot] = a;
+                sm.slotB[slot] = c;
             }
-            stile = 0.0f;
+#endif
+            fa = fc = 0.0f;
         };
         if (internal) {
-            sweep<In, VEC, UNR, true>(tg, dg, V, niters, ti, false,
+            wave_sweep<In, VEC, UNR, true, true>(tg, dg, V, G, nslots, false, pre, &sm.next_slot,
                 [&](const float (&t)[UNR][VEC], const float (&d)[UNR][VEC], int, int) {
-                    float mx = -FLT_MAX, my = -FLT_MAX;
+#pragma unroll
+                    for (int u = 0; u < UNR; ++u)
+#pragma unroll
+                        for (int e = 0; e < VEC; ++e) {
+                            fa += exp2_fast(expo(t[u][e], c2h, c2l, Kt));
+                            fc += exp2_fast(expo(d[u][e], c2h, c2l, Kd));
+                        }
+                },
+                flush);
+        } else {
+            wave_sweep<In, VEC, UNR, false, true>(tg, dg, V, G, nslots, false, pre, &sm.next_slot,
+                [&](const float (&t)[UNR][VEC], const float (&)[UNR][VEC], int, int) {
+#pragma unroll
+                    for (int u = 0; u < UNR; ++u)
+#pragma unroll
+                        for (int e = 0; e < VEC; ++e) fa += exp2_fast(expo(t[u][e], c2h, c2l, Kt));
+                },
+                flush);
+        }
+        if (attempt == 0) {
+            RS_STAMP(row, 2);
+#ifdef RS_TIMING
+            if (lane == 0 && g_timing) g_timing[row * 16 + 8 + wid] = wall_clock64();   // per-wave end
+#endif
+            if (holder && hrank < kMaxCand) {
+                sm.cand_tok[hrank] = hx;
+                sm.cand_u[hrank] = hu;
+                sm.cand_node[hrank] = hnode;
+                sm.cand_lt[hrank] = hlt;
+                sm.cand_ld[hrank] = hld;
+            }
+        }
+        __syncthreads();
+#if RS_LANE_PARTIALS
+        if (tid < nslots) {
+            double a = 0.0, c = 0.0;
+#pragma unroll 8
+            for (int l = 0; l < 64; ++l) a += (double)sm.partA[l][tid];
+            if (internal) {
+#pragma unroll 8
+                for (int l = 0; l < 64; ++l) c += (double)sm.partB[l][tid];
+            }
+            sm.slotA[tid] = a;
+            sm.slotB[tid] = c;
+        }
+        __syncthreads();
+#endif
+        if (wid == 0) {
+            double a0 = 0.0, a1 = 0.0;
+            for (int s2 = lane; s2 < nslots; s2 += 64) {
+                a0 += sm.slotA[s2];
+                a1 += sm.slotB[s2];
+            }
+            const double s0 = wave_sum(a0);
+            const double s1 = wave_sum(a1);
+            const bool ok = s0 >= kLowSum && s0 < INFINITY && (!internal || (s1 >= kLowSum && s1 < INFINITY));
+            if (lane == 0) {
+                sm.St = s0;
+                sm.Sd = s1;
+                sm.st_ds[0] = 1.0;
+                sm.decision = ok ? -1 : -3;   // -3: sum again with exact maxima
+                sm.next_slot = kWaves;
+            }
+        }
+        __syncthreads();
+        if (sm.decision != -3) break;
+        if (attempt == 1) {
+            if (tid == 0) write_outcome(P, row, -1, -1, RS_SEQ_UNDERFLOW);
+            zero_residual_row(P, row);
+            return;
+        }
+        // exact maxima of both rows, then the references are taken from them
+        {
+            float mx = -FLT_MAX, my = -FLT_MAX;
+            wave_sweep<In, VEC, UNR, true, false>(tg, dg, V, G, nslots, false, pre, &sm.next_slot,
+                [&](const float (&t)[UNR][VEC], const float (&d)[UNR][VEC], int, int) {
 #pragma unroll
                     for (int u = 0; u < UNR; ++u)
 #pragma unroll
                         for (int e = 0; e < VEC; ++e) {
                             mx = fmaxf(mx, t[u][e]);
-                            my = fmaxf(my, d[u][e]);
+                            my = internal ? fmaxf(my, d[u][e]) : my;
                         }
-                    if (mx > mt) {
-                        const float nk = -(mx * c2h);
-                        st *= exp2((double)nk - (double)kt);
-                        mt = mx;
-                        kt = nk;
-                    }
-                    if (my > md) {
-                        const float nk = -(my * c2h);
-                        sd *= exp2((double)nk - (double)kd);
-                        md = my;
-                        kd = nk;
-                    }
-                    float a = 0.0f, c = 0.0f;
-#pragma unroll
-                    for (int u = 0; u < UNR; ++u)
-#pragma unroll
-                        for (int e = 0; e < VEC; ++e) {
-                            a += exp2_fast(expo(t[u][e], c2h, c2l, kt));
-                            c += exp2_fast(expo(d[u][e], c2h, c2l, kd));
-                        }
-                    st += (double)a;
-                    sd += (double)c;
                 },
-                flush);
-        } else {
-            sweep<In, VEC, UNR, false>(tg, dg, V, niters, ti, false,
-                [&](const float (&t)[UNR][VEC], const float (&)[UNR][VEC], int, int) {
-                    float mx = -FLT_MAX;
-#pragma unroll
-                    for (int u = 0; u < UNR; ++u)
-#pragma unroll
-                        for (int e = 0; e < VEC; ++e) mx = fmaxf(mx, t[u][e]);
-                    if (mx > mt) {
-                        const float nk = -(mx * c2h);
-                        const double f = exp2((double)nk - (double)kt);
-                        st *= f;
-                        stile = (float)(stile * f);
-                        mt = mx;
-                        kt = nk;
-                    }
-                    float a = 0.0f;
-#pragma unroll
-                    for (int u = 0; u < UNR; ++u)
-#pragma unroll
-                        for (int e = 0; e < VEC; ++e) a += exp2_fast(expo(t[u][e], c2h, c2l, kt));
-                    st += (double)a;
-                    stile += a;
-                },
-                flush);
-        }
-        // combine lanes, then waves (wave 0)
-        {
-            const float mw = wave_max(mt);
-            const float kw = kref(mw, c2h);
-            const double sw = wave_sum(st > 0.0 ? st * exp2((double)kw - (double)kt) : 0.0);
-            float mw2 = -FLT_MAX, kw2 = 0.0f;
-            double sw2 = 0.0;
-            if (internal) {
-                mw2 = wave_max(md);
-                kw2 = kref(mw2, c2h);
-                sw2 = wave_sum(sd > 0.0 ? sd * exp2((double)kw2 - (double)kd) : 0.0);
-            }
+                [](int) {});
+            mx = wave_max(mx);
+            my = wave_max(my);
             if (lane == 0) {
-                sm.redm[0][wid] = mw;
-                sm.redk[0][wid] = kw;
-                sm.reds[0][wid] = sw;
-                sm.redm[1][wid] = mw2;
-                sm.redk[1][wid] = kw2;
-                sm.reds[1][wid] = sw2;
+                sm.wmax[0][wid] = mx;
+                sm.wmax[1][wid] = my;
             }
-        }
-        __syncthreads();
-        if (wid == 0) {
-            const bool in = lane < kWaves;
-            const int w = in ? lane : 0;
-            const float m0 = wave_max(in ? sm.redm[0][w] : -FLT_MAX);
-            const float m1 = wave_max(in ? sm.redm[1][w] : -FLT_MAX);
-            const float k0 = kref(m0, c2h), k1 = kref(m1, c2h);
-            const double s0 = wave_sum(in && sm.reds[0][w] > 0.0
-                                           ? sm.reds[0][w] * exp2((double)k0 - (double)sm.redk[0][w]) : 0.0);
-            const double s1 = wave_sum(in && sm.reds[1][w] > 0.0
-                                           ? sm.reds[1][w] * exp2((double)k1 - (double)sm.redk[1][w]) : 0.0);
-            if (lane == 0) {
-                sm.Kt = k0;
-                sm.Kd = k1;
-                sm.St = s0;
-                sm.Sd = s1;
-                if (!(s0 > 0.0) || (internal && !(s1 > 0.0))) sm.status = RS_SEQ_UNDERFLOW;
-                sm.st_ds[0] = 1.0;
+            __syncthreads();
+            float m0 = -FLT_MAX, m1 = -FLT_MAX;
+            for (int w = 0; w < kWaves; ++w) {
+                m0 = fmaxf(m0, sm.wmax[0][w]);
+                m1 = fmaxf(m1, sm.wmax[1][w]);
             }
-        }
-        __syncthreads();
-        if (sm.status != RS_SEQ_OK) {
-            if (tid == 0) write_outcome(P, row, -1, -1, sm.status);
-            zero_residual_row(P, row);
-            return;
+            Kt = kref(m0, c2h);
+            Kd = kref(m1, c2h);
+            if (tid == 0) {
+                sm.decision = -1;
+                sm.next_slot = kWaves;
+            }
+            __syncthreads();
         }
     }
 
     const double c2d = (double)c2h + (double)c2l;
-    const float Kt = sm.Kt, Kd = sm.Kd;
     const double St = sm.St, Sd = sm.Sd;
     // draft mass in target units: q St / Sd, folded into the step constants
     const double q2t = internal ? St / Sd : 0.0;
@@ -600,6 +766,7 @@ __global__ void __launch_bounds__(kBlock) rs_row_kernel(const KParams P) {
     __syncthreads();
 
     const bool worep = P.worep != 0;
+    RS_STAMP(row, 3);
 
     // ---- sequential accept / reject
     int i = 0;
@@ -625,9 +792,11 @@ __global__ void __launch_bounds__(kBlock) rs_row_kernel(const KParams P) {
                 } else {
                     const double z = Dx - Rx;   // ResiSpec budget
                     sm.st_x[i] = x;
-                    sm.st_iter[i] = x / ITER;
+                    const int hs = (x / CHUNK) / G;
+                    sm.hit_slots[hs >> 5] |= 1u << (hs & 31);
                     sm.st_zd[i] = z;
                     sm.st_c[i] = (float)((MODE == RS_MODE_SPECINFER ? 1.0 : z) * sm.st_ds[i] * q2t);
+                    sm.next_slot = kWaves;
                 }
             }
             sm.decision = dec;
@@ -635,69 +804,120 @@ __global__ void __launch_bounds__(kBlock) rs_row_kernel(const KParams P) {
         __syncthreads();
         if (sm.decision != -1) break;
 
-        // rejection pass: sums of step i with per-tile partials
+        // rejection pass: sums of step i with per-slot partials
         {
-            double accA = 0.0, accB = 0.0;   // this tile's lane partials
-            auto flush = [&](int tile) {
-                const double wa = wave_sum(accA);
-                const double wb = (MODE == RS_MODE_RESISPEC) ? wave_sum(accB) : 0.0;
-                if (lane == 0) {
-                    sm.tpA[tile][wid] = wa;
-                    sm.tpB[tile][wid] = wb;
-                }
-                accA = accB = 0.0;
-            };
+            float accA = 0.0f, accB = 0.0f;   // this slot's lane partials
             const bool reverse = (i & 1) == 0;   // re-read the most recently fetched end first
             const int ii = i;
-            sweep<In, VEC, UNR, true>(tg, dg, V, niters, ti, reverse,
-                [&](const float (&t)[UNR][VEC], const float (&d)[UNR][VEC], int idx0, int it) {
+            const float ci = sm.st_c[i];
+            const int xi = sm.st_x[i];
+            wave_sweep<In, VEC, UNR, true, false>(tg, dg, V, G, nslots, reverse, pre, &sm.next_slot,
+                [&](const float (&t)[UNR][VEC], const float (&d)[UNR][VEC], int idx0, int slot) {
+                    // does this slot hold a rejected token? (uniform)
                     bool hit = false;
                     if (MODE == RS_MODE_RESISPEC) {
-                        for (int s = 0; s <= ii; ++s) hit |= (sm.st_iter[s] == it);
+                        const uint32_t w = __builtin_amdgcn_readfirstlane(sm.hit_slots[slot >> 5]);
+                        hit = (w >> (slot & 31)) & 1u;
+                    }
+                    float R[UNR][VEC], Q[UNR][VEC];
+#pragma unroll
+                    for (int u = 0; u < UNR; ++u)
+#pragma unroll
+                        for (int e = 0; e < VEC; ++e) {
+                            R[u][e] = exp2_fast(expo(t[u][e], c2h, c2l, Kt));
+                            Q[u][e] = exp2_fast(expo(d[u][e], c2h, c2l, Kd));
+                        }
+                    for (int s2 = 0; s2 < ii; ++s2) {
+                        const float c = sm.st_c[s2], inv = sm.st_i[s2];
+                        if (MODE == RS_MODE_SPECINFER) {
+#pragma unroll
+                            for (int u = 0; u < UNR; ++u)
+#pragma unroll
+                                for (int e = 0; e < VEC; ++e)
+                                    R[u][e] = fmaxf(fmaf(-c, Q[u][e], R[u][e]), 0.0f) * inv;
+                        } else {
+                            const float a = sm.st_a[s2];
+#pragma unroll
+                            for (int u = 0; u < UNR; ++u)
+#pragma unroll
+                                for (int e = 0; e < VEC; ++e) {
+                                    const float m = fminf(c * Q[u][e], R[u][e]);
+                                    R[u][e] = fmaf(a, R[u][e] - m, m) * inv;
+                                }
+                            if (hit) {
+                                const int x = sm.st_x[s2];
+#pragma unroll
+                                for (int u = 0; u < UNR; ++u)
+#pragma unroll
+                                    for (int e = 0; e < VEC; ++e)
+                                        if (idx0 + u * 64 * VEC + e == x) R[u][e] = 0.0f;
+                            }
+                        }
                     }
                     float fa = 0.0f, fb = 0.0f;
-                    if (!hit) {
+                    if (MODE == RS_MODE_SPECINFER) {
 #pragma unroll
                         for (int u = 0; u < UNR; ++u)
 #pragma unroll
-                            for (int e = 0; e < VEC; ++e) {
-                                const float R = exp2_fast(expo(t[u][e], c2h, c2l, Kt));
-                                const float Q = exp2_fast(expo(d[u][e], c2h, c2l, Kd));
-                                float A, Bv;
-                                chain_terms<MODE, false>(R, Q, 0, sm, ii, A, Bv);
-                                fa += A;
-                                fb += Bv;
-                            }
+                            for (int e = 0; e < VEC; ++e) fa += fmaxf(fmaf(-ci, Q[u][e], R[u][e]), 0.0f);
                     } else {
+                        if (hit) {
+#pragma unroll
+                            for (int u = 0; u < UNR; ++u)
+#pragma unroll
+                                for (int e = 0; e < VEC; ++e)
+                                    if (idx0 + u * 64 * VEC + e == xi) R[u][e] = 0.0f;
+                        }
 #pragma unroll
                         for (int u = 0; u < UNR; ++u)
 #pragma unroll
                             for (int e = 0; e < VEC; ++e) {
-                                const float R = exp2_fast(expo(t[u][e], c2h, c2l, Kt));
-                                const float Q = exp2_fast(expo(d[u][e], c2h, c2l, Kd));
-                                float A, Bv;
-                                chain_terms<MODE, true>(R, Q, idx0 + u * kBlock * VEC + e, sm, ii, A, Bv);
-                                fa += A;
-                                fb += Bv;
+                                fa += fminf(ci * Q[u][e], R[u][e]);
+                                fb += R[u][e];
                             }
                     }
-                    accA += (double)fa;
-                    accB += (double)fb;
+                    accA += fa;
+                    accB += fb;
                 },
-                flush);
+                [&](int slot) {
+#if RS_LANE_PARTIALS
+                    sm.partA[lane][slot] = accA;
+                    if (MODE == RS_MODE_RESISPEC) sm.partB[lane][slot] = accB;
+#else
+                    const double wa = wave_sum((double)accA);
+                    const double wb = (MODE == RS_MODE_RESISPEC) ? wave_sum((double)accB) : 0.0;
+                    if (lane == 0) {
+                        sm.slotA[slot] = wa;
+                        sm.slotB[slot] = wb;
+                    }
+#endif
+                    accA = accB = 0.0f;
+                });
         }
         __syncthreads();
-        if (wid == 0) {
-            double A = 0.0, Bv = 0.0;
-            if (lane < P.ntiles) {
-                for (int w = 0; w < kWaves; ++w) {
-                    A += sm.tpA[lane][w];
-                    Bv += sm.tpB[lane][w];
-                }
+#if RS_LANE_PARTIALS
+        if (tid < nslots) {
+            double a = 0.0, c = 0.0;
+#pragma unroll 8
+            for (int l = 0; l < 64; ++l) a += (double)sm.partA[l][tid];
+            if (MODE == RS_MODE_RESISPEC) {
+#pragma unroll 8
+                for (int l = 0; l < 64; ++l) c += (double)sm.partB[l][tid];
             }
-            // lane 0's sums, so that every lane derives identical constants
-            const double totA = __shfl(wave_sum(A), 0, 64) / St;   // normalised units
-            const double totB = __shfl(wave_sum(Bv), 0, 64) / St;
+            sm.slotA[tid] = a;
+            sm.slotB[tid] = c;
+        }
+        __syncthreads();
+#endif
+        if (wid == 0) {
+            // per-lane sums over slots lane, lane+64, ... in a fixed order
+            double A = 0.0, Bv = 0.0;
+            for (int s2 = lane; s2 < nslots; s2 += 64) {
+                A += sm.slotA[s2];
+                Bv += sm.slotB[s2];
+            }
+            const double totA = wave_sum(A) / St;   // normalised units
+            const double totB = wave_sum(Bv) / St;
             const double z = sm.st_zd[i];
             double a = 0.0, inv;
             if (MODE == RS_MODE_SPECINFER) {
@@ -708,10 +928,10 @@ __global__ void __launch_bounds__(kBlock) rs_row_kernel(const KParams P) {
                 a = (C > 0.0) ? delta / C : 0.0;
                 inv = 1.0 / z;
             }
-            if (lane < P.ntiles) {
-                // tile totals of the unnormalised next residual (linear in the partials)
-                sm.tileT[lane] = (MODE == RS_MODE_SPECINFER) ? A : (1.0 - a) * A + a * Bv;
-            }
+            // slot totals of the unnormalised next residual (linear in the partials)
+            for (int s2 = lane; s2 < nslots; s2 += 64)
+                sm.slotT[s2] = (MODE == RS_MODE_SPECINFER) ? sm.slotA[s2]
+                                                            : (1.0 - a) * sm.slotA[s2] + a * sm.slotB[s2];
             if (lane == 0) {
                 if (MODE == RS_MODE_SPECINFER && !(totA > 0.0)) {
                     sm.status = RS_SEQ_UNDERFLOW;
@@ -733,6 +953,10 @@ __global__ void __launch_bounds__(kBlock) rs_row_kernel(const KParams P) {
         if (sm.decision == -2) break;
     }
 
+    RS_STAMP(row, 4);
+#ifdef RS_TIMING
+    if (threadIdx.x == 0 && g_timing) g_timing[row * 16 + 7] = i;   // rejection passes
+#endif
     if (sm.decision == -2) {
         if (tid == 0) write_outcome(P, row, -1, -1, sm.status);
         zero_residual_row(P, row);
@@ -747,7 +971,7 @@ __global__ void __launch_bounds__(kBlock) rs_row_kernel(const KParams P) {
         return;
     }
 
-    // ---- every candidate rejected, or no candidates: inverse-CDF draw
+    // ---- every candidate rejected, or no candidates: inverse-CDF draw (wave 0)
     const float u = sm.ur;
     if (!(u >= 0.0f && u < 1.0f)) {
         if (tid == 0) write_outcome(P, row, -1, -1, RS_SEQ_BAD_UNIFORM);
@@ -755,133 +979,166 @@ __global__ void __launch_bounds__(kBlock) rs_row_kernel(const KParams P) {
         return;
     }
     const int last = nc - 1;   // index of the last rejection step (internal rows)
-    if (wid == 0) {
-        double T = 0.0;
-        if (lane < P.ntiles) {
-            if (internal) {
-                T = sm.tileT[lane];
-            } else {
-                for (int w = 0; w < kWaves; ++w) {
-                    const double s = sm.tpA[lane][w];
-                    if (s > 0.0) T += s * exp2((double)Kt - (double)sm.tpK[lane][w]);
-                }
-            }
-        }
-        const double cum = wave_incl_scan(T, lane);
-        const double total = __shfl(cum, 63, 64);
-        const double thr = (double)u * total;
-        const uint64_t hit = __ballot(lane < P.ntiles && cum > thr);
-        int k = hit ? (__ffsll((unsigned long long)hit) - 1) : -1;
-        if (k < 0) {   // rounding guard: last tile with mass
-            const uint64_t pos = __ballot(lane < P.ntiles && T > 0.0);
-            k = pos ? 63 - __clzll((long long)pos) : 0;
-        }
-        const double excl = cum - T;
-        const double base = __shfl(excl, k, 64);
-        if (lane == 0) {
-            sm.ksel = k;
-            sm.base = base;
-            sm.thr = thr;
-            sm.total = total;
-            if (!(total > 0.0)) sm.status = RS_SEQ_UNDERFLOW;
-        }
-    }
-    __syncthreads();
-    if (sm.status != RS_SEQ_OK) {
-        if (tid == 0) write_outcome(P, row, -1, -1, sm.status);
-        zero_residual_row(P, row);
-        return;
-    }
-
-    // element values of the final distribution (unnormalised, target units)
     const float a_last = (internal && MODE == RS_MODE_RESISPEC) ? sm.st_a[last] : 0.0f;
+    // element values of the final distribution (unnormalised, target units)
     auto final_value = [&](float lt, float ld, int j) -> float {
         const float R = exp2_fast(expo(lt, c2h, c2l, Kt));
         if (!internal) return R;
         const float Q = exp2_fast(expo(ld, c2h, c2l, Kd));
         float A, Bv;
-        chain_terms<MODE, true>(R, Q, j, sm, last, A, Bv);
+        chain_terms<MODE>(R, Q, j, sm, last, A, Bv);
         if (MODE == RS_MODE_SPECINFER) return A;
         return fmaf(a_last, Bv - A, A);
     };
-
-    const int tile_elems = ti * ITER;
-    const int CH = tile_elems / kBlock;           // contiguous elements per thread
-    const int t0 = sm.ksel * tile_elems + tid * CH;
-    double own = 0.0;
-    for (int c = 0; c < CH; c += VEC) {
-        float tv[VEC], dv[VEC];
-        load_vec<In, VEC>(tg, t0 + c, V, tv);
-        if (internal) load_vec<In, VEC>(dg, t0 + c, V, dv);
+    if (wid == 0) {
+        // slot totals in vocabulary order; lane l holds slots 4l .. 4l+3
+        double Ts[4];
+        double own = 0.0;
 #pragma unroll
-        for (int e = 0; e < VEC; ++e) {
-            const int j = t0 + c + e;
-            if (j < V) own += (double)final_value(tv[e], internal ? dv[e] : 0.0f, j);
+        for (int q = 0; q < 4; ++q) {
+            const int s2 = 4 * lane + q;
+            double T = 0.0;
+            if (s2 < nslots) T = internal ? sm.slotT[s2] : sm.slotA[s2];
+            Ts[q] = T;
+            own += T;
         }
-    }
-    // block exclusive scan of `own`
-    const double incl = wave_incl_scan(own, lane);
-    if (lane == 63) sm.scan_w[wid] = incl;
-    __syncthreads();
-    double wbase = 0.0;
-    for (int w = 0; w < wid; ++w) wbase += sm.scan_w[w];
-    const double excl = wbase + incl - own;
-    const double thr = sm.thr;
-    const double tbase = sm.base;
-    const bool cond = (own > 0.0) && (tbase + excl + own > thr);
-    const uint64_t cmask = __ballot(cond);
-    if (lane == 0) sm.first_w[wid] = cmask ? wid * 64 + (__ffsll((unsigned long long)cmask) - 1) : kBlock;
-    __syncthreads();
-    if (tid == 0) {
-        int first = kBlock;
-        for (int w = 0; w < kWaves; ++w) first = min(first, sm.first_w[w]);
-        sm.first_w[0] = first;
-        sm.token = -1;
-    }
-    __syncthreads();
-    int chosen = sm.first_w[0];
-    bool fallback = false;
-    if (chosen == kBlock) {   // rounding guard: last thread of the tile with mass
-        const uint64_t pm = __ballot(own > 0.0);
-        if (lane == 0) sm.first_w[1 + wid] = pm ? wid * 64 + (63 - __clzll((long long)pm)) : -1;
-        __syncthreads();
-        if (tid == 0) {
-            int lastt = -1;
-            for (int w = 0; w < kWaves; ++w) lastt = max(lastt, sm.first_w[1 + w]);
-            sm.first_w[0] = lastt;
+        const double incl = wave_incl_scan(own, lane);
+        const double total = readlane_d(incl, 63);
+        const double thr = (double)u * total;
+        const double excl = incl - own;
+        uint64_t hit = __ballot(own > 0.0 && incl > thr);
+        int L = hit ? (__ffsll((unsigned long long)hit) - 1) : -1;
+        if (L < 0) {   // rounding guard: last lane with mass
+            const uint64_t pos = __ballot(own > 0.0);
+            L = pos ? 63 - __clzll((long long)pos) : 0;
         }
-        __syncthreads();
-        chosen = sm.first_w[0];
-        fallback = true;
-    }
-    if (tid == chosen) {
-        double acc = tbase + excl;
-        int tok = -1, lastpos = -1;
-        for (int c = 0; c < CH && tok < 0; c += VEC) {
-            float tv[VEC], dv[VEC];
-            load_vec<In, VEC>(tg, t0 + c, V, tv);
-            if (internal) load_vec<In, VEC>(dg, t0 + c, V, dv);
-            for (int e = 0; e < VEC; ++e) {
-                const int j = t0 + c + e;
-                if (j >= V) break;
-                const float v = final_value(tv[e], internal ? dv[e] : 0.0f, j);
-                if (v > 0.0f) lastpos = j;
-                acc += (double)v;
-                if (!fallback && v > 0.0f && acc > thr) {
-                    tok = j;
-                    break;
+        int ks = -1;
+        double base = 0.0;
+        if (lane == L) {
+            double c = excl;
+            int lastpos = -1;
+            double lastbase = 0.0;
+#pragma unroll
+            for (int q = 0; q < 4; ++q) {
+                if (Ts[q] > 0.0) {
+                    if (ks < 0 && c + Ts[q] > thr) {
+                        ks = 4 * lane + q;
+                        base = c;
+                    }
+                    lastpos = 4 * lane + q;
+                    lastbase = c;
+                }
+                c += Ts[q];
+            }
+            if (ks < 0) {
+                ks = lastpos;
+                base = lastbase;
+            }
+        }
+        ks = __builtin_amdgcn_readlane(ks, L);
+        base = readlane_d(base, L);
+        if (ks < 0) {   // no mass anywhere (degenerate): no draw
+            if (lane == 0) {
+                sm.token = -1;
+                sm.total = total;
+                sm.status = RS_SEQ_UNDERFLOW;
+            }
+        } else {
+        // the slot's elements: lane l takes a contiguous run of R = G * VEC * UNR
+        const int R = G * VEC * UNR;
+        const int t0 = ks * G * CHUNK + lane * R;
+        constexpr int kRegRun = 32;
+        float vals[kRegRun];
+        double own2 = 0.0;
+        const bool inreg = R <= kRegRun;
+        if (inreg) {
+#pragma unroll
+            for (int c = 0; c < kRegRun; c += VEC) {
+                float tv[VEC], dv[VEC];
+                if (c < R) {
+                    load_vec<In, VEC>(tg, t0 + c, V, tv);
+                    if (internal) load_vec<In, VEC>(dg, t0 + c, V, dv);
+                }
+#pragma unroll
+                for (int e = 0; e < VEC; ++e) {
+                    const int j = t0 + c + e;
+                    const float v = (c < R && j < V) ? final_value(tv[e], internal ? dv[e] : 0.0f, j) : 0.0f;
+                    vals[c + e] = v;
+                    own2 += (double)v;
+                }
+            }
+        } else {
+            for (int c = 0; c < R; c += VEC) {
+                float tv[VEC], dv[VEC];
+                load_vec<In, VEC>(tg, t0 + c, V, tv);
+                if (internal) load_vec<In, VEC>(dg, t0 + c, V, dv);
+#pragma unroll
+                for (int e = 0; e < VEC; ++e) {
+                    const int j = t0 + c + e;
+                    if (j < V) own2 += (double)final_value(tv[e], internal ? dv[e] : 0.0f, j);
                 }
             }
         }
-        if (tok < 0) tok = lastpos;
-        sm.token = tok;
+        const double incl2 = wave_incl_scan(own2, lane);
+        const double excl2 = incl2 - own2;
+        const uint64_t hit2 = __ballot(own2 > 0.0 && base + incl2 > thr);
+        int L2 = hit2 ? (__ffsll((unsigned long long)hit2) - 1) : -1;
+        const bool fallback = L2 < 0;
+        if (fallback) {   // rounding guard: last lane of the slot with mass
+            const uint64_t pos = __ballot(own2 > 0.0);
+            L2 = pos ? 63 - __clzll((long long)pos) : -1;
+        }
+        if (lane == L2) {
+            double acc = base + excl2;
+            int tok = -1, lastpos = -1;
+            if (inreg) {
+#pragma unroll
+                for (int c = 0; c < kRegRun; ++c) {
+                    const float v = vals[c];
+                    const int j = t0 + c;
+                    if (tok < 0 && c < R && j < V) {
+                        if (v > 0.0f) lastpos = j;
+                        acc += (double)v;
+                        if (!fallback && v > 0.0f && acc > thr) tok = j;
+                    }
+                }
+            } else {
+                for (int c = 0; c < R && tok < 0; c += VEC) {
+                    float tv[VEC], dv[VEC];
+                    load_vec<In, VEC>(tg, t0 + c, V, tv);
+                    if (internal) load_vec<In, VEC>(dg, t0 + c, V, dv);
+                    for (int e = 0; e < VEC; ++e) {
+                        const int j = t0 + c + e;
+                        if (j >= V) break;
+                        const float v = final_value(tv[e], internal ? dv[e] : 0.0f, j);
+                        if (v > 0.0f) lastpos = j;
+                        acc += (double)v;
+                        if (!fallback && v > 0.0f && acc > thr) {
+                            tok = j;
+                            break;
+                        }
+                    }
+                }
+            }
+            if (tok < 0) tok = lastpos;
+            sm.token = tok;
+        }
+        if (lane == 0) {
+            if (L2 < 0) sm.token = -1;
+            sm.total = total;
+            if (!(total > 0.0)) sm.status = RS_SEQ_UNDERFLOW;
+        }
+        }
     }
     __syncthreads();
+    RS_STAMP(row, 5);
     const int32_t tok = sm.token;
     if (tid == 0) {
-        if (tok < 0) write_outcome(P, row, -1, -1, RS_SEQ_UNDERFLOW);
+        if (sm.status != RS_SEQ_OK) write_outcome(P, row, -1, -1, sm.status);
+        else if (tok < 0) write_outcome(P, row, -1, -1, RS_SEQ_UNDERFLOW);
         else write_outcome(P, row, -1, tok, RS_SEQ_OK);
     }
+    RS_STAMP(row, 6);
 
     // debug: the normalised distribution of the draw
     if (P.residual_out) {
@@ -962,12 +1219,11 @@ rs_status check_params(const rs_params* prm) {
 
 template <typename In, int VEC, int UNR, int MODE>
 hipError_t launch_rows_t(KParams P, int64_t nrows, hipStream_t s) {
-    constexpr int64_t ITER = (int64_t)kBlock * VEC * UNR;
-    const int64_t niters = ((int64_t)P.V + ITER - 1) / ITER;
-    const int64_t tile_iters = (niters + kMaxTiles - 1) / kMaxTiles;
-    P.niters = (int32_t)niters;
-    P.tile_iters = (int32_t)tile_iters;
-    P.ntiles = (int32_t)((niters + tile_iters - 1) / tile_iters);
+    constexpr int64_t CHUNK = 64 * VEC * UNR;
+    const int64_t nch = ((int64_t)P.V + CHUNK - 1) / CHUNK;
+    const int64_t G = (nch + kMaxSlots - 1) / kMaxSlots;
+    P.G = (int32_t)G;
+    P.nslots = (int32_t)((nch + G - 1) / G);
     hipLaunchKernelGGL((rs_row_kernel<In, VEC, UNR, MODE>), dim3((unsigned)nrows), dim3(kBlock), 0, s, P);
     return hipGetLastError();
 }
@@ -975,10 +1231,10 @@ hipError_t launch_rows_t(KParams P, int64_t nrows, hipStream_t s) {
 template <int MODE>
 hipError_t launch_rows_m(const KParams& P, int dtype, bool vec, int64_t nrows, hipStream_t s) {
     if (dtype == RS_BF16) {
-        return vec ? launch_rows_t<uint16_t, 8, 2, MODE>(P, nrows, s)
+        return vec ? launch_rows_t<uint16_t, 8, RS_UNR16, MODE>(P, nrows, s)
                    : launch_rows_t<uint16_t, 1, 4, MODE>(P, nrows, s);
     }
-    return vec ? launch_rows_t<float, 4, 2, MODE>(P, nrows, s)
+    return vec ? launch_rows_t<float, 4, RS_UNR32, MODE>(P, nrows, s)
                : launch_rows_t<float, 1, 4, MODE>(P, nrows, s);
 }
 
@@ -1083,6 +1339,12 @@ rs_status check_tree_args(const void* target_logits, const void* draft_logits,
 }  // namespace
 
 extern "C" {
+
+#ifdef RS_TIMING
+int32_t resispec_debug_set_timing(void* dev_ptr) {
+    return hipMemcpyToSymbol(HIP_SYMBOL(g_timing), &dev_ptr, sizeof(dev_ptr)) == hipSuccess ? 0 : 1;
+}
+#endif
 
 int32_t resispec_abi_version(void) { return RESISPEC_ABI_VERSION; }
 

@@ -217,6 +217,28 @@ def test_masked_logits(gpu_lib, cfg, over):
         assert (gpu["status"].cpu().numpy() == 0).all()
 
 
+def test_reference_fallback(gpu_lib):
+    """Rows whose exponent reference (taken from the first chunks) does not fit: a +200
+    logit placed late in target rows (the sums overflow), and draft rows shifted by -60
+    (their sums underflow; a constant shift leaves the softmax unchanged).  Both take the
+    exact-maximum path and must still agree with the oracle."""
+    w = synth.make_workload(2, device="cuda", B=3, V=40000)
+    w["target"][:, 3, 39990] = 200.0
+    w["target"][1, 0, 39000] = 150.0
+    h = host_tree(w)
+    for mode in MODES:
+        gpu = gpu_tree(gpu_lib, w, mode, debug=True)
+        compare_walk(gpu, oracle_walk(h, w, mode))
+        compare_nodes(gpu, h, w, mode)
+    ws = dict(w)
+    ws["draft"] = (w["draft"].float() - 60.0).to(w["draft"].dtype)
+    hs = host_tree(ws)
+    for mode in MODES:
+        a = gpu_tree(gpu_lib, ws, mode, debug=True)
+        compare_walk(a, oracle_walk(hs, ws, mode))
+        compare_nodes(a, hs, ws, mode)
+
+
 def test_max_children(gpu_lib):
     """A node with RS_MAX_CANDIDATES children, and one with one more (device status 7)."""
     for n_kids, expect_status in ((64, 0), (65, 7)):
