@@ -89,6 +89,9 @@ struct Vec<float, 4> {
         if (idx < V) return *reinterpret_cast<const uint4*>(row + idx);
         return make_uint4(0xff800000u, 0xff800000u, 0xff800000u, 0xff800000u);
     }
+    static __device__ __forceinline__ raw load_full(const float* __restrict__ row, int idx) {
+        return *reinterpret_cast<const uint4*>(row + idx);
+    }
     static __device__ __forceinline__ void unpack(const raw& r, float (&v)[4]) {
         v[0] = __uint_as_float(r.x); v[1] = __uint_as_float(r.y);
         v[2] = __uint_as_float(r.z); v[3] = __uint_as_float(r.w);
@@ -101,6 +104,9 @@ struct Vec<uint16_t, 8> {
     static __device__ __forceinline__ raw load(const uint16_t* __restrict__ row, int idx, int V) {
         if (idx < V) return *reinterpret_cast<const uint4*>(row + idx);
         return make_uint4(0xff80ff80u, 0xff80ff80u, 0xff80ff80u, 0xff80ff80u);
+    }
+    static __device__ __forceinline__ raw load_full(const uint16_t* __restrict__ row, int idx) {
+        return *reinterpret_cast<const uint4*>(row + idx);
     }
     static __device__ __forceinline__ void unpack(const raw& r, float (&v)[8]) {
         v[0] = bf16_lo(r.x); v[1] = bf16_hi(r.x);
@@ -116,6 +122,9 @@ struct Vec<float, 1> {
     static __device__ __forceinline__ raw load(const float* __restrict__ row, int idx, int V) {
         return idx < V ? __float_as_uint(row[idx]) : 0xff800000u;
     }
+    static __device__ __forceinline__ raw load_full(const float* __restrict__ row, int idx) {
+        return __float_as_uint(row[idx]);
+    }
     static __device__ __forceinline__ void unpack(const raw& r, float (&v)[1]) { v[0] = __uint_as_float(r); }
 };
 
@@ -124,6 +133,9 @@ struct Vec<uint16_t, 1> {
     using raw = uint32_t;
     static __device__ __forceinline__ raw load(const uint16_t* __restrict__ row, int idx, int V) {
         return idx < V ? ((uint32_t)row[idx]) << 16 : 0xff800000u;
+    }
+    static __device__ __forceinline__ raw load_full(const uint16_t* __restrict__ row, int idx) {
+        return ((uint32_t)row[idx]) << 16;
     }
     static __device__ __forceinline__ void unpack(const raw& r, float (&v)[1]) { v[0] = __uint_as_float(r); }
 };
@@ -217,11 +229,22 @@ struct Smem {
     double cand_q[kMaxCand];
     // rejection steps, in test order; fp32 copies are in target-mass units
     int32_t st_x[kMaxCand + 1];
-    float st_c[kMaxCand + 1];       // ResiSpec: Z * dscale * St/Sd.  Standard: dscale * St/Sd
+    float st_c[kMaxCand + 1];       // ResiSpec: Z * dscale * St/Sd.  Standard: C * St/Sd
     float st_a[kMaxCand + 1];       // ResiSpec: a
-    float st_i[kMaxCand + 1];       // ResiSpec: 1/Z.  Standard: 1/S
-    double st_zd[kMaxCand + 1], st_ad[kMaxCand + 1], st_id[kMaxCand + 1];
+    float st_i[kMaxCand + 1];       // ResiSpec: 1/Z
+    double st_zd[kMaxCand + 1], st_ad[kMaxCand + 1];
     double st_ds[kMaxCand + 1];     // draft scale (without replacement)
+    double st_rx[kMaxCand + 1];     // R(x_i) of the tested candidate (normalised)
+    // standard residual after i + 1 rejections, collapsed:
+    //   R = max(p - C_i q, 0) / Tot_i,  C_i = C_{i-1} + Tot_{i-1} dscale_i
+    double st_C[kMaxCand + 1], st_tot[kMaxCand + 1];
+    // ResiSpec, first rejection: min(c Q, R) = 2^f0 exp2(min(aR - f0, aQ + e)) with
+    // log2 c = e + f0; kq0 = Kd + e (integer valued)
+    float st_f0, st_kq0;
+    double st_2f0;                  // 2^f0 (as v_exp_f32 gives it)
+    double rx0e;                    // the fp32 element value of R at x_0 (target units)
+    int32_t sx0;                    // slot holding x_0
+    double slotP[kMaxSlots];        // pass-1 slot totals of the target row
     uint32_t hit_slots[kMaxSlots / 32];  // slots that hold a rejected token
     // per-lane partials of every slot of the running pass ([lane][slot], padded so a
     // wave's 64 stores hit 64 distinct banks), reduced after the pass in a fixed order
@@ -312,57 +335,56 @@ __device__ void zero_residual_row(const KParams& P, int64_t row) {
 }
 
 // Rejection-step terms of one element (exact token comparisons), given its target
-// mass R (target units) and unnormalised draft mass Q; the chain over the earlier
-// steps 0..i-1 first.
-//   standard: A = max(R - c_i Q, 0)                    (c_i = dscale_i St/Sd)
-//   ResiSpec: A = min(c_i Q, R), B = R, both 0 at x_i   (c_i = Z_i dscale_i St/Sd)
+// mass R (target units) and unnormalised draft mass Q:
+//   standard: A = max(R - C_i Q, 0)          (the collapsed recurrence, C_i = st_c[i])
+//   ResiSpec: A = min(c_i Q, R), B = R, both 0 at x_i   (c_i = Z_i dscale_i St/Sd),
+//             after the chain over the earlier steps 0..i-1.
 template <int MODE>
 __device__ __forceinline__ void chain_terms(float R, float Q, int j, const Smem& sm, int i,
                                             float& A, float& Bv) {
-    for (int t = 0; t < i; ++t) {
-        const float c = sm.st_c[t];
-        if (MODE == RS_MODE_SPECINFER) {
-            R = fmaxf(fmaf(-c, Q, R), 0.0f) * sm.st_i[t];
-        } else {
-            const float m = fminf(c * Q, R);
-            R = fmaf(sm.st_a[t], R - m, m) * sm.st_i[t];
-            if (j == sm.st_x[t]) R = 0.0f;
-        }
-    }
-    const float c = sm.st_c[i];
     if (MODE == RS_MODE_SPECINFER) {
-        A = fmaxf(fmaf(-c, Q, R), 0.0f);
+        A = fmaxf(fmaf(-sm.st_c[i], Q, R), 0.0f);
         Bv = 0.0f;
-    } else {
-        const bool x0 = j == sm.st_x[i];
-        A = x0 ? 0.0f : fminf(c * Q, R);
-        Bv = x0 ? 0.0f : R;
+        return;
     }
+    for (int t = 0; t < i; ++t) {
+        const float m = fminf(sm.st_c[t] * Q, R);
+        R = fmaf(sm.st_a[t], R - m, m) * sm.st_i[t];
+        if (j == sm.st_x[t]) R = 0.0f;
+    }
+    const bool x0 = j == sm.st_x[i];
+    A = x0 ? 0.0f : fminf(sm.st_c[i] * Q, R);
+    Bv = x0 ? 0.0f : R;
 }
 
 // Scalar chain for the accept test of candidate i (fp64, normalised units).
 template <int MODE>
 __device__ double scalar_residual(const Smem& sm, int i, double p, double q, int32_t x,
                                   bool worep, double& Dout) {
-    double R = p;
     bool removed = false;
+    if (worep)
+        for (int t = 0; t < i; ++t) removed |= x == sm.st_x[t];
+    Dout = removed ? 0.0 : q * sm.st_ds[i];
+    if (MODE == RS_MODE_SPECINFER) {
+        // the standard recurrence max(R - D, 0) / S applied i times equals
+        // max(p - C q, 0) / Tot (every factor is positive)
+        if (i == 0) return p;
+        const double w = p - sm.st_C[i - 1] * q;
+        return w > 0.0 ? w / sm.st_tot[i - 1] : 0.0;
+    }
+    double R = p;
+    removed = false;
     for (int t = 0; t < i; ++t) {
         const double Dt = removed ? 0.0 : q * sm.st_ds[t];
-        if (MODE == RS_MODE_SPECINFER) {
-            const double w = R - Dt;
-            R = (w > 0.0 ? w : 0.0) * sm.st_id[t];
+        if (x == sm.st_x[t]) {
+            R = 0.0;
         } else {
-            if (x == sm.st_x[t]) {
-                R = 0.0;
-            } else {
-                const double zd = sm.st_zd[t] * Dt;
-                const double m = zd < R ? zd : R;
-                R = ((1.0 - sm.st_ad[t]) * m + sm.st_ad[t] * R) / sm.st_zd[t];
-            }
+            const double zd = sm.st_zd[t] * Dt;
+            const double m = zd < R ? zd : R;
+            R = ((1.0 - sm.st_ad[t]) * m + sm.st_ad[t] * R) / sm.st_zd[t];
         }
         if (worep && x == sm.st_x[t]) removed = true;
     }
-    Dout = removed ? 0.0 : q * sm.st_ds[i];
     return R;
 }
 
@@ -370,10 +392,12 @@ __device__ double scalar_residual(const Smem& sm, int i, double p, double q, int
 // 128-bit load per lane and UNR) and runs of G chunks form slots.  Waves take slots
 // from a shared counter, so the eight waves of the block finish within about one chunk
 // of each other; a wave's first slot is its own index, so its first loads can be
-// issued before the counter is set.  The next chunk is loaded while the current one is
-// processed.  body(t, d, idx0, slot) gets the unpacked elements of a chunk (element
-// (u, e) has index idx0 + u * 64 * VEC + e); flush(slot) runs after a slot's last
-// chunk.  reverse: slots in descending order, chunks descending inside a slot.
+// issued before the counter is set.  Two register sets alternate: the next chunk is
+// loaded into one while the other is processed.  Chunks wholly below V are loaded
+// without per-lane bounds checks.  body(t, d, idx0, slot) gets the unpacked elements
+// of a chunk (element (u, e) has index idx0 + u * 64 * VEC + e); flush(slot) runs
+// after a slot's last chunk.  reverse: slots in descending order, chunks descending
+// inside a slot.
 template <typename In, int VEC, int UNR, bool PAIR, bool PRE, typename Body, typename Flush>
 __device__ __forceinline__ void wave_sweep(const In* __restrict__ tg, const In* __restrict__ dg,
                                            int V, int G, int nslots, bool reverse,
@@ -385,8 +409,9 @@ __device__ __forceinline__ void wave_sweep(const In* __restrict__ tg, const In* 
     const int lane = threadIdx.x & 63;
     const int wid = threadIdx.x >> 6;
     const int lane0 = lane * VEC;
-    auto chunk_base = [&](int slot, int j) -> int {
-        return (slot * G + (reverse ? G - 1 - j : j)) * CHUNK + lane0;
+    // first element of chunk j of a slot (the same for every lane)
+    auto chunk_start = [&](int slot, int j) -> int {
+        return (slot * G + (reverse ? G - 1 - j : j)) * CHUNK;
     };
     int slot = wid < nslots ? (reverse ? nslots - 1 - wid : wid) : -1;
     if (slot < 0) return;
@@ -398,55 +423,71 @@ __device__ __forceinline__ void wave_sweep(const In* __restrict__ tg, const In* 
         return v < nslots ? (reverse ? nslots - 1 - v : v) : -1;
     };
     int ahead = take();
-    raw ct[UNR], cd[UNR];
-    {
-        const int base = chunk_base(slot, 0);
-#pragma unroll
-        for (int u = 0; u < UNR; ++u) {
-            ct[u] = PRE ? pre[u] : W::load(tg, base + u * 64 * VEC, V);
-            if (PAIR) cd[u] = W::load(dg, base + u * 64 * VEC, V);
+    auto advance = [&](int& s, int& j) {
+        if (++j == G) {
+            s = ahead;
+            j = 0;
+            if (s >= 0) ahead = take();
         }
-    }
-    int j = 0;
-    for (;;) {
-        int nslot = slot, nj = j + 1;
-        if (nj == G) {
-            nslot = ahead;
-            nj = 0;
-            if (nslot >= 0) ahead = take();
-        }
-        raw nt[UNR], nd[UNR];
-        if (nslot >= 0) {
-            const int base = chunk_base(nslot, nj);
+    };
+    auto load = [&](int s, int j, raw (&t)[UNR], raw (&d)[UNR]) {
+        const int c0 = chunk_start(s, j);
+        if (c0 + CHUNK <= V) {
 #pragma unroll
             for (int u = 0; u < UNR; ++u) {
-                nt[u] = W::load(tg, base + u * 64 * VEC, V);
-                if (PAIR) nd[u] = W::load(dg, base + u * 64 * VEC, V);
+                t[u] = W::load_full(tg, c0 + lane0 + u * 64 * VEC);
+                if (PAIR) d[u] = W::load_full(dg, c0 + lane0 + u * 64 * VEC);
+            }
+        } else {
+#pragma unroll
+            for (int u = 0; u < UNR; ++u) {
+                t[u] = W::load(tg, c0 + lane0 + u * 64 * VEC, V);
+                if (PAIR) d[u] = W::load(dg, c0 + lane0 + u * 64 * VEC, V);
             }
         }
+    };
+    auto process = [&](const raw (&ct)[UNR], const raw (&cd)[UNR], int s, int j) {
         float t[UNR][VEC], d[UNR][VEC];
 #pragma unroll
         for (int u = 0; u < UNR; ++u) {
             W::unpack(ct[u], t[u]);
             if (PAIR) W::unpack(cd[u], d[u]);
         }
-        body(t, d, chunk_base(slot, j), slot);
-        if (j == G - 1) flush(slot);
-        if (nslot < 0) break;
-        slot = nslot;
-        j = nj;
+        body(t, d, chunk_start(s, j) + lane0, s);
+        if (j == G - 1) flush(s);
+    };
+    raw at[UNR], ad[UNR], bt[UNR], bd[UNR];
+    int sa = slot, ja = 0;
+    if (PRE) {
 #pragma unroll
-        for (int u = 0; u < UNR; ++u) {
-            ct[u] = nt[u];
-            if (PAIR) cd[u] = nd[u];
+        for (int u = 0; u < UNR; ++u) at[u] = pre[u];
+        if (PAIR) {
+            const int c0 = chunk_start(sa, 0);
+#pragma unroll
+            for (int u = 0; u < UNR; ++u) ad[u] = W::load(dg, c0 + lane0 + u * 64 * VEC, V);
         }
+    } else {
+        load(sa, ja, at, ad);
+    }
+    for (;;) {
+        int sb = sa, jb = ja;
+        advance(sb, jb);
+        if (sb >= 0) load(sb, jb, bt, bd);
+        process(at, ad, sa, ja);
+        if (sb < 0) break;
+        sa = sb;
+        ja = jb;
+        advance(sa, ja);
+        if (sa >= 0) load(sa, ja, at, ad);
+        process(bt, bd, sb, jb);
+        if (sa < 0) break;
     }
 }
 
 // ------------------------------------------------------------ row kernel ----
 
 template <typename In, int VEC, int UNR, int MODE>
-__global__ void __launch_bounds__(kBlock) rs_row_kernel(const KParams P) {
+__global__ void __launch_bounds__(kBlock) __attribute__((amdgpu_waves_per_eu(4))) rs_row_kernel(const KParams P) {
     __shared__ Smem sm;
     const int tid = threadIdx.x;
     const int lane = tid & 63;
@@ -633,6 +674,7 @@ __global__ void __launch_bounds__(kBlock) rs_row_kernel(const KParams P) {
             if (lane == 0) {
                 sm.slotA[slot] = a;
                 sm.slotB[slot] = c;
+                sm.slotP[slot] = a;
             }
 #endif
             fa = fc = 0.0f;
@@ -684,6 +726,7 @@ __global__ void __launch_bounds__(kBlock) rs_row_kernel(const KParams P) {
             }
             sm.slotA[tid] = a;
             sm.slotB[tid] = c;
+            sm.slotP[tid] = a;
         }
         __syncthreads();
 #endif
@@ -792,10 +835,31 @@ __global__ void __launch_bounds__(kBlock) rs_row_kernel(const KParams P) {
                 } else {
                     const double z = Dx - Rx;   // ResiSpec budget
                     sm.st_x[i] = x;
+                    sm.st_rx[i] = Rx;
                     const int hs = (x / CHUNK) / G;
                     sm.hit_slots[hs >> 5] |= 1u << (hs & 31);
                     sm.st_zd[i] = z;
-                    sm.st_c[i] = (float)((MODE == RS_MODE_SPECINFER ? 1.0 : z) * sm.st_ds[i] * q2t);
+                    if (MODE == RS_MODE_SPECINFER) {
+                        const double C = (i == 0) ? sm.st_ds[0]
+                                                  : sm.st_C[i - 1] + sm.st_tot[i - 1] * sm.st_ds[i];
+                        sm.st_C[i] = C;
+                        sm.st_c[i] = (float)(C * q2t);
+                    } else {
+                        const double c = z * sm.st_ds[i] * q2t;
+                        sm.st_c[i] = (float)c;
+                        if (i == 0) {
+                            // c = m 2^e exactly, m in [0.5, 1); log2 m in fp32.  The split
+                            // only has to reproduce c to fp32 accuracy, like st_c itself.
+                            int e;
+                            const double m = frexp(c, &e);
+                            const float f0 = __builtin_amdgcn_logf((float)m);
+                            sm.st_f0 = f0;
+                            sm.st_kq0 = Kd + (float)e;
+                            sm.st_2f0 = (double)exp2_fast(f0);
+                            sm.rx0e = (double)exp2_fast(expo(sm.cand_lt[0], c2h, c2l, Kt));
+                            sm.sx0 = hs;
+                        }
+                    }
                     sm.next_slot = kWaves;
                 }
             }
@@ -811,32 +875,85 @@ __global__ void __launch_bounds__(kBlock) rs_row_kernel(const KParams P) {
             const int ii = i;
             const float ci = sm.st_c[i];
             const int xi = sm.st_x[i];
-            wave_sweep<In, VEC, UNR, true, false>(tg, dg, V, G, nslots, reverse, pre, &sm.next_slot,
-                [&](const float (&t)[UNR][VEC], const float (&d)[UNR][VEC], int idx0, int slot) {
-                    // does this slot hold a rejected token? (uniform)
-                    bool hit = false;
-                    if (MODE == RS_MODE_RESISPEC) {
-                        const uint32_t w = __builtin_amdgcn_readfirstlane(sm.hit_slots[slot >> 5]);
-                        hit = (w >> (slot & 31)) & 1u;
-                    }
-                    float R[UNR][VEC], Q[UNR][VEC];
+            // ResiSpec needs the per-slot sums of R only after the first rejection
+            const bool wantB = MODE == RS_MODE_RESISPEC && ii > 0;
+            auto flush = [&](int slot) {
+#if RS_LANE_PARTIALS
+                sm.partA[lane][slot] = accA;
+                if (wantB) sm.partB[lane][slot] = accB;
+#else
+                const double wa = wave_sum((double)accA);
+                const double wb = wantB ? wave_sum((double)accB) : 0.0;
+                if (lane == 0) {
+                    sm.slotA[slot] = wa;
+                    sm.slotB[slot] = wb;
+                }
+#endif
+                accA = accB = 0.0f;
+            };
+            // does this slot hold a rejected token? (wave-uniform)
+            auto slot_hit = [&](int slot) -> bool {
+                const uint32_t w = __builtin_amdgcn_readfirstlane(sm.hit_slots[slot >> 5]);
+                return (w >> (slot & 31)) & 1u;
+            };
+            if (MODE == RS_MODE_SPECINFER) {
+                // A = max(R - C_i Q, 0)
+                wave_sweep<In, VEC, UNR, true, false>(tg, dg, V, G, nslots, reverse, pre, &sm.next_slot,
+                    [&](const float (&t)[UNR][VEC], const float (&d)[UNR][VEC], int, int) {
+                        float fa = 0.0f;
 #pragma unroll
-                    for (int u = 0; u < UNR; ++u)
+                        for (int u = 0; u < UNR; ++u)
 #pragma unroll
-                        for (int e = 0; e < VEC; ++e) {
-                            R[u][e] = exp2_fast(expo(t[u][e], c2h, c2l, Kt));
-                            Q[u][e] = exp2_fast(expo(d[u][e], c2h, c2l, Kd));
-                        }
-                    for (int s2 = 0; s2 < ii; ++s2) {
-                        const float c = sm.st_c[s2], inv = sm.st_i[s2];
-                        if (MODE == RS_MODE_SPECINFER) {
+                            for (int e = 0; e < VEC; ++e) {
+                                const float R = exp2_fast(expo(t[u][e], c2h, c2l, Kt));
+                                const float Q = exp2_fast(expo(d[u][e], c2h, c2l, Kd));
+                                fa += fmaxf(fmaf(-ci, Q, R), 0.0f);
+                            }
+                        accA += fa;
+                    },
+                    flush);
+            } else if (ii == 0) {
+                // first rejection: A = min(c Q, R) / 2^f0 = exp2(min(aR - f0, aQ + e)), one
+                // exponential per element; the sum of R over j != x_0 is 1 - R(x_0)
+                const float f0 = sm.st_f0, kq0 = sm.st_kq0;
+                wave_sweep<In, VEC, UNR, true, false>(tg, dg, V, G, nslots, reverse, pre, &sm.next_slot,
+                    [&](const float (&t)[UNR][VEC], const float (&d)[UNR][VEC], int idx0, int slot) {
+                        float v[UNR][VEC];
+#pragma unroll
+                        for (int u = 0; u < UNR; ++u)
+#pragma unroll
+                            for (int e = 0; e < VEC; ++e)
+                                v[u][e] = exp2_fast(fminf(expo(t[u][e], c2h, c2l, Kt) - f0,
+                                                          expo(d[u][e], c2h, c2l, kq0)));
+                        if (slot_hit(slot)) {
 #pragma unroll
                             for (int u = 0; u < UNR; ++u)
 #pragma unroll
                                 for (int e = 0; e < VEC; ++e)
-                                    R[u][e] = fmaxf(fmaf(-c, Q[u][e], R[u][e]), 0.0f) * inv;
-                        } else {
-                            const float a = sm.st_a[s2];
+                                    if (idx0 + u * 64 * VEC + e == xi) v[u][e] = 0.0f;
+                        }
+                        float fa = 0.0f;
+#pragma unroll
+                        for (int u = 0; u < UNR; ++u)
+#pragma unroll
+                            for (int e = 0; e < VEC; ++e) fa += v[u][e];
+                        accA += fa;
+                    },
+                    flush);
+            } else {
+                wave_sweep<In, VEC, UNR, true, false>(tg, dg, V, G, nslots, reverse, pre, &sm.next_slot,
+                    [&](const float (&t)[UNR][VEC], const float (&d)[UNR][VEC], int idx0, int slot) {
+                        const bool hit = slot_hit(slot);
+                        float R[UNR][VEC], Q[UNR][VEC];
+#pragma unroll
+                        for (int u = 0; u < UNR; ++u)
+#pragma unroll
+                            for (int e = 0; e < VEC; ++e) {
+                                R[u][e] = exp2_fast(expo(t[u][e], c2h, c2l, Kt));
+                                Q[u][e] = exp2_fast(expo(d[u][e], c2h, c2l, Kd));
+                            }
+                        for (int s2 = 0; s2 < ii; ++s2) {
+                            const float c = sm.st_c[s2], inv = sm.st_i[s2], a = sm.st_a[s2];
 #pragma unroll
                             for (int u = 0; u < UNR; ++u)
 #pragma unroll
@@ -853,14 +970,6 @@ __global__ void __launch_bounds__(kBlock) rs_row_kernel(const KParams P) {
                                         if (idx0 + u * 64 * VEC + e == x) R[u][e] = 0.0f;
                             }
                         }
-                    }
-                    float fa = 0.0f, fb = 0.0f;
-                    if (MODE == RS_MODE_SPECINFER) {
-#pragma unroll
-                        for (int u = 0; u < UNR; ++u)
-#pragma unroll
-                            for (int e = 0; e < VEC; ++e) fa += fmaxf(fmaf(-ci, Q[u][e], R[u][e]), 0.0f);
-                    } else {
                         if (hit) {
 #pragma unroll
                             for (int u = 0; u < UNR; ++u)
@@ -868,6 +977,7 @@ __global__ void __launch_bounds__(kBlock) rs_row_kernel(const KParams P) {
                                 for (int e = 0; e < VEC; ++e)
                                     if (idx0 + u * 64 * VEC + e == xi) R[u][e] = 0.0f;
                         }
+                        float fa = 0.0f, fb = 0.0f;
 #pragma unroll
                         for (int u = 0; u < UNR; ++u)
 #pragma unroll
@@ -875,24 +985,11 @@ __global__ void __launch_bounds__(kBlock) rs_row_kernel(const KParams P) {
                                 fa += fminf(ci * Q[u][e], R[u][e]);
                                 fb += R[u][e];
                             }
-                    }
-                    accA += fa;
-                    accB += fb;
-                },
-                [&](int slot) {
-#if RS_LANE_PARTIALS
-                    sm.partA[lane][slot] = accA;
-                    if (MODE == RS_MODE_RESISPEC) sm.partB[lane][slot] = accB;
-#else
-                    const double wa = wave_sum((double)accA);
-                    const double wb = (MODE == RS_MODE_RESISPEC) ? wave_sum((double)accB) : 0.0;
-                    if (lane == 0) {
-                        sm.slotA[slot] = wa;
-                        sm.slotB[slot] = wb;
-                    }
-#endif
-                    accA = accB = 0.0f;
-                });
+                        accA += fa;
+                        accB += fb;
+                    },
+                    flush);
+            }
         }
         __syncthreads();
 #if RS_LANE_PARTIALS
@@ -900,7 +997,7 @@ __global__ void __launch_bounds__(kBlock) rs_row_kernel(const KParams P) {
             double a = 0.0, c = 0.0;
 #pragma unroll 8
             for (int l = 0; l < 64; ++l) a += (double)sm.partA[l][tid];
-            if (MODE == RS_MODE_RESISPEC) {
+            if (MODE == RS_MODE_RESISPEC && i > 0) {
 #pragma unroll 8
                 for (int l = 0; l < 64; ++l) c += (double)sm.partB[l][tid];
             }
@@ -916,31 +1013,43 @@ __global__ void __launch_bounds__(kBlock) rs_row_kernel(const KParams P) {
                 A += sm.slotA[s2];
                 Bv += sm.slotB[s2];
             }
-            const double totA = wave_sum(A) / St;   // normalised units
-            const double totB = wave_sum(Bv) / St;
             const double z = sm.st_zd[i];
-            double a = 0.0, inv;
             if (MODE == RS_MODE_SPECINFER) {
-                inv = 1.0 / totA;
-            } else {
-                const double delta = z - totA;   // GetProxy deficit
-                const double C = totB - totA;    // remaining capacity, x0 excluded
-                a = (C > 0.0) ? delta / C : 0.0;
-                inv = 1.0 / z;
-            }
-            // slot totals of the unnormalised next residual (linear in the partials)
-            for (int s2 = lane; s2 < nslots; s2 += 64)
-                sm.slotT[s2] = (MODE == RS_MODE_SPECINFER) ? sm.slotA[s2]
-                                                            : (1.0 - a) * sm.slotA[s2] + a * sm.slotB[s2];
-            if (lane == 0) {
-                if (MODE == RS_MODE_SPECINFER && !(totA > 0.0)) {
-                    sm.status = RS_SEQ_UNDERFLOW;
-                    sm.decision = -2;
+                const double tot = wave_sum(A) / St;   // normalised units
+                if (lane == 0) {
+                    if (!(tot > 0.0)) {
+                        sm.status = RS_SEQ_UNDERFLOW;
+                        sm.decision = -2;
+                    }
+                    sm.st_tot[i] = tot;
                 }
-                sm.st_ad[i] = a;
-                sm.st_a[i] = (float)a;
-                sm.st_id[i] = inv;
-                sm.st_i[i] = (float)inv;
+                for (int s2 = lane; s2 < nslots; s2 += 64) sm.slotT[s2] = sm.slotA[s2];
+            } else {
+                // GetProxy: M = sum min(Z D, R), SR = sum R (both over j != x_i),
+                // a = (Z - M) / (SR - M)
+                const double scale = (i == 0) ? sm.st_2f0 : 1.0;
+                const double M = wave_sum(A) * scale / St;
+                const double SR = (i == 0) ? 1.0 - sm.st_rx[0] : wave_sum(Bv) / St;
+                const double C = SR - M;                 // remaining capacity, x0 excluded
+                const double a = (C > 0.0) ? (z - M) / C : 0.0;
+                // slot totals of the unnormalised next residual (linear in the partials);
+                // after the first rejection the slot sums of R are the pass-1 totals
+                // without x_0
+                for (int s2 = lane; s2 < nslots; s2 += 64) {
+                    double Bs = sm.slotB[s2];
+                    if (i == 0) {
+                        Bs = sm.slotP[s2] - (s2 == sm.sx0 ? sm.rx0e : 0.0);
+                        Bs = Bs > 0.0 ? Bs : 0.0;
+                    }
+                    sm.slotT[s2] = (1.0 - a) * sm.slotA[s2] * scale + a * Bs;
+                }
+                if (lane == 0) {
+                    sm.st_ad[i] = a;
+                    sm.st_a[i] = (float)a;
+                    sm.st_i[i] = (float)(1.0 / z);
+                }
+            }
+            if (lane == 0) {
                 if (worep) {
                     const double rest = 1.0 - sm.cand_q[i] * sm.st_ds[i];
                     sm.st_ds[i + 1] = rest > 0.0 ? sm.st_ds[i] / rest : 0.0;
@@ -980,10 +1089,20 @@ __global__ void __launch_bounds__(kBlock) rs_row_kernel(const KParams P) {
     }
     const int last = nc - 1;   // index of the last rejection step (internal rows)
     const float a_last = (internal && MODE == RS_MODE_RESISPEC) ? sm.st_a[last] : 0.0f;
-    // element values of the final distribution (unnormalised, target units)
+    const bool first_only = internal && MODE == RS_MODE_RESISPEC && last == 0;
+    const float f0 = first_only ? sm.st_f0 : 0.0f, kq0 = first_only ? sm.st_kq0 : 0.0f;
+    const float s2f0 = first_only ? (float)sm.st_2f0 : 0.0f;
+    const int32_t x0 = first_only ? sm.st_x[0] : -1;
+    // element values of the final distribution (unnormalised, target units), computed
+    // as in the pass that produced the slot totals
     auto final_value = [&](float lt, float ld, int j) -> float {
         const float R = exp2_fast(expo(lt, c2h, c2l, Kt));
         if (!internal) return R;
+        if (first_only) {
+            if (j == x0) return 0.0f;
+            const float A = s2f0 * exp2_fast(fminf(expo(lt, c2h, c2l, Kt) - f0, expo(ld, c2h, c2l, kq0)));
+            return fmaf(a_last, R - A, A);
+        }
         const float Q = exp2_fast(expo(ld, c2h, c2l, Kd));
         float A, Bv;
         chain_terms<MODE>(R, Q, j, sm, last, A, Bv);
