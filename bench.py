@@ -73,7 +73,7 @@ def cpu_baseline(w, seconds, mode):
                       "one thread, %.1f s CPU" % (seqs, B, rows_done, w["cfg"]["name"], t_used)}
 
 
-def time_mode(native, torch, w, mode, steps, warmup, ws, out_tok, out_len, out_st):
+def time_mode(native, torch, w, mode, steps, warmup, settle, ws, out_tok, out_len, out_st):
     args = (w["target"], w["draft"], w["node_token"], w["parent"], w["u_accept"], w["u_resample"])
     kw = dict(temperature=w["temperature"], mode=mode, without_replacement=w["without_replacement"],
               bonus=w["bonus"])
@@ -87,6 +87,12 @@ def time_mode(native, torch, w, mode, steps, warmup, ws, out_tok, out_len, out_s
         native.resispec_walk(w["node_token"], ws, out_tok, out_len, out_st,
                              max_depth=w["max_depth"])
 
+    # untimed: steps for at least `settle` seconds (clocks ramp up after the idle time of
+    # workload generation), then the W warmup steps
+    t_end = time.perf_counter() + settle
+    while time.perf_counter() < t_end:
+        step()
+        torch.cuda.synchronize()
     for _ in range(warmup):
         step()
     ev = [(torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True))
@@ -108,6 +114,8 @@ def main():
     ap.add_argument("--warmup", type=int, default=5)
     ap.add_argument("--config", type=int, default=2)
     ap.add_argument("--mode", default="resispec", choices=("resispec", "specinfer"))
+    ap.add_argument("--settle-ms", type=float, default=300.0,
+                    help="untimed steps for at least this long before the warmup steps")
     ap.add_argument("--cpu-seconds", type=float, default=15.0)
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--no-other-mode", action="store_true")
@@ -154,8 +162,8 @@ def main():
     modes = [args.mode] + ([] if args.no_other_mode else
                            [m for m in ("resispec", "specinfer") if m != args.mode])
     for mode in modes:
-        wall, kern_ms = time_mode(native, torch, w, mode, args.steps, args.warmup, ws, out_tok,
-                                  out_len, out_st)
+        wall, kern_ms = time_mode(native, torch, w, mode, args.steps, args.warmup,
+                                  args.settle_ms * 1e-3, ws, out_tok, out_len, out_st)
         lens = out_len.cpu().numpy()
         assert (out_st.cpu().numpy() == 0).all(), "device status not OK"
         kms = float(np.mean(kern_ms))

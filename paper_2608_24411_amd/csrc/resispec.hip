@@ -63,6 +63,14 @@ constexpr int kMaxCand = RS_MAX_CANDIDATES;
 #ifndef RS_UNR32
 #define RS_UNR32 2
 #endif
+// Load policy.  Data whose last full use is the current pass is read with nontemporal
+// loads (about 12% more streaming bandwidth on gfx950): pass 1 of rows without
+// children and every rejection pass.  Pass 1 of a row with children uses ordinary loads,
+// so a rejection pass that follows soon after can still find part of the row in the
+// last-level cache.
+constexpr bool kNtPass1 = false;
+constexpr bool kNtRej = true;
+constexpr bool kNtLeaf = true;
 constexpr int kMaxSlots = RS_MAX_SLOTS;   // per-row slots (runs of chunks) with partial sums
 // A row's exponent reference is fixed before pass 1; sums outside [2^-kLow, inf) send the
 // row through an exact-maximum pass and a second pass 1.
@@ -79,18 +87,41 @@ __device__ __forceinline__ float widen(uint16_t h) { return __uint_as_float(((ui
 // VEC consecutive elements starting at element idx, kept as raw words until used;
 // elements at or beyond V read as -inf, which makes them contribute exactly zero to
 // every sum below.
+// 16-byte load; NT: nontemporal (streamed past the caches' normal allocation)
+typedef unsigned int u32x4 __attribute__((ext_vector_type(4)));
+template <bool NT>
+__device__ __forceinline__ uint4 ld16(const void* p) {
+    if (NT) {
+        const u32x4 r = __builtin_nontemporal_load(reinterpret_cast<const u32x4*>(p));
+        return make_uint4(r.x, r.y, r.z, r.w);
+    }
+    return *reinterpret_cast<const uint4*>(p);
+}
+template <bool NT>
+__device__ __forceinline__ uint32_t ld4(const void* p) {
+    if (NT) return __builtin_nontemporal_load(reinterpret_cast<const uint32_t*>(p));
+    return *reinterpret_cast<const uint32_t*>(p);
+}
+template <bool NT>
+__device__ __forceinline__ uint32_t ld2(const void* p) {
+    if (NT) return __builtin_nontemporal_load(reinterpret_cast<const uint16_t*>(p));
+    return *reinterpret_cast<const uint16_t*>(p);
+}
+
 template <typename In, int VEC>
 struct Vec;
 
 template <>
 struct Vec<float, 4> {
     using raw = uint4;
+    template <bool NT = false>
     static __device__ __forceinline__ raw load(const float* __restrict__ row, int idx, int V) {
-        if (idx < V) return *reinterpret_cast<const uint4*>(row + idx);
+        if (idx < V) return ld16<NT>(row + idx);
         return make_uint4(0xff800000u, 0xff800000u, 0xff800000u, 0xff800000u);
     }
+    template <bool NT = false>
     static __device__ __forceinline__ raw load_full(const float* __restrict__ row, int idx) {
-        return *reinterpret_cast<const uint4*>(row + idx);
+        return ld16<NT>(row + idx);
     }
     static __device__ __forceinline__ void unpack(const raw& r, float (&v)[4]) {
         v[0] = __uint_as_float(r.x); v[1] = __uint_as_float(r.y);
@@ -101,12 +132,14 @@ struct Vec<float, 4> {
 template <>
 struct Vec<uint16_t, 8> {
     using raw = uint4;
+    template <bool NT = false>
     static __device__ __forceinline__ raw load(const uint16_t* __restrict__ row, int idx, int V) {
-        if (idx < V) return *reinterpret_cast<const uint4*>(row + idx);
+        if (idx < V) return ld16<NT>(row + idx);
         return make_uint4(0xff80ff80u, 0xff80ff80u, 0xff80ff80u, 0xff80ff80u);
     }
+    template <bool NT = false>
     static __device__ __forceinline__ raw load_full(const uint16_t* __restrict__ row, int idx) {
-        return *reinterpret_cast<const uint4*>(row + idx);
+        return ld16<NT>(row + idx);
     }
     static __device__ __forceinline__ void unpack(const raw& r, float (&v)[8]) {
         v[0] = bf16_lo(r.x); v[1] = bf16_hi(r.x);
@@ -119,11 +152,13 @@ struct Vec<uint16_t, 8> {
 template <>
 struct Vec<float, 1> {
     using raw = uint32_t;
+    template <bool NT = false>
     static __device__ __forceinline__ raw load(const float* __restrict__ row, int idx, int V) {
-        return idx < V ? __float_as_uint(row[idx]) : 0xff800000u;
+        return idx < V ? ld4<NT>(row + idx) : 0xff800000u;
     }
+    template <bool NT = false>
     static __device__ __forceinline__ raw load_full(const float* __restrict__ row, int idx) {
-        return __float_as_uint(row[idx]);
+        return ld4<NT>(row + idx);
     }
     static __device__ __forceinline__ void unpack(const raw& r, float (&v)[1]) { v[0] = __uint_as_float(r); }
 };
@@ -131,11 +166,13 @@ struct Vec<float, 1> {
 template <>
 struct Vec<uint16_t, 1> {
     using raw = uint32_t;
+    template <bool NT = false>
     static __device__ __forceinline__ raw load(const uint16_t* __restrict__ row, int idx, int V) {
-        return idx < V ? ((uint32_t)row[idx]) << 16 : 0xff800000u;
+        return idx < V ? ld2<NT>(row + idx) << 16 : 0xff800000u;
     }
+    template <bool NT = false>
     static __device__ __forceinline__ raw load_full(const uint16_t* __restrict__ row, int idx) {
-        return ((uint32_t)row[idx]) << 16;
+        return ld2<NT>(row + idx) << 16;
     }
     static __device__ __forceinline__ void unpack(const raw& r, float (&v)[1]) { v[0] = __uint_as_float(r); }
 };
@@ -398,7 +435,7 @@ __device__ double scalar_residual(const Smem& sm, int i, double p, double q, int
 // of a chunk (element (u, e) has index idx0 + u * 64 * VEC + e); flush(slot) runs
 // after a slot's last chunk.  reverse: slots in descending order, chunks descending
 // inside a slot.
-template <typename In, int VEC, int UNR, bool PAIR, bool PRE, typename Body, typename Flush>
+template <typename In, int VEC, int UNR, bool PAIR, bool PRE, bool NT, typename Body, typename Flush>
 __device__ __forceinline__ void wave_sweep(const In* __restrict__ tg, const In* __restrict__ dg,
                                            int V, int G, int nslots, bool reverse,
                                            const typename Vec<In, VEC>::raw (&pre)[UNR],
@@ -435,14 +472,14 @@ __device__ __forceinline__ void wave_sweep(const In* __restrict__ tg, const In* 
         if (c0 + CHUNK <= V) {
 #pragma unroll
             for (int u = 0; u < UNR; ++u) {
-                t[u] = W::load_full(tg, c0 + lane0 + u * 64 * VEC);
-                if (PAIR) d[u] = W::load_full(dg, c0 + lane0 + u * 64 * VEC);
+                t[u] = W::template load_full<NT>(tg, c0 + lane0 + u * 64 * VEC);
+                if (PAIR) d[u] = W::template load_full<NT>(dg, c0 + lane0 + u * 64 * VEC);
             }
         } else {
 #pragma unroll
             for (int u = 0; u < UNR; ++u) {
-                t[u] = W::load(tg, c0 + lane0 + u * 64 * VEC, V);
-                if (PAIR) d[u] = W::load(dg, c0 + lane0 + u * 64 * VEC, V);
+                t[u] = W::template load<NT>(tg, c0 + lane0 + u * 64 * VEC, V);
+                if (PAIR) d[u] = W::template load<NT>(dg, c0 + lane0 + u * 64 * VEC, V);
             }
         }
     };
@@ -464,7 +501,7 @@ __device__ __forceinline__ void wave_sweep(const In* __restrict__ tg, const In* 
         if (PAIR) {
             const int c0 = chunk_start(sa, 0);
 #pragma unroll
-            for (int u = 0; u < UNR; ++u) ad[u] = W::load(dg, c0 + lane0 + u * 64 * VEC, V);
+            for (int u = 0; u < UNR; ++u) ad[u] = W::template load<NT>(dg, c0 + lane0 + u * 64 * VEC, V);
         }
     } else {
         load(sa, ja, at, ad);
@@ -519,7 +556,7 @@ __global__ void __launch_bounds__(kBlock) __attribute__((amdgpu_waves_per_eu(4))
     // overlaps the row description below (the first slot of wave w is slot w).
     typename W::raw pre[UNR];
 #pragma unroll
-    for (int u = 0; u < UNR; ++u) pre[u] = W::load(tg, wid * G * CHUNK + lane * VEC + u * 64 * VEC, V);
+    for (int u = 0; u < UNR; ++u) pre[u] = W::template load<kNtPass1>(tg, wid * G * CHUNK + lane * VEC + u * 64 * VEC, V);
 
     // ---- row description.  "Holder" threads own one candidate each: node, token and
     // uniform now; the two logits of its token are gathered while pass 1 streams and
@@ -680,7 +717,7 @@ __global__ void __launch_bounds__(kBlock) __attribute__((amdgpu_waves_per_eu(4))
             fa = fc = 0.0f;
         };
         if (internal) {
-            wave_sweep<In, VEC, UNR, true, true>(tg, dg, V, G, nslots, false, pre, &sm.next_slot,
+            wave_sweep<In, VEC, UNR, true, true, kNtPass1>(tg, dg, V, G, nslots, false, pre, &sm.next_slot,
                 [&](const float (&t)[UNR][VEC], const float (&d)[UNR][VEC], int, int) {
 #pragma unroll
                     for (int u = 0; u < UNR; ++u)
@@ -692,7 +729,7 @@ __global__ void __launch_bounds__(kBlock) __attribute__((amdgpu_waves_per_eu(4))
                 },
                 flush);
         } else {
-            wave_sweep<In, VEC, UNR, false, true>(tg, dg, V, G, nslots, false, pre, &sm.next_slot,
+            wave_sweep<In, VEC, UNR, false, true, kNtLeaf>(tg, dg, V, G, nslots, false, pre, &sm.next_slot,
                 [&](const float (&t)[UNR][VEC], const float (&)[UNR][VEC], int, int) {
 #pragma unroll
                     for (int u = 0; u < UNR; ++u)
@@ -757,7 +794,7 @@ __global__ void __launch_bounds__(kBlock) __attribute__((amdgpu_waves_per_eu(4))
         // exact maxima of both rows, then the references are taken from them
         {
             float mx = -FLT_MAX, my = -FLT_MAX;
-            wave_sweep<In, VEC, UNR, true, false>(tg, dg, V, G, nslots, false, pre, &sm.next_slot,
+            wave_sweep<In, VEC, UNR, true, false, kNtPass1>(tg, dg, V, G, nslots, false, pre, &sm.next_slot,
                 [&](const float (&t)[UNR][VEC], const float (&d)[UNR][VEC], int, int) {
 #pragma unroll
                     for (int u = 0; u < UNR; ++u)
@@ -898,7 +935,7 @@ __global__ void __launch_bounds__(kBlock) __attribute__((amdgpu_waves_per_eu(4))
             };
             if (MODE == RS_MODE_SPECINFER) {
                 // A = max(R - C_i Q, 0)
-                wave_sweep<In, VEC, UNR, true, false>(tg, dg, V, G, nslots, reverse, pre, &sm.next_slot,
+                wave_sweep<In, VEC, UNR, true, false, kNtRej>(tg, dg, V, G, nslots, reverse, pre, &sm.next_slot,
                     [&](const float (&t)[UNR][VEC], const float (&d)[UNR][VEC], int, int) {
                         float fa = 0.0f;
 #pragma unroll
@@ -916,7 +953,7 @@ __global__ void __launch_bounds__(kBlock) __attribute__((amdgpu_waves_per_eu(4))
                 // first rejection: A = min(c Q, R) / 2^f0 = exp2(min(aR - f0, aQ + e)), one
                 // exponential per element; the sum of R over j != x_0 is 1 - R(x_0)
                 const float f0 = sm.st_f0, kq0 = sm.st_kq0;
-                wave_sweep<In, VEC, UNR, true, false>(tg, dg, V, G, nslots, reverse, pre, &sm.next_slot,
+                wave_sweep<In, VEC, UNR, true, false, kNtRej>(tg, dg, V, G, nslots, reverse, pre, &sm.next_slot,
                     [&](const float (&t)[UNR][VEC], const float (&d)[UNR][VEC], int idx0, int slot) {
                         float v[UNR][VEC];
 #pragma unroll
@@ -941,7 +978,7 @@ __global__ void __launch_bounds__(kBlock) __attribute__((amdgpu_waves_per_eu(4))
                     },
                     flush);
             } else {
-                wave_sweep<In, VEC, UNR, true, false>(tg, dg, V, G, nslots, reverse, pre, &sm.next_slot,
+                wave_sweep<In, VEC, UNR, true, false, kNtRej>(tg, dg, V, G, nslots, reverse, pre, &sm.next_slot,
                     [&](const float (&t)[UNR][VEC], const float (&d)[UNR][VEC], int idx0, int slot) {
                         const bool hit = slot_hit(slot);
                         float R[UNR][VEC], Q[UNR][VEC];
