@@ -3,34 +3,41 @@
 // Paper: "ResiSpec: Enhancing Multi-Candidate Speculative Sampling via Residual
 // Distribution Shaping".  One workgroup verifies one tree node (one logits row):
 //
-//   pass 1   online softmax statistics (max, sum of exp) of the target row and, for
-//            nodes with children, the draft row (Preliminary; temperature T);
+//   pass 1   softmax statistics (sums of exp) of the target row and, for nodes with
+//            children, the draft row (Preliminary; temperature T);
 //   tests    candidate i is accepted iff u_i < R_i(x_i) / D_i(x_i) (Eq. 2 and
 //            Algorithm 1), evaluated in fp64 on the gathered candidate logits;
 //   pass i+1 after the i-th rejection one more pass over the row computes the sums the
 //            residual update needs:
-//              standard (Eq. 1/2):   S = sum_j max(R_j - D_j, 0)
-//              ResiSpec (Algorithm 1, GetProxy): M = sum_{j != x0} min(Z D_j, R_j) and
-//                                    SR = sum_{j != x0} R_j, with Z = D(x0) - R(x0).
+//              standard (Eq. 1/2):   Tot = sum_j max(p_j - C_i q_j, 0); applying
+//                                    max(R - D, 0) / S i times gives
+//                                    max(p - C_i q, 0) / Tot with C_i from the earlier
+//                                    totals, so one step per element for any i;
+//              ResiSpec (Algorithm 1, GetProxy): M = sum_{j != x0} min(Z D_j, R_j), with
+//                                    Z = D(x0) - R(x0); SR = sum_{j != x0} R_j is
+//                                    1 - R(x0) because R is normalised.
 //            GetProxy's one-shot redistribution of Delta = Z - M into the capacity
 //            R_j - m_j gives, with a = Delta / (SR - M), the residual
 //              R'_j = ((1 - a) min(Z D_j, R_j) + a R_j) / Z   (j != x0),   R'_x0 = 0,
 //            i.e. norm(max(R - K, 0)) for the proxy K = R - r, K(x0) = D(x0).  So the
 //            residual is never materialised: every pass re-derives R_j from the two
-//            logits of token j through the chain of per-rejection scalars;
+//            logits of token j through the chain of per-rejection scalars.  After the
+//            first rejection min(c Q, R) = exp2(min(log2 R, log2 Q + log2 c)) takes a
+//            single exponential per element;
 //   draw     when every candidate is rejected (or the node is a leaf: bonus draw from
 //            p), the token is the smallest j whose running sum of the final residual in
 //            vocabulary order exceeds u * total.  The last pass records partial sums
-//            per slot (a run of 64 * 16 elements for bf16), so the draw re-reads one
-//            slot.
+//            per slot (a run of G chunks of 64 * VEC * UNR elements), so the draw
+//            re-reads one slot.
 //
-// Numerics: elements in fp32 (bf16 widened exactly), every sum accumulated in fp64,
-// the candidates' probabilities and the scalar chain in fp64.  Exponents are taken as
-// exp2(l * c2 + K) with c2 = log2(e)/T split into two floats and K = -max * c2 rounded
-// once; the rounding of K is common to a whole row and cancels in the normalisation,
-// and the fp64 gathers use the same constants, so candidate probabilities agree with
-// the fp32 sums they are divided by.  Residual elements are carried in units of the
-// target row's unnormalised mass (the target normaliser is folded into the step
+// Numerics: elements in fp32 (bf16 widened exactly), sums of fp32 lane partials in
+// fp64, the candidates' probabilities and the scalar chain in fp64.  Exponents are
+// exp2(l * c2 + K) with c2 = log2(e)/T split into two floats and K an integer-valued
+// reference fixed per row before pass 1 (from the first chunks' maximum; a row whose
+// sums overflow or underflow against it takes an exact-maximum pass), so an element's
+// value does not depend on which wave read it and every reduction runs in a fixed
+// order: results are bitwise reproducible.  Residual elements are carried in units of
+// the target row's unnormalised mass (the target normaliser is folded into the step
 // constants).
 //
 // A second kernel walks each tree from the root along accepted children.
@@ -425,20 +432,46 @@ __device__ double scalar_residual(const Smem& sm, int i, double p, double q, int
     return R;
 }
 
+// One chunk (UNR loads of 64 * VEC elements per row) starting at element c0 + lane * VEC;
+// chunks wholly below V load without per-lane bounds checks.
+template <typename In, int VEC, int UNR, bool PAIR, bool NT>
+__device__ __forceinline__ void load_chunk(const In* __restrict__ tg, const In* __restrict__ dg,
+                                           int c0, int V, typename Vec<In, VEC>::raw (&t)[UNR],
+                                           typename Vec<In, VEC>::raw (&d)[UNR]) {
+    using W = Vec<In, VEC>;
+    constexpr int CHUNK = 64 * VEC * UNR;
+    const int l0 = c0 + (threadIdx.x & 63) * VEC;
+    if (c0 + CHUNK <= V) {
+#pragma unroll
+        for (int u = 0; u < UNR; ++u) {
+            t[u] = W::template load_full<NT>(tg, l0 + u * 64 * VEC);
+            if (PAIR) d[u] = W::template load_full<NT>(dg, l0 + u * 64 * VEC);
+        }
+    } else {
+#pragma unroll
+        for (int u = 0; u < UNR; ++u) {
+            t[u] = W::template load<NT>(tg, l0 + u * 64 * VEC, V);
+            if (PAIR) d[u] = W::template load<NT>(dg, l0 + u * 64 * VEC, V);
+        }
+    }
+}
+
 // One pass over the row.  The row is cut into chunks of 64 * VEC * UNR elements (one
 // 128-bit load per lane and UNR) and runs of G chunks form slots.  Waves take slots
 // from a shared counter, so the eight waves of the block finish within about one chunk
 // of each other; a wave's first slot is its own index, so its first loads can be
-// issued before the counter is set.  Two register sets alternate: the next chunk is
-// loaded into one while the other is processed.  Chunks wholly below V are loaded
-// without per-lane bounds checks.  body(t, d, idx0, slot) gets the unpacked elements
+// issued before the counter is set (PRE = 1: its target part was loaded by the caller
+// into pre_t; PRE = 2: target and draft parts, into pre_t and pre_d).  Two register
+// sets alternate: the next chunk is loaded into one while the other is processed.
+// body(t, d, idx0, slot) gets the unpacked elements
 // of a chunk (element (u, e) has index idx0 + u * 64 * VEC + e); flush(slot) runs
 // after a slot's last chunk.  reverse: slots in descending order, chunks descending
 // inside a slot.
-template <typename In, int VEC, int UNR, bool PAIR, bool PRE, bool NT, typename Body, typename Flush>
+template <typename In, int VEC, int UNR, bool PAIR, int PRE, bool NT, typename Body, typename Flush>
 __device__ __forceinline__ void wave_sweep(const In* __restrict__ tg, const In* __restrict__ dg,
                                            int V, int G, int nslots, bool reverse,
-                                           const typename Vec<In, VEC>::raw (&pre)[UNR],
+                                           const typename Vec<In, VEC>::raw (&pre_t)[UNR],
+                                           const typename Vec<In, VEC>::raw (&pre_d)[UNR],
                                            int* counter, Body&& body, Flush&& flush) {
     using W = Vec<In, VEC>;
     using raw = typename W::raw;
@@ -468,20 +501,7 @@ __device__ __forceinline__ void wave_sweep(const In* __restrict__ tg, const In* 
         }
     };
     auto load = [&](int s, int j, raw (&t)[UNR], raw (&d)[UNR]) {
-        const int c0 = chunk_start(s, j);
-        if (c0 + CHUNK <= V) {
-#pragma unroll
-            for (int u = 0; u < UNR; ++u) {
-                t[u] = W::template load_full<NT>(tg, c0 + lane0 + u * 64 * VEC);
-                if (PAIR) d[u] = W::template load_full<NT>(dg, c0 + lane0 + u * 64 * VEC);
-            }
-        } else {
-#pragma unroll
-            for (int u = 0; u < UNR; ++u) {
-                t[u] = W::template load<NT>(tg, c0 + lane0 + u * 64 * VEC, V);
-                if (PAIR) d[u] = W::template load<NT>(dg, c0 + lane0 + u * 64 * VEC, V);
-            }
-        }
+        load_chunk<In, VEC, UNR, PAIR, NT>(tg, dg, chunk_start(s, j), V, t, d);
     };
     auto process = [&](const raw (&ct)[UNR], const raw (&cd)[UNR], int s, int j) {
         float t[UNR][VEC], d[UNR][VEC];
@@ -495,13 +515,18 @@ __device__ __forceinline__ void wave_sweep(const In* __restrict__ tg, const In* 
     };
     raw at[UNR], ad[UNR], bt[UNR], bd[UNR];
     int sa = slot, ja = 0;
-    if (PRE) {
+    if (PRE >= 1) {
 #pragma unroll
-        for (int u = 0; u < UNR; ++u) at[u] = pre[u];
+        for (int u = 0; u < UNR; ++u) at[u] = pre_t[u];
         if (PAIR) {
-            const int c0 = chunk_start(sa, 0);
+            if (PRE == 2) {
 #pragma unroll
-            for (int u = 0; u < UNR; ++u) ad[u] = W::template load<NT>(dg, c0 + lane0 + u * 64 * VEC, V);
+                for (int u = 0; u < UNR; ++u) ad[u] = pre_d[u];
+            } else {
+                const int c0 = chunk_start(sa, 0);
+#pragma unroll
+                for (int u = 0; u < UNR; ++u) ad[u] = W::template load<NT>(dg, c0 + lane0 + u * 64 * VEC, V);
+            }
         }
     } else {
         load(sa, ja, at, ad);
@@ -541,7 +566,9 @@ __global__ void __launch_bounds__(kBlock) __attribute__((amdgpu_waves_per_eu(4))
         n = 0;
     } else {
         // node-major order: the roots of all sequences first, then node 1, ... (nodes
-        // with children come early in a topological numbering)
+        // with children, whose rows take rejection passes, come early in a topological
+        // numbering, so the grid ends on short rows; an order that mixes sequences'
+        // rows runs 1.5x longer on a 128-tree batch because late roots form a tail)
         const int32_t g = blockIdx.x;
         n = g / P.B;
         b = g - n * P.B;
@@ -717,7 +744,7 @@ __global__ void __launch_bounds__(kBlock) __attribute__((amdgpu_waves_per_eu(4))
             fa = fc = 0.0f;
         };
         if (internal) {
-            wave_sweep<In, VEC, UNR, true, true, kNtPass1>(tg, dg, V, G, nslots, false, pre, &sm.next_slot,
+            wave_sweep<In, VEC, UNR, true, 1, kNtPass1>(tg, dg, V, G, nslots, false, pre, pre, &sm.next_slot,
                 [&](const float (&t)[UNR][VEC], const float (&d)[UNR][VEC], int, int) {
 #pragma unroll
                     for (int u = 0; u < UNR; ++u)
@@ -729,7 +756,7 @@ __global__ void __launch_bounds__(kBlock) __attribute__((amdgpu_waves_per_eu(4))
                 },
                 flush);
         } else {
-            wave_sweep<In, VEC, UNR, false, true, kNtLeaf>(tg, dg, V, G, nslots, false, pre, &sm.next_slot,
+            wave_sweep<In, VEC, UNR, false, 1, kNtLeaf>(tg, dg, V, G, nslots, false, pre, pre, &sm.next_slot,
                 [&](const float (&t)[UNR][VEC], const float (&)[UNR][VEC], int, int) {
 #pragma unroll
                     for (int u = 0; u < UNR; ++u)
@@ -794,7 +821,7 @@ __global__ void __launch_bounds__(kBlock) __attribute__((amdgpu_waves_per_eu(4))
         // exact maxima of both rows, then the references are taken from them
         {
             float mx = -FLT_MAX, my = -FLT_MAX;
-            wave_sweep<In, VEC, UNR, true, false, kNtPass1>(tg, dg, V, G, nslots, false, pre, &sm.next_slot,
+            wave_sweep<In, VEC, UNR, true, 0, kNtPass1>(tg, dg, V, G, nslots, false, pre, pre, &sm.next_slot,
                 [&](const float (&t)[UNR][VEC], const float (&d)[UNR][VEC], int, int) {
 #pragma unroll
                     for (int u = 0; u < UNR; ++u)
@@ -935,7 +962,7 @@ __global__ void __launch_bounds__(kBlock) __attribute__((amdgpu_waves_per_eu(4))
             };
             if (MODE == RS_MODE_SPECINFER) {
                 // A = max(R - C_i Q, 0)
-                wave_sweep<In, VEC, UNR, true, false, kNtRej>(tg, dg, V, G, nslots, reverse, pre, &sm.next_slot,
+                wave_sweep<In, VEC, UNR, true, 0, kNtRej>(tg, dg, V, G, nslots, reverse, pre, pre, &sm.next_slot,
                     [&](const float (&t)[UNR][VEC], const float (&d)[UNR][VEC], int, int) {
                         float fa = 0.0f;
 #pragma unroll
@@ -953,7 +980,7 @@ __global__ void __launch_bounds__(kBlock) __attribute__((amdgpu_waves_per_eu(4))
                 // first rejection: A = min(c Q, R) / 2^f0 = exp2(min(aR - f0, aQ + e)), one
                 // exponential per element; the sum of R over j != x_0 is 1 - R(x_0)
                 const float f0 = sm.st_f0, kq0 = sm.st_kq0;
-                wave_sweep<In, VEC, UNR, true, false, kNtRej>(tg, dg, V, G, nslots, reverse, pre, &sm.next_slot,
+                wave_sweep<In, VEC, UNR, true, 0, kNtRej>(tg, dg, V, G, nslots, reverse, pre, pre, &sm.next_slot,
                     [&](const float (&t)[UNR][VEC], const float (&d)[UNR][VEC], int idx0, int slot) {
                         float v[UNR][VEC];
 #pragma unroll
@@ -978,7 +1005,7 @@ __global__ void __launch_bounds__(kBlock) __attribute__((amdgpu_waves_per_eu(4))
                     },
                     flush);
             } else {
-                wave_sweep<In, VEC, UNR, true, false, kNtRej>(tg, dg, V, G, nslots, reverse, pre, &sm.next_slot,
+                wave_sweep<In, VEC, UNR, true, 0, kNtRej>(tg, dg, V, G, nslots, reverse, pre, pre, &sm.next_slot,
                     [&](const float (&t)[UNR][VEC], const float (&d)[UNR][VEC], int idx0, int slot) {
                         const bool hit = slot_hit(slot);
                         float R[UNR][VEC], Q[UNR][VEC];
