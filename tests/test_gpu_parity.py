@@ -262,6 +262,59 @@ def test_max_children(gpu_lib):
                 compare_walk(gpu, oracle_walk(host_tree(w), w, mode))
 
 
+@pytest.mark.parametrize("worep", [False, True])
+@pytest.mark.parametrize("V,dtype", [(10007, "f32"), (12288, "bf16")])
+def test_long_rejection_chains(gpu_lib, worep, V, dtype):
+    """Nodes that reject several candidates in a row: a root with 12 children and two
+    nodes with 6, candidates taken where the draft over-weights the target (Gumbel-top-k
+    of d - t; with replacement the second candidate repeats the first).  Exercises the
+    later steps of both residual updates, with and without replacement, and checks the
+    drawn distributions entry by entry."""
+    g = torch.Generator().manual_seed(V + 7 * worep)
+    par = [-1] + [0] * 12 + [1] * 6 + [13] * 6
+    B, N = 6, len(par)
+    t = 2.0 * torch.randn((B, N, V), generator=g)
+    d = 0.3 * t + 2.0 * torch.randn((B, N, V), generator=g)
+    if dtype == "bf16":
+        t, d = t.to(torch.bfloat16), d.to(torch.bfloat16)
+    parent = torch.tensor(par, dtype=torch.int32).repeat(B, 1)
+    tok = torch.zeros((B, N), dtype=torch.int32)
+    kids_of = {n: [m for m in range(N) if par[m] == n] for n in range(N)}
+    for b in range(B):
+        for n, kids in kids_of.items():
+            if not kids:
+                continue
+            gum = -torch.log(-torch.log(torch.rand(V, generator=g).clamp_(min=1e-20)))
+            pick = torch.topk(d[b, n].float() - t[b, n].float() + gum, len(kids)).indices
+            if not worep and len(kids) > 2:
+                pick[1] = pick[0]
+            tok[b, torch.as_tensor(kids)] = pick.to(torch.int32)
+    w = dict(target=t.cuda(), draft=d.cuda(), node_token=tok.cuda(), parent=parent.cuda(),
+             u_accept=torch.rand((B, N), generator=g).cuda(),
+             u_resample=torch.rand((B, N), generator=g).cuda(), temperature=1.0,
+             without_replacement=worep, max_depth=3)
+    h = host_tree(w)
+    internal = [n for n in range(N) if kids_of[n]]
+    for mode in MODES:
+        _log("long chains", V, dtype, "worep", worep, mode)
+        gpu = gpu_tree(gpu_lib, w, mode, debug=True, want_residual=True)
+        compare_walk(gpu, oracle_walk(h, w, mode))
+        drew = [r for r in range(B * N) if gpu["node_child"].reshape(-1)[r].item() < 0]
+        n_cmp, n_flag, orc = compare_nodes(gpu, h, w, mode, residual_rows=drew)
+        _log("  nodes compared", n_cmp, "flagged", n_flag, compare_nodes.last)
+        assert n_cmp >= 0.8 * B * N
+        # the chains are long: internal nodes reject candidates before they accept (the
+        # proxy-shaped residual accepts within two or three), and with the standard
+        # residual most of them reject every candidate and draw
+        child = orc["child"].reshape(B, N)
+        rejected = np.array([len(kids_of[n]) if child[b, n] < 0 else child[b, n] - kids_of[n][0]
+                             for b in range(B) for n in internal])
+        assert np.mean(rejected >= 1) > 0.8, rejected
+        if mode == "specinfer":
+            assert np.mean(rejected == np.array([len(kids_of[n]) for b in range(B)
+                                                 for n in internal])) > 0.5, rejected
+
+
 def test_determinism(gpu_lib):
     w = synth.make_workload(2, device="cuda", B=16)
     for mode in MODES:
