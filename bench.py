@@ -119,6 +119,7 @@ def main():
     ap.add_argument("--cpu-seconds", type=float, default=15.0)
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--no-other-mode", action="store_true")
+    ap.add_argument("--no-path", action="store_true", help="skip the path-only schedule")
     ap.add_argument("--copy-probe", type=int, default=0, metavar="MIB",
                     help="only run a plain device copy of MIB MiB (counter calibration)")
     args = ap.parse_args()
@@ -176,6 +177,36 @@ def main():
             "mean_accepted_len": float(lens.mean()),
         }
 
+    # the path-only schedule of the same step (only the nodes each walk reaches)
+    path = None
+    if not args.no_path:
+        kw = dict(temperature=w["temperature"], max_depth=w["max_depth"], mode=args.mode,
+                  without_replacement=w["without_replacement"], bonus=w["bonus"])
+        pargs = (w["target"], w["draft"], w["node_token"], w["parent"], w["u_accept"],
+                 w["u_resample"])
+
+        def pstep():
+            native.resispec_verify_tree_path(*pargs, out_tokens=out_tok, out_accepted_len=out_len,
+                                             out_status=out_st, **kw)
+        t_end = time.perf_counter() + args.settle_ms * 1e-3
+        while time.perf_counter() < t_end:
+            pstep()
+            torch.cuda.synchronize()
+        for _ in range(args.warmup):
+            pstep()
+        torch.cuda.synchronize()
+        t0 = time.perf_counter()
+        for _ in range(args.steps):
+            pstep()
+        torch.cuda.synchronize()
+        pwall = (time.perf_counter() - t0) / args.steps
+        plens = out_len.cpu().numpy()
+        assert (out_st.cpu().numpy() == 0).all(), "device status not OK"
+        path = {"ms_per_step": 1e3 * pwall, "sequences_per_s": B / pwall,
+                "rows_verified_per_step": int(plens.sum() + B),
+                "accepted_tokens_per_s": float(plens.sum()) / pwall,
+                "speedup_vs_all_nodes": results[args.mode]["ms_per_step"] / (1e3 * pwall)}
+
     r = results[args.mode]
     achieved = r["row_kernel_gbps"]
     out = {
@@ -201,6 +232,7 @@ def main():
                      "kernel": "rs_row_kernel", "alg_bytes_per_launch": alg_bytes,
                      "rows_target": rows_t, "rows_draft": rows_d},
         "modes": results,
+        "path_schedule": path,
     }
     if not args.no_cpu_baseline:
         out["cpu_baseline"] = cpu_baseline(w, args.cpu_seconds, args.mode)

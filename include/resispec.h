@@ -136,6 +136,24 @@ rs_status resispec_verify_tree(const void* target_logits, const void* draft_logi
                                void* workspace, size_t workspace_bytes, void* stream);
 
 /*
+ * Path-only schedule of resispec_verify_tree (same arguments without the workspace, same
+ * results): one workgroup per sequence walks its tree from the root and verifies only
+ * the nodes the walk reaches, one after another (Preliminary, tree-structured
+ * verification: a node is verified only after its parent accepted it).  It reads the
+ * rows of about accepted_len + 1 nodes per sequence instead of all N, and runs
+ * B workgroups.  Per-node outcomes are the same functions of the node's rows and
+ * uniforms as in the all-nodes schedule, so the tokens, lengths and statuses are
+ * identical, faults included: both report only what the walk meets (a malformed
+ * parent array is met at the root, whose row checks the whole array).
+ */
+rs_status resispec_verify_tree_path(const void* target_logits, const void* draft_logits,
+                                    const int32_t* node_token, const int32_t* parent,
+                                    const float* u_accept, const float* u_resample,
+                                    int32_t B, int32_t N, int32_t V, int32_t max_depth,
+                                    const rs_params* prm, int32_t* out_tokens,
+                                    int32_t* out_accepted_len, int32_t* out_status, void* stream);
+
+/*
  * The two stages of resispec_verify_tree, for callers that schedule them separately
  * (same kernels, same results):
  *   resispec_verify_nodes: every node's own outcome (accepted child or drawn token) into

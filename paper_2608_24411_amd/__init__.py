@@ -5,7 +5,8 @@ include/resispec.h); `native` is its Python binding and `synth` generates the
 seeded synthetic workloads.  The binding is loaded on first use of an entry point.
 """
 
-_API = ("resispec_verify", "resispec_verify_tree", "resispec_verify_tree_debug",
+_API = ("resispec_verify", "resispec_verify_tree", "resispec_verify_tree_path",
+        "resispec_verify_tree_debug",
         "resispec_workspace_bytes", "resispec_validate_tree_host", "resispec_status_string",
         "resispec_abi_version")
 

@@ -303,6 +303,8 @@ struct Smem {
     // draw
     int32_t token;
     double total;
+    // outcome of the row (path schedule)
+    int32_t res_child, res_tok, res_status;
 };
 
 struct KParams {
@@ -548,9 +550,12 @@ __device__ __forceinline__ void wave_sweep(const In* __restrict__ tg, const In* 
 
 // ------------------------------------------------------------ row kernel ----
 
-template <typename In, int VEC, int UNR, int MODE>
-__global__ void __launch_bounds__(kBlock) __attribute__((amdgpu_waves_per_eu(4))) rs_row_kernel(const KParams P) {
-    __shared__ Smem sm;
+// Verification of one node row by the whole workgroup: node n of sequence b (row
+// b * N + n; flat rows: b = row, n = 0).  emit(child, token, status) is called by
+// thread 0 once, with the node's outcome.
+template <typename In, int VEC, int UNR, int MODE, typename Emit>
+__device__ __forceinline__ void verify_row(const KParams& P, Smem& sm, const int64_t row,
+                                           const int32_t b, const int32_t n, Emit&& emit) {
     const int tid = threadIdx.x;
     const int lane = tid & 63;
     const int wid = tid >> 6;
@@ -558,22 +563,6 @@ __global__ void __launch_bounds__(kBlock) __attribute__((amdgpu_waves_per_eu(4))
     constexpr int CHUNK = 64 * VEC * UNR;
     const int G = P.G, nslots = P.nslots;
 
-    int64_t row;
-    int32_t b, n;
-    if (P.flat) {
-        row = blockIdx.x;
-        b = (int32_t)row;
-        n = 0;
-    } else {
-        // node-major order: the roots of all sequences first, then node 1, ... (nodes
-        // with children, whose rows take rejection passes, come early in a topological
-        // numbering, so the grid ends on short rows; an order that mixes sequences'
-        // rows runs 1.5x longer on a 128-tree batch because late roots form a tail)
-        const int32_t g = blockIdx.x;
-        n = g / P.B;
-        b = g - n * P.B;
-        row = (int64_t)b * P.N + n;
-    }
     const In* __restrict__ tg = reinterpret_cast<const In*>(P.tgt) + row * V;
     const In* __restrict__ dg = reinterpret_cast<const In*>(P.dft) + row * V;
 
@@ -694,12 +683,12 @@ __global__ void __launch_bounds__(kBlock) __attribute__((amdgpu_waves_per_eu(4))
         status = sm.status;
     }
     if (status != RS_SEQ_OK) {
-        if (tid == 0) write_outcome(P, row, -1, -1, status);
+        if (tid == 0) emit(-1, -1, status);
         zero_residual_row(P, row);
         return;
     }
     if (nc == 0 && !P.flat && !P.bonus) {
-        if (tid == 0) write_outcome(P, row, -1, -1, RS_SEQ_OK);
+        if (tid == 0) emit(-1, -1, RS_SEQ_OK);
         zero_residual_row(P, row);
         return;
     }
@@ -814,7 +803,7 @@ __global__ void __launch_bounds__(kBlock) __attribute__((amdgpu_waves_per_eu(4))
         __syncthreads();
         if (sm.decision != -3) break;
         if (attempt == 1) {
-            if (tid == 0) write_outcome(P, row, -1, -1, RS_SEQ_UNDERFLOW);
+            if (tid == 0) emit(-1, -1, RS_SEQ_UNDERFLOW);
             zero_residual_row(P, row);
             return;
         }
@@ -1131,14 +1120,14 @@ __global__ void __launch_bounds__(kBlock) __attribute__((amdgpu_waves_per_eu(4))
     if (threadIdx.x == 0 && g_timing) g_timing[row * 16 + 7] = i;   // rejection passes
 #endif
     if (sm.decision == -2) {
-        if (tid == 0) write_outcome(P, row, -1, -1, sm.status);
+        if (tid == 0) emit(-1, -1, sm.status);
         zero_residual_row(P, row);
         return;
     }
     if (sm.decision >= 0) {
         if (tid == 0) {
             const int d = sm.decision;
-            write_outcome(P, row, sm.cand_node[d], sm.cand_tok[d], RS_SEQ_OK);
+            emit(sm.cand_node[d], sm.cand_tok[d], RS_SEQ_OK);
         }
         zero_residual_row(P, row);
         return;
@@ -1147,7 +1136,7 @@ __global__ void __launch_bounds__(kBlock) __attribute__((amdgpu_waves_per_eu(4))
     // ---- every candidate rejected, or no candidates: inverse-CDF draw (wave 0)
     const float u = sm.ur;
     if (!(u >= 0.0f && u < 1.0f)) {
-        if (tid == 0) write_outcome(P, row, -1, -1, RS_SEQ_BAD_UNIFORM);
+        if (tid == 0) emit(-1, -1, RS_SEQ_BAD_UNIFORM);
         zero_residual_row(P, row);
         return;
     }
@@ -1317,9 +1306,9 @@ __global__ void __launch_bounds__(kBlock) __attribute__((amdgpu_waves_per_eu(4))
     RS_STAMP(row, 5);
     const int32_t tok = sm.token;
     if (tid == 0) {
-        if (sm.status != RS_SEQ_OK) write_outcome(P, row, -1, -1, sm.status);
-        else if (tok < 0) write_outcome(P, row, -1, -1, RS_SEQ_UNDERFLOW);
-        else write_outcome(P, row, -1, tok, RS_SEQ_OK);
+        if (sm.status != RS_SEQ_OK) emit(-1, -1, sm.status);
+        else if (tok < 0) emit(-1, -1, RS_SEQ_UNDERFLOW);
+        else emit(-1, tok, RS_SEQ_OK);
     }
     RS_STAMP(row, 6);
 
@@ -1332,6 +1321,88 @@ __global__ void __launch_bounds__(kBlock) __attribute__((amdgpu_waves_per_eu(4))
             const float ld = internal ? widen(dg[j]) : 0.0f;
             out[j] = (float)((double)final_value(lt, ld, j) * inv_total);
         }
+    }
+}
+
+
+// One workgroup per node row; the grid is node-major: the roots of all sequences first,
+// then node 1, ... (nodes with children, whose rows take rejection passes, come early
+// in a topological numbering, so the grid ends on short rows; an order that mixes
+// sequences' rows runs 1.5x longer on a 128-tree batch because late roots form a tail).
+template <typename In, int VEC, int UNR, int MODE>
+__global__ void __launch_bounds__(kBlock) __attribute__((amdgpu_waves_per_eu(4))) rs_row_kernel(const KParams P) {
+    __shared__ Smem sm;
+    int64_t row;
+    int32_t b, n;
+    if (P.flat) {
+        row = blockIdx.x;
+        b = (int32_t)row;
+        n = 0;
+    } else {
+        const int32_t g = blockIdx.x;
+        n = g / P.B;
+        b = g - n * P.B;
+        row = (int64_t)b * P.N + n;
+    }
+    verify_row<In, VEC, UNR, MODE>(P, sm, row, b, n, [&](int32_t child, int32_t tok, int32_t st) {
+        write_outcome(P, row, child, tok, st);
+    });
+}
+
+// Path-only schedule: one workgroup per sequence walks its own tree from the root and
+// verifies only the nodes it reaches (each node's outcome depends on that node's rows
+// and uniforms alone, so the result equals the all-nodes schedule followed by the walk).
+template <typename In, int VEC, int UNR, int MODE>
+__global__ void __launch_bounds__(kBlock) __attribute__((amdgpu_waves_per_eu(4)))
+rs_path_kernel(const KParams P, int32_t max_depth, int32_t* __restrict__ out_tokens,
+               int32_t* __restrict__ out_len, int32_t* __restrict__ out_status) {
+    __shared__ Smem sm;
+    const int tid = threadIdx.x;
+    const int32_t b = blockIdx.x;
+    const int32_t N = P.N;
+    const int64_t W = (int64_t)max_depth + 1;
+    int32_t* out = out_tokens + (int64_t)b * W;
+    for (int64_t i = tid; i < W; i += kBlock) out[i] = -1;
+    int32_t n = 0, len = 0, status = RS_SEQ_OK;
+    for (int32_t steps = 0; steps <= N; ++steps) {
+        verify_row<In, VEC, UNR, MODE>(P, sm, (int64_t)b * N + n, b, n,
+                                       [&](int32_t child, int32_t tok, int32_t st) {
+            sm.res_child = child;
+            sm.res_tok = tok;
+            sm.res_status = st;
+        });
+        __syncthreads();
+        const int32_t st = sm.res_status, c = sm.res_child, t = sm.res_tok;
+        __syncthreads();   // the next row rewrites the shared state
+        if (st != RS_SEQ_OK) {
+            status = st;
+            break;
+        }
+        if (c >= 0) {
+            if (c <= n || c >= N) {
+                status = RS_SEQ_BAD_TREE;
+                break;
+            }
+            if (len >= max_depth) {
+                status = RS_SEQ_DEPTH_EXCEEDED;
+                break;
+            }
+            if (tid == 0) out[len] = P.node_token[(int64_t)b * N + c];
+            ++len;
+            n = c;
+            continue;
+        }
+        if (t >= 0 && tid == 0) out[len] = t;
+        break;
+    }
+    if (status != RS_SEQ_OK) {
+        __syncthreads();
+        for (int64_t i = tid; i < W; i += kBlock) out[i] = -1;
+        len = -1;
+    }
+    if (tid == 0) {
+        out_len[b] = len;
+        if (out_status) out_status[b] = status;
     }
 }
 
@@ -1400,30 +1471,46 @@ rs_status check_params(const rs_params* prm) {
     return RS_OK;
 }
 
+// Outputs of the path schedule (NULL: all-nodes schedule).
+struct PathOut {
+    int32_t max_depth;
+    int32_t* out_tokens;
+    int32_t* out_len;
+    int32_t* out_status;
+};
+
 template <typename In, int VEC, int UNR, int MODE>
-hipError_t launch_rows_t(KParams P, int64_t nrows, hipStream_t s) {
+hipError_t launch_rows_t(KParams P, int64_t nrows, const PathOut* path, hipStream_t s) {
     constexpr int64_t CHUNK = 64 * VEC * UNR;
     const int64_t nch = ((int64_t)P.V + CHUNK - 1) / CHUNK;
     const int64_t G = (nch + kMaxSlots - 1) / kMaxSlots;
     P.G = (int32_t)G;
     P.nslots = (int32_t)((nch + G - 1) / G);
-    hipLaunchKernelGGL((rs_row_kernel<In, VEC, UNR, MODE>), dim3((unsigned)nrows), dim3(kBlock), 0, s, P);
+    if (path) {
+        hipLaunchKernelGGL((rs_path_kernel<In, VEC, UNR, MODE>), dim3((unsigned)P.B), dim3(kBlock), 0, s,
+                           P, path->max_depth, path->out_tokens, path->out_len, path->out_status);
+    } else {
+        hipLaunchKernelGGL((rs_row_kernel<In, VEC, UNR, MODE>), dim3((unsigned)nrows), dim3(kBlock), 0, s, P);
+    }
     return hipGetLastError();
 }
 
 template <int MODE>
-hipError_t launch_rows_m(const KParams& P, int dtype, bool vec, int64_t nrows, hipStream_t s) {
+hipError_t launch_rows_m(const KParams& P, int dtype, bool vec, int64_t nrows, const PathOut* path,
+                         hipStream_t s) {
     if (dtype == RS_BF16) {
-        return vec ? launch_rows_t<uint16_t, 8, RS_UNR16, MODE>(P, nrows, s)
-                   : launch_rows_t<uint16_t, 1, 4, MODE>(P, nrows, s);
+        return vec ? launch_rows_t<uint16_t, 8, RS_UNR16, MODE>(P, nrows, path, s)
+                   : launch_rows_t<uint16_t, 1, 4, MODE>(P, nrows, path, s);
     }
-    return vec ? launch_rows_t<float, 4, RS_UNR32, MODE>(P, nrows, s)
-               : launch_rows_t<float, 1, 4, MODE>(P, nrows, s);
+    return vec ? launch_rows_t<float, 4, RS_UNR32, MODE>(P, nrows, path, s)
+               : launch_rows_t<float, 1, 4, MODE>(P, nrows, path, s);
 }
 
-hipError_t launch_rows(const KParams& P, const rs_params* prm, bool vec, int64_t nrows, hipStream_t s) {
-    if (prm->mode == RS_MODE_SPECINFER) return launch_rows_m<RS_MODE_SPECINFER>(P, prm->logits_dtype, vec, nrows, s);
-    return launch_rows_m<RS_MODE_RESISPEC>(P, prm->logits_dtype, vec, nrows, s);
+hipError_t launch_rows(const KParams& P, const rs_params* prm, bool vec, int64_t nrows, hipStream_t s,
+                       const PathOut* path = nullptr) {
+    if (prm->mode == RS_MODE_SPECINFER)
+        return launch_rows_m<RS_MODE_SPECINFER>(P, prm->logits_dtype, vec, nrows, path, s);
+    return launch_rows_m<RS_MODE_RESISPEC>(P, prm->logits_dtype, vec, nrows, path, s);
 }
 
 bool vector_ok(const void* t, const void* d, int64_t V, int dtype) {
@@ -1593,6 +1680,23 @@ rs_status resispec_verify_tree(const void* target_logits, const void* draft_logi
                      max_depth, prm, out_tokens, out_accepted_len, out_status,
                      ws_array(workspace, rows, 0), ws_array(workspace, rows, 1),
                      ws_array(workspace, rows, 2), nullptr, (hipStream_t)stream);
+}
+
+rs_status resispec_verify_tree_path(const void* target_logits, const void* draft_logits,
+                                    const int32_t* node_token, const int32_t* parent,
+                                    const float* u_accept, const float* u_resample, int32_t B,
+                                    int32_t N, int32_t V, int32_t max_depth, const rs_params* prm,
+                                    int32_t* out_tokens, int32_t* out_accepted_len,
+                                    int32_t* out_status, void* stream) {
+    const rs_status as = check_tree_args(target_logits, draft_logits, node_token, parent, u_accept,
+                                         u_resample, B, N, V, max_depth, prm, out_tokens,
+                                         out_accepted_len);
+    if (as != RS_OK || B == 0) return as;
+    const KParams P = tree_params(target_logits, draft_logits, node_token, parent, u_accept,
+                                  u_resample, B, N, V, prm, nullptr, nullptr, nullptr, nullptr);
+    const bool vec = vector_ok(target_logits, draft_logits, V, prm->logits_dtype);
+    const PathOut path{max_depth, out_tokens, out_accepted_len, out_status};
+    return launch_rows(P, prm, vec, B, (hipStream_t)stream, &path) == hipSuccess ? RS_OK : RS_ERR_HIP;
 }
 
 rs_status resispec_verify_nodes(const void* target_logits, const void* draft_logits,

@@ -21,7 +21,8 @@ RS_MAX_CANDIDATES = 64
 MODES = {"resispec": RS_MODE_RESISPEC, "specinfer": RS_MODE_SPECINFER}
 
 # Every symbol include/resispec.h declares.
-EXPORTS = ("resispec_verify", "resispec_verify_tree", "resispec_verify_nodes", "resispec_walk",
+EXPORTS = ("resispec_verify", "resispec_verify_tree", "resispec_verify_tree_path",
+           "resispec_verify_nodes", "resispec_walk",
            "resispec_workspace_bytes", "resispec_validate_tree_host",
            "resispec_verify_tree_debug", "resispec_status_string", "resispec_abi_version")
 
@@ -48,6 +49,9 @@ def _load():
     lib.resispec_verify_tree.argtypes = [P, P, P, P, P, P, i32, i32, i32, i32, prm, P, P, P,
                                          P, sz, P]
     lib.resispec_verify_tree.restype = i32
+    lib.resispec_verify_tree_path.argtypes = [P, P, P, P, P, P, i32, i32, i32, i32, prm, P, P, P,
+                                              P]
+    lib.resispec_verify_tree_path.restype = i32
     lib.resispec_verify_tree_debug.argtypes = [P, P, P, P, P, P, i32, i32, i32, i32, prm, P, P,
                                                P, P, sz, P, P, P, P, P]
     lib.resispec_verify_tree_debug.restype = i32
@@ -231,6 +235,39 @@ def resispec_verify_tree(target_logits, draft_logits, node_token, parent, u_acce
         _dev(out_accepted_len, torch.int32, "out_accepted_len"),
         _dev(out_status, torch.int32, "out_status"),
         _dev(workspace, torch.uint8, "workspace"), workspace.numel(), _stream(stream))
+    _check(st)
+    return out_tokens, out_accepted_len, out_status
+
+
+def resispec_verify_tree_path(target_logits, draft_logits, node_token, parent, u_accept,
+                              u_resample, *, temperature, max_depth, mode="resispec",
+                              without_replacement=False, bonus=True, out_tokens=None,
+                              out_accepted_len=None, out_status=None, stream=None):
+    """Path-only schedule of resispec_verify_tree (same results); returns
+    (tokens [B, max_depth+1], accepted_len [B], status [B])."""
+    import torch
+    B, N, V = _tree_common(target_logits, draft_logits, node_token, parent, u_accept, u_resample,
+                           max_depth)
+    dev = target_logits.device
+    if out_tokens is None:
+        out_tokens = torch.empty((B, max_depth + 1), dtype=torch.int32, device=dev)
+    if out_accepted_len is None:
+        out_accepted_len = torch.empty(B, dtype=torch.int32, device=dev)
+    if out_status is None:
+        out_status = torch.empty(B, dtype=torch.int32, device=dev)
+    _shape(out_tokens, (B, max_depth + 1), "out_tokens")
+    _shape(out_accepted_len, (B,), "out_accepted_len")
+    _shape(out_status, (B,), "out_status")
+    prm = _params(target_logits, temperature, mode, without_replacement, bonus)
+    st = lib.resispec_verify_tree_path(
+        _dev(target_logits, target_logits.dtype, "target_logits"),
+        _dev(draft_logits, target_logits.dtype, "draft_logits"),
+        _dev(node_token, torch.int32, "node_token"), _dev(parent, torch.int32, "parent"),
+        _dev(u_accept, torch.float32, "u_accept"), _dev(u_resample, torch.float32, "u_resample"),
+        B, N, V, int(max_depth), ctypes.byref(prm),
+        _dev(out_tokens, torch.int32, "out_tokens"),
+        _dev(out_accepted_len, torch.int32, "out_accepted_len"),
+        _dev(out_status, torch.int32, "out_status"), _stream(stream))
     _check(st)
     return out_tokens, out_accepted_len, out_status
 
