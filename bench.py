@@ -202,8 +202,25 @@ def main():
         pwall = (time.perf_counter() - t0) / args.steps
         plens = out_len.cpu().numpy()
         assert (out_st.cpu().numpy() == 0).all(), "device status not OK"
+        # rows the walks read: every node on a walk (target row; draft row too when the
+        # node has children), from the per-node outcomes of one untimed debug call
+        dbg = native.resispec_verify_tree_debug(*pargs, **kw)
+        child = dbg["node_child"].cpu().numpy()
+        par = w["parent"].cpu().numpy()
+        pbytes = 0
+        for b in range(B):
+            has_kids = np.zeros(N, dtype=bool)
+            has_kids[np.unique(par[b, 1:])] = True
+            n = 0
+            while True:
+                pbytes += V * esz * (2 if has_kids[n] else 1)
+                if child[b, n] < 0:
+                    break
+                n = child[b, n]
         path = {"ms_per_step": 1e3 * pwall, "sequences_per_s": B / pwall,
                 "rows_verified_per_step": int(plens.sum() + B),
+                "alg_bytes_per_step": int(pbytes),
+                "achieved_gbps": pbytes / pwall / 1e9,
                 "accepted_tokens_per_s": float(plens.sum()) / pwall,
                 "speedup_vs_all_nodes": results[args.mode]["ms_per_step"] / (1e3 * pwall)}
 

@@ -44,6 +44,7 @@
 
 #include <hip/hip_runtime.h>
 
+#include <atomic>
 #include <cfloat>
 #include <cmath>
 #include <cstdint>
@@ -55,8 +56,9 @@ namespace {
 #ifndef RS_BLOCK
 #define RS_BLOCK 512
 #endif
-constexpr int kBlock = RS_BLOCK;
-constexpr int kWaves = kBlock / 64;
+constexpr int kBlock = RS_BLOCK;          // threads per row workgroup (all-nodes schedule)
+constexpr int kBlockWide = 1024;         // path schedule with few sequences: one workgroup per CU
+constexpr int kMaxWaves = kBlockWide / 64;
 constexpr int kMaxCand = RS_MAX_CANDIDATES;
 #ifndef RS_MAX_SLOTS
 #define RS_MAX_SLOTS 128
@@ -262,8 +264,8 @@ struct Smem {
     int32_t nc;           // rows with more nodes than threads only
     float ur;
     double St, Sd;        // sums of exp2(l c2 + K)
-    int32_t wcount[kWaves];
-    int32_t wbad[kWaves];
+    int32_t wcount[kMaxWaves];
+    int32_t wbad[kMaxWaves];
     int32_t cand_tok[kMaxCand];
     int32_t cand_node[kMaxCand];
     float cand_u[kMaxCand];
@@ -299,7 +301,7 @@ struct Smem {
     double slotA[kMaxSlots];
     double slotB[kMaxSlots];
     double slotT[kMaxSlots];
-    float wmax[2][kWaves];
+    float wmax[2][kMaxWaves];
     // draw
     int32_t token;
     double total;
@@ -377,7 +379,7 @@ __device__ __forceinline__ void write_outcome(const KParams& P, int64_t row, int
 __device__ void zero_residual_row(const KParams& P, int64_t row) {
     if (!P.residual_out) return;
     float* out = P.residual_out + row * P.V;
-    for (int j = threadIdx.x; j < P.V; j += kBlock) out[j] = 0.0f;
+    for (int j = threadIdx.x; j < P.V; j += blockDim.x) out[j] = 0.0f;
 }
 
 // Rejection-step terms of one element (exact token comparisons), given its target
@@ -553,9 +555,11 @@ __device__ __forceinline__ void wave_sweep(const In* __restrict__ tg, const In* 
 // Verification of one node row by the whole workgroup: node n of sequence b (row
 // b * N + n; flat rows: b = row, n = 0).  emit(child, token, status) is called by
 // thread 0 once, with the node's outcome.
-template <typename In, int VEC, int UNR, int MODE, typename Emit>
+template <typename In, int VEC, int UNR, int MODE, int BLK, typename Emit>
 __device__ __forceinline__ void verify_row(const KParams& P, Smem& sm, const int64_t row,
                                            const int32_t b, const int32_t n, Emit&& emit) {
+    constexpr int kBlock = BLK;
+    constexpr int kWaves = BLK / 64;
     const int tid = threadIdx.x;
     const int lane = tid & 63;
     const int wid = tid >> 6;
@@ -1344,7 +1348,7 @@ __global__ void __launch_bounds__(kBlock) __attribute__((amdgpu_waves_per_eu(4))
         b = g - n * P.B;
         row = (int64_t)b * P.N + n;
     }
-    verify_row<In, VEC, UNR, MODE>(P, sm, row, b, n, [&](int32_t child, int32_t tok, int32_t st) {
+    verify_row<In, VEC, UNR, MODE, kBlock>(P, sm, row, b, n, [&](int32_t child, int32_t tok, int32_t st) {
         write_outcome(P, row, child, tok, st);
     });
 }
@@ -1352,10 +1356,11 @@ __global__ void __launch_bounds__(kBlock) __attribute__((amdgpu_waves_per_eu(4))
 // Path-only schedule: one workgroup per sequence walks its own tree from the root and
 // verifies only the nodes it reaches (each node's outcome depends on that node's rows
 // and uniforms alone, so the result equals the all-nodes schedule followed by the walk).
-template <typename In, int VEC, int UNR, int MODE>
-__global__ void __launch_bounds__(kBlock) __attribute__((amdgpu_waves_per_eu(4)))
+template <typename In, int VEC, int UNR, int MODE, int BLK>
+__global__ void __launch_bounds__(BLK) __attribute__((amdgpu_waves_per_eu(4)))
 rs_path_kernel(const KParams P, int32_t max_depth, int32_t* __restrict__ out_tokens,
                int32_t* __restrict__ out_len, int32_t* __restrict__ out_status) {
+    constexpr int kBlock = BLK;
     __shared__ Smem sm;
     const int tid = threadIdx.x;
     const int32_t b = blockIdx.x;
@@ -1365,7 +1370,7 @@ rs_path_kernel(const KParams P, int32_t max_depth, int32_t* __restrict__ out_tok
     for (int64_t i = tid; i < W; i += kBlock) out[i] = -1;
     int32_t n = 0, len = 0, status = RS_SEQ_OK;
     for (int32_t steps = 0; steps <= N; ++steps) {
-        verify_row<In, VEC, UNR, MODE>(P, sm, (int64_t)b * N + n, b, n,
+        verify_row<In, VEC, UNR, MODE, BLK>(P, sm, (int64_t)b * N + n, b, n,
                                        [&](int32_t child, int32_t tok, int32_t st) {
             sm.res_child = child;
             sm.res_tok = tok;
@@ -1463,6 +1468,20 @@ constexpr int kWalkBlock = 256;
 
 bool aligned16(const void* p) { return (reinterpret_cast<uintptr_t>(p) & 15u) == 0; }
 
+// compute units of the current device (queried once per device)
+int cu_count() {
+    static std::atomic<int> cache[64];
+    int dev = 0;
+    if (hipGetDevice(&dev) != hipSuccess || dev < 0 || dev >= 64) return 256;
+    int n = cache[dev].load(std::memory_order_relaxed);
+    if (n <= 0) {
+        if (hipDeviceGetAttribute(&n, hipDeviceAttributeMultiprocessorCount, dev) != hipSuccess || n <= 0)
+            n = 256;
+        cache[dev].store(n, std::memory_order_relaxed);
+    }
+    return n;
+}
+
 rs_status check_params(const rs_params* prm) {
     if (!prm) return RS_ERR_INVALID_ARG;
     if (prm->mode != RS_MODE_RESISPEC && prm->mode != RS_MODE_SPECINFER) return RS_ERR_INVALID_ARG;
@@ -1473,6 +1492,7 @@ rs_status check_params(const rs_params* prm) {
 
 // Outputs of the path schedule (NULL: all-nodes schedule).
 struct PathOut {
+    int wide;            // 1024-thread workgroups (few sequences: one per CU)
     int32_t max_depth;
     int32_t* out_tokens;
     int32_t* out_len;
@@ -1486,9 +1506,14 @@ hipError_t launch_rows_t(KParams P, int64_t nrows, const PathOut* path, hipStrea
     const int64_t G = (nch + kMaxSlots - 1) / kMaxSlots;
     P.G = (int32_t)G;
     P.nslots = (int32_t)((nch + G - 1) / G);
-    if (path) {
-        hipLaunchKernelGGL((rs_path_kernel<In, VEC, UNR, MODE>), dim3((unsigned)P.B), dim3(kBlock), 0, s,
-                           P, path->max_depth, path->out_tokens, path->out_len, path->out_status);
+    if (path && path->wide) {
+        hipLaunchKernelGGL((rs_path_kernel<In, VEC, UNR, MODE, kBlockWide>), dim3((unsigned)P.B),
+                           dim3(kBlockWide), 0, s, P, path->max_depth, path->out_tokens,
+                           path->out_len, path->out_status);
+    } else if (path) {
+        hipLaunchKernelGGL((rs_path_kernel<In, VEC, UNR, MODE, kBlock>), dim3((unsigned)P.B),
+                           dim3(kBlock), 0, s, P, path->max_depth, path->out_tokens, path->out_len,
+                           path->out_status);
     } else {
         hipLaunchKernelGGL((rs_row_kernel<In, VEC, UNR, MODE>), dim3((unsigned)nrows), dim3(kBlock), 0, s, P);
     }
@@ -1695,7 +1720,9 @@ rs_status resispec_verify_tree_path(const void* target_logits, const void* draft
     const KParams P = tree_params(target_logits, draft_logits, node_token, parent, u_accept,
                                   u_resample, B, N, V, prm, nullptr, nullptr, nullptr, nullptr);
     const bool vec = vector_ok(target_logits, draft_logits, V, prm->logits_dtype);
-    const PathOut path{max_depth, out_tokens, out_accepted_len, out_status};
+    // with fewer sequences than two per CU, give each sequence a whole CU
+    const PathOut path{B < 2 * cu_count() ? 1 : 0, max_depth, out_tokens, out_accepted_len,
+                       out_status};
     return launch_rows(P, prm, vec, B, (hipStream_t)stream, &path) == hipSuccess ? RS_OK : RS_ERR_HIP;
 }
 
