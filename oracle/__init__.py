@@ -68,9 +68,19 @@ def _load():
                                         i32, i32, i32, P, P, P, P]
     lib.or_verify_tree_nodes.argtypes = [P, P, i32, P, P, P, P, i32, i32, i64, f32,
                                          i32, i32, i32, P, i64, P, P, P, P, P, P]
+    u32, u64 = ctypes.c_uint32, ctypes.c_uint64
+    lib.or_philox4x32_10.argtypes = [P, P, P]
+    lib.or_philox4x32_10.restype = None
+    lib.or_u01.argtypes = [u32]
+    lib.or_u01.restype = f32
+    lib.or_node_uniforms.argtypes = [u64, u64, i32, i32, P, P, P]
+    lib.or_node_uniforms.restype = None
+    lib.or_sample_candidates.argtypes = [P, i32, i64, f32, i32, i32, P, P, P]
+    lib.or_draft_tree.argtypes = [P, i32, P, i32, i32, i64, f32, i32, u64, u64, P, P, P, P, P]
     for name in ("or_softmax", "or_get_proxy", "or_residual_update", "or_draft_remove",
                  "or_invcdf", "or_verify_node", "or_verify_node_batch", "or_enumerate",
-                 "or_verify_tree_walk", "or_verify_tree_nodes"):
+                 "or_verify_tree_walk", "or_verify_tree_nodes", "or_sample_candidates",
+                 "or_draft_tree"):
         getattr(lib, name).restype = i32
     _lib = lib
     return lib
@@ -241,3 +251,54 @@ def verify_tree_nodes(target, draft, node_token, parent, u_accept, u_resample, r
     if want_residual:
         out["final_R"] = fr
     return out
+
+
+# ------------------------------------------------------------------ draft step ----
+
+def philox4x32_10(counter, key):
+    """Philox4x32-10 of a 4-word counter under a 2-word key -> 4 uint32 words."""
+    c = np.ascontiguousarray(counter, dtype=np.uint32)
+    k = np.ascontiguousarray(key, dtype=np.uint32)
+    out = np.empty(4, dtype=np.uint32)
+    _load().or_philox4x32_10(_ptr(c), _ptr(k), _ptr(out))
+    return out
+
+
+def u01(word):
+    return _load().or_u01(int(word))
+
+
+def node_uniforms(seed, offset, b, n):
+    """(u_accept, u_resample, u_cand) of node n of sequence b."""
+    ua, ur, uc = ctypes.c_float(), ctypes.c_float(), ctypes.c_float()
+    _load().or_node_uniforms(int(seed), int(offset), int(b), int(n), ctypes.byref(ua),
+                             ctypes.byref(ur), ctypes.byref(uc))
+    return ua.value, ur.value, uc.value
+
+
+def sample_candidates(draft_row, k, uc, *, temperature, without_replacement=False):
+    a, dt = _logits(draft_row)
+    uc = np.ascontiguousarray(uc, dtype=np.float32)
+    tok = np.empty(k, dtype=np.int32)
+    mg = np.empty(k, dtype=np.float64)
+    st = _load().or_sample_candidates(_ptr(a), dt, a.shape[-1], float(temperature), int(k),
+                                      int(bool(without_replacement)), _ptr(uc), _ptr(tok), _ptr(mg))
+    return tok, mg, st
+
+
+def draft_tree(draft, parent, *, temperature, without_replacement=False, seed=0, offset=0):
+    """The draft step of a tree batch: node_token, u_accept, u_resample, flagged, margin
+    (all [B, N]) and the status (OK or BAD_TREE)."""
+    d, dt = _logits(draft)
+    par = np.ascontiguousarray(parent, dtype=np.int32)
+    B, N, V = d.shape
+    tok = np.empty((B, N), dtype=np.int32)
+    ua = np.empty((B, N), dtype=np.float32)
+    ur = np.empty((B, N), dtype=np.float32)
+    fl = np.empty((B, N), dtype=np.int32)
+    mg = np.empty((B, N), dtype=np.float64)
+    st = _load().or_draft_tree(_ptr(d), dt, _ptr(par), B, N, V, float(temperature),
+                               int(bool(without_replacement)), int(seed), int(offset), _ptr(tok),
+                               _ptr(ua), _ptr(ur), _ptr(fl), _ptr(mg))
+    return {"node_token": tok, "u_accept": ua, "u_resample": ur, "flagged": fl, "margin": mg,
+            "status": st}

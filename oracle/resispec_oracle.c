@@ -494,3 +494,117 @@ int32_t or_verify_tree_nodes(const void* target, const void* draft, int32_t dtyp
     free(p); free(q); free(kids); free(cand); free(ua);
     return rc;
 }
+
+/* ------------------------------------------------------------------------------------
+ * The draft step: Philox4x32-10 uniforms and candidate draws.
+ * ---------------------------------------------------------------------------------- */
+
+void or_philox4x32_10(const uint32_t ctr[4], const uint32_t key[2], uint32_t out[4]) {
+    uint32_t c0 = ctr[0], c1 = ctr[1], c2 = ctr[2], c3 = ctr[3];
+    uint32_t k0 = key[0], k1 = key[1];
+    for (int round = 0; round < 10; ++round) {
+        if (round > 0) {              /* key schedule: add the Weyl constants */
+            k0 += 0x9E3779B9u;
+            k1 += 0xBB67AE85u;
+        }
+        const uint64_t p0 = (uint64_t)0xD2511F53u * (uint64_t)c0;
+        const uint64_t p1 = (uint64_t)0xCD9E8D57u * (uint64_t)c2;
+        const uint32_t hi0 = (uint32_t)(p0 >> 32), lo0 = (uint32_t)p0;
+        const uint32_t hi1 = (uint32_t)(p1 >> 32), lo1 = (uint32_t)p1;
+        c0 = hi1 ^ c1 ^ k0;
+        c1 = lo1;
+        c2 = hi0 ^ c3 ^ k1;
+        c3 = lo0;
+    }
+    out[0] = c0; out[1] = c1; out[2] = c2; out[3] = c3;
+}
+
+float or_u01(uint32_t w) { return (float)(w >> 8) * (1.0f / 16777216.0f); }
+
+void or_node_uniforms(uint64_t seed, uint64_t offset, int32_t b, int32_t n, float* ua,
+                      float* ur, float* uc) {
+    const uint32_t ctr[4] = {(uint32_t)n, (uint32_t)b, (uint32_t)offset, (uint32_t)(offset >> 32)};
+    const uint32_t key[2] = {(uint32_t)seed, (uint32_t)(seed >> 32)};
+    uint32_t w[4];
+    or_philox4x32_10(ctr, key, w);
+    if (ua) *ua = or_u01(w[0]);
+    if (ur) *ur = or_u01(w[1]);
+    if (uc) *uc = or_u01(w[2]);
+}
+
+int32_t or_sample_candidates(const void* draft, int32_t dtype, int64_t V, float temperature,
+                             int32_t k, int32_t without_replacement, const float* uc,
+                             int32_t* tokens, double* margins) {
+    if (!draft || V <= 0 || k < 0 || (k > 0 && (!uc || !tokens || !margins))) return OR_BAD_ARG;
+    double* D = (double*)malloc((size_t)V * sizeof(double));
+    if (!D) return OR_BAD_ARG;
+    int32_t st = or_softmax(draft, dtype, V, temperature, D);
+    for (int32_t i = 0; i < k; ++i) {
+        tokens[i] = -1;
+        margins[i] = 0.0;
+    }
+    if (st == OR_OK) {
+        for (int32_t i = 0; i < k; ++i) {
+            int32_t tok = -1;
+            double margin = 0.0;
+            st = or_invcdf(D, V, (double)uc[i], &tok, &margin);
+            if (st != OR_OK) break;
+            tokens[i] = tok;
+            margins[i] = margin;
+            if (without_replacement && i + 1 < k) {
+                st = or_draft_remove(D, V, tok);
+                if (st != OR_OK) break;
+            }
+        }
+    }
+    free(D);
+    return st;
+}
+
+int32_t or_draft_tree(const void* draft, int32_t dtype, const int32_t* parent, int32_t B,
+                      int32_t N, int64_t V, float temperature, int32_t without_replacement,
+                      uint64_t seed, uint64_t offset, int32_t* node_token, float* u_accept,
+                      float* u_resample, int32_t* flagged, double* margin) {
+    if (!draft || !parent || !node_token || !u_accept || !u_resample || !flagged || !margin ||
+        B < 0 || N <= 0 || V <= 0)
+        return OR_BAD_ARG;
+    int32_t* kids = (int32_t*)malloc((size_t)N * sizeof(int32_t));
+    int32_t* toks = (int32_t*)malloc((size_t)N * sizeof(int32_t));
+    float* uc = (float*)malloc((size_t)N * sizeof(float));
+    double* mg = (double*)malloc((size_t)N * sizeof(double));
+    if (!kids || !toks || !uc || !mg) {
+        free(kids); free(toks); free(uc); free(mg);
+        return OR_BAD_ARG;
+    }
+    int32_t status = OR_OK;
+    for (int32_t b = 0; b < B; ++b) {
+        const int32_t* par = parent + (int64_t)b * N;
+        int32_t* nt = node_token + (int64_t)b * N;
+        for (int32_t n = 0; n < N; ++n) {
+            or_node_uniforms(seed, offset, b, n, &u_accept[(int64_t)b * N + n],
+                             &u_resample[(int64_t)b * N + n], NULL);
+            nt[n] = -1;
+            flagged[(int64_t)b * N + n] = 0;
+            margin[(int64_t)b * N + n] = 1e300;
+        }
+        if (!tree_is_valid(par, N)) {
+            status = OR_BAD_TREE;
+            continue;
+        }
+        for (int32_t n = 0; n < N; ++n) {
+            const int32_t k = children_of(par, N, n, kids);
+            if (k == 0) continue;
+            for (int32_t i = 0; i < k; ++i) or_node_uniforms(seed, offset, b, kids[i], NULL, NULL, &uc[i]);
+            const void* row = row_ptr(draft, dtype, (int64_t)b * N + n, V);
+            const int32_t st = or_sample_candidates(row, dtype, V, temperature, k, without_replacement,
+                                                    uc, toks, mg);
+            for (int32_t i = 0; i < k; ++i) {
+                nt[kids[i]] = (st == OR_OK) ? toks[i] : -1;
+                margin[(int64_t)b * N + kids[i]] = mg[i];
+                flagged[(int64_t)b * N + kids[i]] = (st == OR_OK && mg[i] < OR_FLAG_WINDOW) ? 1 : 0;
+            }
+        }
+    }
+    free(kids); free(toks); free(uc); free(mg);
+    return status;
+}

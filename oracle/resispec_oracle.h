@@ -138,6 +138,42 @@ int32_t or_verify_tree_nodes(const void* target, const void* draft, int32_t dtyp
                              int32_t* out_flagged, double* out_margin /* n_rows or NULL */,
                              double* out_final_R /* n_rows*V or NULL */);
 
+/* ---- the draft step: uniforms and candidate draws (run before verification) ---- */
+
+/* Philox4x32-10 (Salmon, Moraes, Dror and Shaw, "Parallel random numbers: as easy as
+ * 1, 2, 3", SC'11): ten rounds over the 4-word counter, each round two 32x32->64
+ * multiplications and xors with the 2-word key, the key advanced by the Weyl
+ * constants between rounds. */
+void or_philox4x32_10(const uint32_t ctr[4], const uint32_t key[2], uint32_t out[4]);
+
+/* Uniform in [0, 1) from a 32-bit word: its top 24 bits times 2^-24 (exact in fp32). */
+float or_u01(uint32_t w);
+
+/* The uniforms of node n of sequence b: Philox4x32-10 of counter
+ * (n, b, offset low word, offset high word) under key (seed low word, seed high word);
+ * word 0 -> u_accept, word 1 -> u_resample, word 2 -> uc, the uniform that draws node
+ * n's own token from its parent's draft distribution. */
+void or_node_uniforms(uint64_t seed, uint64_t offset, int32_t b, int32_t n, float* ua,
+                      float* ur, float* uc);
+
+/* k candidates from D = softmax(draft / T): candidate i is the inverse-CDF draw
+ * (or_invcdf) of D with uniform uc[i]; without replacement D loses the drawn token and
+ * is renormalised (or_draft_remove) before the next draw.  tokens[k], margins[k]. */
+int32_t or_sample_candidates(const void* draft, int32_t dtype, int64_t V, float temperature,
+                             int32_t k, int32_t without_replacement, const float* uc,
+                             int32_t* tokens, double* margins);
+
+/* The draft step of a tree batch: for every node with children, its children's
+ * tokens drawn from its draft row (children in ascending node index), and every
+ * node's u_accept / u_resample.  node_token[.,0] = -1.  flagged[b][n] = 1 when node
+ * n's draw margin is below OR_FLAG_WINDOW; margin[b][n] the margin (1e300 for the
+ * root).  Returns OR_BAD_TREE for a malformed parent array, else OR_OK (per-row
+ * underflow leaves that row's children at -1). */
+int32_t or_draft_tree(const void* draft, int32_t dtype, const int32_t* parent, int32_t B,
+                      int32_t N, int64_t V, float temperature, int32_t without_replacement,
+                      uint64_t seed, uint64_t offset, int32_t* node_token, float* u_accept,
+                      float* u_resample, int32_t* flagged, double* margin);
+
 #ifdef __cplusplus
 }
 #endif
