@@ -70,11 +70,11 @@ def test_sampler_brute_force(worep):
         assert st == O.OK
         D = _softmax(l, T)
         for i in range(k):
-            if mg[i] < 1e-9:
-                continue
             x = _invcdf(D, float(uc[i]))
-            assert tok[i] == x
-            if worep:
+            if mg[i] >= 1e-9:      # rounding-level margins may fall either way
+                assert tok[i] == x
+            x = int(tok[i])
+            if worep and i + 1 < k:
                 D = D.copy()
                 D[x] = 0.0
                 D /= D.sum()
