@@ -154,6 +154,32 @@ rs_status resispec_verify_tree_path(const void* target_logits, const void* draft
                                     int32_t* out_accepted_len, int32_t* out_status, void* stream);
 
 /*
+ * The draft step that precedes verification (Preliminary: candidates are drawn from the
+ * draft distribution; Algorithm 1 draws x_i ~ D and r_i ~ Uniform(0, 1)), on the device:
+ *   - every node's uniforms: Philox4x32-10 (Salmon, Moraes, Dror and Shaw, SC'11) of
+ *     counter (n, b, offset low word, offset high word) under key (seed low word, seed
+ *     high word); word 0 -> u_accept[b][n], word 1 -> u_resample[b][n], word 2 -> the
+ *     uniform that draws node n's own token; a word w maps to (w >> 8) * 2^-24;
+ *   - every node's children's tokens, drawn from softmax(draft[b][n] / T) by inverse CDF
+ *     in ascending vocabulary order, children in ascending node index; with
+ *     prm->without_replacement each draw removes its token (and renormalises) before the
+ *     next.
+ *   draft_logits : [B][N][V] (prm->logits_dtype); draft rows of leaves are not read
+ *   parent       : [B][N] int32, as for resispec_verify_tree
+ *   node_token   : [B][N] int32 out; entry 0 = -1.  A node whose draft row has no usable
+ *                  mass, or which has more than RS_MAX_CANDIDATES children, leaves its
+ *                  children at -1; a malformed tree sets every entry of the sequence to -1.
+ *   u_accept, u_resample : [B][N] fp32 out
+ *   out_status   : [B] int32 out (RS_SEQ_OK or RS_SEQ_BAD_TREE), may be NULL
+ * prm->mode and prm->bonus are ignored.  The outputs feed resispec_verify_tree directly.
+ */
+rs_status resispec_draft_candidates(const void* draft_logits, const int32_t* parent,
+                                    int32_t B, int32_t N, int32_t V, const rs_params* prm,
+                                    uint64_t seed, uint64_t offset, int32_t* node_token,
+                                    float* u_accept, float* u_resample, int32_t* out_status,
+                                    void* stream);
+
+/*
  * The two stages of resispec_verify_tree, for callers that schedule them separately
  * (same kernels, same results):
  *   resispec_verify_nodes: every node's own outcome (accepted child or drawn token) into

@@ -22,6 +22,7 @@ MODES = {"resispec": RS_MODE_RESISPEC, "specinfer": RS_MODE_SPECINFER}
 
 # Every symbol include/resispec.h declares.
 EXPORTS = ("resispec_verify", "resispec_verify_tree", "resispec_verify_tree_path",
+           "resispec_draft_candidates",
            "resispec_verify_nodes", "resispec_walk",
            "resispec_workspace_bytes", "resispec_validate_tree_host",
            "resispec_verify_tree_debug", "resispec_status_string", "resispec_abi_version")
@@ -52,6 +53,9 @@ def _load():
     lib.resispec_verify_tree_path.argtypes = [P, P, P, P, P, P, i32, i32, i32, i32, prm, P, P, P,
                                               P]
     lib.resispec_verify_tree_path.restype = i32
+    lib.resispec_draft_candidates.argtypes = [P, P, i32, i32, i32, prm, ctypes.c_uint64,
+                                              ctypes.c_uint64, P, P, P, P, P]
+    lib.resispec_draft_candidates.restype = i32
     lib.resispec_verify_tree_debug.argtypes = [P, P, P, P, P, P, i32, i32, i32, i32, prm, P, P,
                                                P, P, sz, P, P, P, P, P]
     lib.resispec_verify_tree_debug.restype = i32
@@ -270,6 +274,41 @@ def resispec_verify_tree_path(target_logits, draft_logits, node_token, parent, u
         _dev(out_status, torch.int32, "out_status"), _stream(stream))
     _check(st)
     return out_tokens, out_accepted_len, out_status
+
+
+def resispec_draft_candidates(draft_logits, parent, *, temperature, without_replacement=False,
+                              seed=0, offset=0, node_token=None, u_accept=None, u_resample=None,
+                              out_status=None, stream=None):
+    """The draft step on the device: children's candidate tokens drawn from each node's
+    draft row, and every node's uniforms (Philox4x32-10 under seed / offset).
+    Returns (node_token [B, N], u_accept [B, N], u_resample [B, N], status [B])."""
+    import torch
+    if draft_logits.dim() != 3:
+        raise ValueError("draft_logits must be [B, N, V]")
+    B, N, V = draft_logits.shape
+    _shape(parent, (B, N), "parent")
+    dev = draft_logits.device
+    _same_device(draft_logits, parent, node_token, u_accept, u_resample, out_status)
+    if node_token is None:
+        node_token = torch.empty((B, N), dtype=torch.int32, device=dev)
+    if u_accept is None:
+        u_accept = torch.empty((B, N), dtype=torch.float32, device=dev)
+    if u_resample is None:
+        u_resample = torch.empty((B, N), dtype=torch.float32, device=dev)
+    if out_status is None:
+        out_status = torch.empty(B, dtype=torch.int32, device=dev)
+    for t, nm in ((node_token, "node_token"), (u_accept, "u_accept"), (u_resample, "u_resample")):
+        _shape(t, (B, N), nm)
+    _shape(out_status, (B,), "out_status")
+    prm = _params(draft_logits, temperature, "resispec", without_replacement, False)
+    st = lib.resispec_draft_candidates(
+        _dev(draft_logits, draft_logits.dtype, "draft_logits"), _dev(parent, torch.int32, "parent"),
+        B, N, V, ctypes.byref(prm), int(seed) & 0xFFFFFFFFFFFFFFFF, int(offset) & 0xFFFFFFFFFFFFFFFF,
+        _dev(node_token, torch.int32, "node_token"), _dev(u_accept, torch.float32, "u_accept"),
+        _dev(u_resample, torch.float32, "u_resample"), _dev(out_status, torch.int32, "out_status"),
+        _stream(stream))
+    _check(st)
+    return node_token, u_accept, u_resample, out_status
 
 
 def resispec_verify_nodes(target_logits, draft_logits, node_token, parent, u_accept, u_resample,

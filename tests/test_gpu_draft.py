@@ -1,0 +1,158 @@
+"""The draft step on the device (resispec_draft_candidates) against the oracle's
+draft step: uniforms bit-exact (Philox4x32-10 integers), candidate tokens exact on
+every draw whose oracle margin is outside the 1e-6 window, statuses exact; then the
+device draft feeding the device verification equals the oracle chain end to end."""
+import numpy as np
+import pytest
+import torch
+
+import oracle as O
+from paper_2608_24411_amd import synth
+from parity_util import compare_walk, gpu_tree, oracle_walk
+
+pytestmark = pytest.mark.gpu
+
+
+def _log(*a):
+    print(*a, flush=True)
+
+
+def gpu_draft(native, w, seed, offset, worep=None):
+    wr = w["without_replacement"] if worep is None else worep
+    tok, ua, ur, st = native.resispec_draft_candidates(
+        w["draft"], w["parent"], temperature=w["temperature"], without_replacement=wr,
+        seed=seed, offset=offset)
+    torch.cuda.synchronize()
+    return {"node_token": tok.cpu().numpy(), "u_accept": ua.cpu().numpy(),
+            "u_resample": ur.cpu().numpy(), "status": st.cpu().numpy()}
+
+
+def oracle_draft(w, seed, offset, worep=None):
+    wr = w["without_replacement"] if worep is None else worep
+    return O.draft_tree(synth.to_host(w["draft"]), synth.to_host(w["parent"]),
+                        temperature=w["temperature"], without_replacement=wr, seed=seed,
+                        offset=offset)
+
+
+def compare_draft(g, o):
+    assert np.array_equal(g["u_accept"], o["u_accept"])
+    assert np.array_equal(g["u_resample"], o["u_resample"])
+    keep = o["flagged"] == 0
+    bad = np.argwhere(keep & (g["node_token"] != o["node_token"]))
+    assert bad.size == 0, (bad[:5], g["node_token"][tuple(bad[:5].T)], o["node_token"][tuple(bad[:5].T)])
+    return int(keep.sum()), int((~keep).sum())
+
+
+CASES = [(1, dict(B=6)), (2, dict(B=4)), (3, dict(B=3)), (4, dict(B=6)),
+         (2, dict(B=2, V=100003, dtype="f32")), (4, dict(B=3, V=4099)),
+         (3, dict(B=2, V=65537, dtype="bf16"))]
+
+
+@pytest.mark.parametrize("cfg,over", CASES, ids=[f"cfg{c}-{o}" for c, o in CASES])
+@pytest.mark.parametrize("worep", [False, True])
+def test_draft_parity(gpu_lib, cfg, over, worep):
+    _log("draft parity", cfg, over, worep)
+    w = synth.make_workload(cfg, device="cuda", **over)
+    seed, offset = 24411 + cfg, 7
+    g = gpu_draft(gpu_lib, w, seed, offset, worep)
+    o = oracle_draft(w, seed, offset, worep)
+    n_cmp, n_flag = compare_draft(g, o)
+    _log("  tokens compared", n_cmp, "flagged", n_flag)
+    assert (g["status"] == 0).all() and o["status"] == O.OK
+    assert (g["node_token"][:, 0] == -1).all()
+    if worep:   # siblings are distinct
+        par = synth.to_host(w["parent"])
+        for b in range(par.shape[0]):
+            for n in range(par.shape[1]):
+                kids = np.flatnonzero(par[b] == n)
+                t = g["node_token"][b, kids]
+                assert len(set(t.tolist())) == len(t)
+
+
+@pytest.mark.parametrize("cfg", [2, 4])
+def test_draft_full_size(gpu_lib, cfg):
+    """Full configurations: uniforms bit-exact everywhere; tokens of a sample of sequences
+    against the oracle."""
+    w = synth.make_workload(cfg, device="cuda")
+    g = gpu_draft(gpu_lib, w, 5, 0)
+    rng = np.random.default_rng(cfg)
+    seqs = np.sort(rng.choice(w["B"], size=4, replace=False))
+    sub = dict(w)
+    sub["draft"] = w["draft"][torch.as_tensor(seqs, device="cuda")]
+    sub["parent"] = w["parent"][torch.as_tensor(seqs, device="cuda")]
+    o = oracle_draft(sub, 5, 0)
+    # the oracle numbers sequences 0..3 of the sample; the device numbers them by b
+    for i, b in enumerate(seqs):
+        ua, ur, _ = O.node_uniforms(5, 0, int(b), 3)
+        assert g["u_accept"][b, 3] == np.float32(ua) and g["u_resample"][b, 3] == np.float32(ur)
+    B, N = w["B"], w["N"]
+    # uniforms of every node from the oracle's generator
+    for b in range(0, B, max(1, B // 16)):
+        for n in range(N):
+            ua, ur, _ = O.node_uniforms(5, 0, b, n)
+            assert g["u_accept"][b, n] == np.float32(ua) and g["u_resample"][b, n] == np.float32(ur)
+    # tokens: the sampled sequences, drawn with the device's sequence index b
+    par = synth.to_host(w["parent"])
+    for b in seqs:
+        for n in range(N):
+            kids = np.flatnonzero(par[b] == n)
+            if kids.size == 0:
+                continue
+            uc = np.array([O.node_uniforms(5, 0, int(b), int(m))[2] for m in kids], dtype=np.float32)
+            tok, mg, st = O.sample_candidates(synth.to_host(w["draft"][b, n]), kids.size, uc,
+                                              temperature=w["temperature"],
+                                              without_replacement=w["without_replacement"])
+            assert st == O.OK
+            ok = mg >= 1e-6
+            assert (g["node_token"][b, kids][ok] == tok[ok]).all(), (b, n)
+    del o
+
+
+def test_draft_edges(gpu_lib):
+    """A malformed tree (every token -1, status BAD_TREE), a draft row with no mass
+    (-inf everywhere: its children stay -1), more than RS_MAX_CANDIDATES children, B = 0."""
+    w = synth.make_workload(1, device="cuda", B=4, V=3001)
+    w["parent"][1, 7] = 9
+    w["draft"][2, 0] = float("-inf")
+    g = gpu_draft(gpu_lib, w, 3, 1)
+    assert g["status"][1] == 4 and (g["node_token"][1] == -1).all()
+    par = synth.to_host(w["parent"])
+    assert (g["node_token"][2, np.flatnonzero(par[2] == 0)] == -1).all()
+    o = oracle_draft(w, 3, 1)
+    keep = (o["flagged"] == 0)
+    keep[1] = False          # the oracle leaves a malformed sequence at -1 as well
+    assert (g["node_token"][keep] == o["node_token"][keep]).all()
+    assert (o["node_token"][1] == -1).all()
+    # 65 children of the root: none drawn
+    N, V = 66, 2048
+    t = torch.randn((2, N, V), device="cuda")
+    parent = torch.zeros((2, N), dtype=torch.int32, device="cuda")
+    parent[:, 0] = -1
+    tok, ua, ur, st = gpu_lib.resispec_draft_candidates(t, parent, temperature=1.0)
+    torch.cuda.synchronize()
+    assert (tok.cpu().numpy() == -1).all()
+    e = gpu_lib.resispec_draft_candidates(t[:0], parent[:0], temperature=1.0)
+    assert e[0].numel() == 0
+
+
+@pytest.mark.parametrize("cfg", [1, 2, 4])
+def test_draft_then_verify(gpu_lib, cfg):
+    """Device draft feeding device verification equals the oracle's draft feeding the
+    oracle's verification (sequences with a flagged draw are left out)."""
+    w = synth.make_workload(cfg, device="cuda", B=6)
+    g = gpu_draft(gpu_lib, w, 99, 3)
+    o = oracle_draft(w, 99, 3)
+    w2 = dict(w)
+    w2["node_token"] = torch.as_tensor(g["node_token"], device="cuda")
+    w2["u_accept"] = torch.as_tensor(g["u_accept"], device="cuda")
+    w2["u_resample"] = torch.as_tensor(g["u_resample"], device="cuda")
+    for mode in ("resispec", "specinfer"):
+        gpu = gpu_tree(gpu_lib, w2, mode)
+        h = {"target": synth.to_host(w["target"]), "draft": synth.to_host(w["draft"]),
+             "node_token": o["node_token"].copy(), "parent": synth.to_host(w["parent"]),
+             "u_accept": o["u_accept"], "u_resample": o["u_resample"]}
+        h["node_token"][:, 0] = 0
+        orc = oracle_walk(h, w, mode)
+        clean = (o["flagged"] == 0).all(axis=1)
+        orc["flagged"] = orc["flagged"] | ~clean
+        compare_walk(gpu, orc)
