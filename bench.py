@@ -120,6 +120,7 @@ def main():
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--no-other-mode", action="store_true")
     ap.add_argument("--no-path", action="store_true", help="skip the path-only schedule")
+    ap.add_argument("--no-draft", action="store_true", help="skip the draft step")
     ap.add_argument("--copy-probe", type=int, default=0, metavar="MIB",
                     help="only run a plain device copy of MIB MiB (counter calibration)")
     args = ap.parse_args()
@@ -224,6 +225,43 @@ def main():
                 "accepted_tokens_per_s": float(plens.sum()) / pwall,
                 "speedup_vs_all_nodes": results[args.mode]["ms_per_step"] / (1e3 * pwall)}
 
+    # the draft step that precedes verification (candidates and uniforms on the device)
+    draft = None
+    if not args.no_draft:
+        dkw = dict(temperature=w["temperature"], without_replacement=w["without_replacement"],
+                   seed=24411)
+        d_tok = torch.empty((B, N), dtype=torch.int32, device="cuda")
+        d_ua = torch.empty((B, N), dtype=torch.float32, device="cuda")
+        d_ur = torch.empty((B, N), dtype=torch.float32, device="cuda")
+        d_st = torch.empty(B, dtype=torch.int32, device="cuda")
+
+        def dstep(i):
+            native.resispec_draft_candidates(w["draft"], w["parent"], offset=i, node_token=d_tok,
+                                             u_accept=d_ua, u_resample=d_ur, out_status=d_st, **dkw)
+        t_end = time.perf_counter() + args.settle_ms * 1e-3
+        i = 0
+        while time.perf_counter() < t_end:
+            dstep(i)
+            torch.cuda.synchronize()
+            i += 1
+        for _ in range(args.warmup):
+            dstep(i)
+            i += 1
+        ev = [(torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True))
+              for _ in range(args.steps)]
+        torch.cuda.synchronize()
+        for e0, e1 in ev:
+            e0.record()
+            dstep(i)
+            e1.record()
+            i += 1
+        torch.cuda.synchronize()
+        dms = float(np.mean([e0.elapsed_time(e1) for e0, e1 in ev]))
+        assert (d_st.cpu().numpy() == 0).all() and (d_tok.cpu().numpy()[:, 1:] >= 0).all()
+        d_bytes = rows_d * V * esz + 12 * B * N + 4 * B * N   # draft rows of internal nodes; outputs; parents
+        draft = {"kernel_ms": dms, "rows_per_s": B * N / (dms * 1e-3),
+                 "alg_bytes_per_launch": d_bytes, "achieved_gbps": d_bytes / (dms * 1e-3) / 1e9}
+
     r = results[args.mode]
     achieved = r["row_kernel_gbps"]
     out = {
@@ -250,6 +288,7 @@ def main():
                      "rows_target": rows_t, "rows_draft": rows_d},
         "modes": results,
         "path_schedule": path,
+        "draft_step": draft,
     }
     if not args.no_cpu_baseline:
         out["cpu_baseline"] = cpu_baseline(w, args.cpu_seconds, args.mode)

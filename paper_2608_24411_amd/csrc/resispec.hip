@@ -1468,10 +1468,6 @@ __global__ void __launch_bounds__(kBlock) __attribute__((amdgpu_waves_per_eu(4))
     const int64_t row = (int64_t)b * P.N + n;
     const In* __restrict__ dg = reinterpret_cast<const In*>(P.dft) + row * V;
 
-    typename W::raw pre[UNR];
-#pragma unroll
-    for (int u = 0; u < UNR; ++u) pre[u] = W::template load<true>(dg, wid * G * CHUNK + lane * VEC + u * 64 * VEC, V);
-
     if (tid == 0) {
         uint32_t c[4] = {(uint32_t)n, (uint32_t)b, P.off_lo, P.off_hi};
         philox4x32_10(c, P.seed_lo, P.seed_hi);
@@ -1480,7 +1476,8 @@ __global__ void __launch_bounds__(kBlock) __attribute__((amdgpu_waves_per_eu(4))
         if (n == 0) P.node_token[row] = -1;
         sm.next_slot = kWaves;
     }
-    // children of node n (ascending node index) and the uniforms that draw them
+    // children of node n (ascending node index) and the uniforms that draw them; the
+    // draft row is only read when there are children
     const int64_t sb = (int64_t)b * P.N;
     int nc = 0, anybad = 0;
     for (int base = 0; base < P.N; base += kBlock) {
@@ -1497,18 +1494,6 @@ __global__ void __launch_bounds__(kBlock) __attribute__((amdgpu_waves_per_eu(4))
         if (lane == 0) {
             sm.wcount[wid] = __popcll(cm);
             sm.wbad[wid] = bm != 0;
-        }
-        if (base == 0) {
-            float mx = -FLT_MAX;
-#pragma unroll
-            for (int u = 0; u < UNR; ++u) {
-                float v[VEC];
-                W::unpack(pre[u], v);
-#pragma unroll
-                for (int e = 0; e < VEC; ++e) mx = fmaxf(mx, v[e]);
-            }
-            mx = wave_max(mx);
-            if (lane == 0) sm.wmax[0][wid] = mx;
         }
         __syncthreads();
         int rank = nc + __popcll(cm & __lanemask_lt());
@@ -1538,6 +1523,23 @@ __global__ void __launch_bounds__(kBlock) __attribute__((amdgpu_waves_per_eu(4))
         return;
     }
     if (nc == 0) return;
+    // this wave's first chunk; its maximum fixes the row's exponent reference
+    typename W::raw pre[UNR];
+#pragma unroll
+    for (int u = 0; u < UNR; ++u) pre[u] = W::template load<true>(dg, wid * G * CHUNK + lane * VEC + u * 64 * VEC, V);
+    {
+        float mx = -FLT_MAX;
+#pragma unroll
+        for (int u = 0; u < UNR; ++u) {
+            float v[VEC];
+            W::unpack(pre[u], v);
+#pragma unroll
+            for (int e = 0; e < VEC; ++e) mx = fmaxf(mx, v[e]);
+        }
+        mx = wave_max(mx);
+        if (lane == 0) sm.wmax[0][wid] = mx;
+    }
+    __syncthreads();
     const float c2h = P.c2h, c2l = P.c2l;
 
     // ---- one pass: the draft row's sum of exp2 against a fixed reference, per slot
