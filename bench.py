@@ -107,6 +107,77 @@ def time_mode(native, torch, w, mode, steps, warmup, settle, ws, out_tok, out_le
     return wall, kern_ms
 
 
+def run_study(native, torch, np, synth):
+    """Synthetic analogues of the paper's studies on the device path (Zipf+noise rows,
+    candidates and uniforms from the device draft step, many trials per workload by
+    advancing the Philox offset): acceptance by candidate index at one node (the
+    paper's first figure), mean accepted length over tree shapes of similar size (its
+    topology ablation), and the marginal gain per extra candidate (its efficiency
+    score).  Not timed; prints one JSON line."""
+    base = dict(kind="tree", V=32000, T=1.0, dtype="f32", zipf=1.1, tgt_sigma=1.0, worep=False)
+
+    def trials(cfg, n_off, fn):
+        w = synth.make_workload(cfg, device="cuda")
+        out = []
+        for off in range(n_off):
+            tok, ua, ur, st = native.resispec_draft_candidates(
+                w["draft"], w["parent"], temperature=w["temperature"],
+                without_replacement=w["without_replacement"], seed=2608, offset=off)
+            w2 = dict(w, node_token=tok, u_accept=ua, u_resample=ur)
+            out.append(fn(w2))
+        return w, out
+
+    res = {}
+    # 1. acceptance by candidate index: a root with 8 i.i.d. candidates
+    cfg = dict(base, name="root8", B=512, draft=("add", 1.5), tree=("first_child_chain", (8,)))
+    for mode in ("resispec", "specinfer"):
+        def one(w2):
+            d = native.resispec_verify_tree_debug(
+                w2["target"], w2["draft"], w2["node_token"], w2["parent"], w2["u_accept"],
+                w2["u_resample"], temperature=1.0, max_depth=w2["max_depth"], mode=mode)
+            torch.cuda.synchronize()
+            return d["node_child"][:, 0].cpu().numpy()
+        _, outs = trials(cfg, 16, one)
+        c = np.concatenate(outs)
+        hist = [float(np.mean(c == i + 1)) for i in range(8)]
+        res.setdefault("accept_by_candidate_index", {})[mode] = {
+            "P(accept candidate i), i=1..8": hist, "P(all rejected)": float(np.mean(c < 0)),
+            "trials": int(c.size)}
+
+    def eal(cfg, n_off):
+        r = {}
+        for mode in ("resispec", "specinfer"):
+            def one(w2):
+                t, l, s = native.resispec_verify_tree(
+                    w2["target"], w2["draft"], w2["node_token"], w2["parent"], w2["u_accept"],
+                    w2["u_resample"], temperature=1.0, max_depth=w2["max_depth"], mode=mode)
+                torch.cuda.synchronize()
+                assert (s.cpu().numpy() == 0).all()
+                return l.cpu().numpy()
+            _, outs = trials(cfg, n_off, one)
+            r[mode] = float(np.concatenate(outs).mean())
+        r["ratio"] = r["resispec"] / r["specinfer"]
+        return r
+
+    # 2. tree shapes of similar size: depth d, b candidates per level under the first
+    for d, bw in ((7, 2), (5, 3), (4, 5), (3, 11)):
+        cfg = dict(base, name="d%db%d" % (d, bw), B=256,
+                   draft=("add_depth", 1.0, 0.25, 4), tree=("first_child_chain", (bw,) * d))
+        res.setdefault("mean_accepted_length_by_shape", {})["d%db%d" % (d, bw)] = eal(cfg, 8)
+    # 3. marginal gain per extra candidate at depth 3
+    curve = {}
+    for k in (1, 2, 3, 4, 6, 8):
+        cfg = dict(base, name="d3b%d" % k, B=256, draft=("add_depth", 1.0, 0.25, 4),
+                   tree=("first_child_chain", (k,) * 3))
+        curve[k] = eal(cfg, 8)
+    eta = {}
+    for mode in ("resispec", "specinfer"):
+        eta[mode] = {str(k): (curve[k][mode] - curve[1][mode]) / (k - 1) for k in curve if k > 1}
+    res["mean_accepted_length_by_width_depth3"] = {str(k): v for k, v in curve.items()}
+    res["eta_marginal_gain_per_extra_candidate"] = eta
+    return res
+
+
 def main():
     ap = argparse.ArgumentParser(description=__doc__.split("\n")[0])
     ap.add_argument("--gpus", type=int, default=1)
@@ -121,6 +192,8 @@ def main():
     ap.add_argument("--no-other-mode", action="store_true")
     ap.add_argument("--no-path", action="store_true", help="skip the path-only schedule")
     ap.add_argument("--no-draft", action="store_true", help="skip the draft step")
+    ap.add_argument("--study", action="store_true",
+                    help="only run the synthetic acceptance studies (not a benchmark)")
     ap.add_argument("--copy-probe", type=int, default=0, metavar="MIB",
                     help="only run a plain device copy of MIB MiB (counter calibration)")
     args = ap.parse_args()
@@ -137,6 +210,9 @@ def main():
     from paper_2608_24411_amd import native, synth
 
     torch.cuda.set_device(0)
+    if args.study:
+        print(json.dumps({"study": run_study(native, torch, np, synth)}), flush=True)
+        return
     if args.copy_probe:
         # A plain copy of known size: FETCH_SIZE / WRITE_SIZE of this kernel divided by
         # its bytes is the scale applied to the row kernel's counters.

@@ -149,9 +149,10 @@ def _store(x, dtype):
 
 def make_workload(cfg_id, *, seed=SEED, device="cpu", B=None, V=None, N=None, dtype=None,
                   T=None):
-    """Generate one workload.  Overrides (B, V, N for random trees, dtype, T) give
-    smaller or ragged variants of the same recipe for tests."""
-    cfg = dict(CONFIGS[cfg_id])
+    """Generate one workload.  cfg_id: a key of CONFIGS, or a config dict of the same
+    form.  Overrides (B, V, N for random trees, dtype, T) give smaller or ragged
+    variants of the same recipe for tests."""
+    cfg = dict(CONFIGS[cfg_id]) if not isinstance(cfg_id, dict) else dict(cfg_id)
     if B is not None:
         cfg["B"] = B
     if V is not None:
