@@ -63,9 +63,6 @@ constexpr int kMaxCand = RS_MAX_CANDIDATES;
 #ifndef RS_MAX_SLOTS
 #define RS_MAX_SLOTS 128
 #endif
-#ifndef RS_LANE_PARTIALS
-#define RS_LANE_PARTIALS 1
-#endif
 #ifndef RS_UNR16
 #define RS_UNR16 2
 #endif
@@ -294,10 +291,8 @@ struct Smem {
     uint32_t hit_slots[kMaxSlots / 32];  // slots that hold a rejected token
     // per-lane partials of every slot of the running pass ([lane][slot], padded so a
     // wave's 64 stores hit 64 distinct banks), reduced after the pass in a fixed order
-#if RS_LANE_PARTIALS
     float partA[64][kMaxSlots + 1];
     float partB[64][kMaxSlots + 1];
-#endif
     double slotA[kMaxSlots];
     double slotB[kMaxSlots];
     double slotT[kMaxSlots];
@@ -352,14 +347,10 @@ __device__ long long* g_timing = nullptr;
 #endif
 
 // Exponent reference for a maximum m: an integer-valued float near -m * c2, so that
-// moving between references rescales sums by an exact power of two (ldexp).
+// the fp32 exponents near the maximum are small and exactly offset, and a shift of
+// the reference by an integer (the first-rejection split of log2 c) stays exact.
 __device__ __forceinline__ float kref(float m, float c2h) {
     return m > -FLT_MAX ? -ceilf(m * c2h) : 0.0f;
-}
-
-// acc * 2^(to - from) for integer-valued references
-__device__ __forceinline__ double rescale(double acc, float to, float from) {
-    return ldexp(acc, (int)(to - from));
 }
 
 __device__ __forceinline__ void write_outcome(const KParams& P, int64_t row, int32_t child,
@@ -722,18 +713,8 @@ __device__ __forceinline__ void verify_row(const KParams& P, Smem& sm, const int
     for (int attempt = 0;; ++attempt) {
         float fa = 0.0f, fc = 0.0f;   // this slot's lane partials
         auto flush = [&](int slot) {
-#if RS_LANE_PARTIALS
             sm.partA[lane][slot] = fa;
             if (internal) sm.partB[lane][slot] = fc;
-#else
-            const double a = wave_sum((double)fa);
-            const double c = internal ? wave_sum((double)fc) : 0.0;
-            if (lane == 0) {
-                sm.slotA[slot] = a;
-                sm.slotB[slot] = c;
-                sm.slotP[slot] = a;
-            }
-#endif
             fa = fc = 0.0f;
         };
         if (internal) {
@@ -772,7 +753,6 @@ __device__ __forceinline__ void verify_row(const KParams& P, Smem& sm, const int
             }
         }
         __syncthreads();
-#if RS_LANE_PARTIALS
         if (tid < nslots) {
             double a = 0.0, c = 0.0;
 #pragma unroll 8
@@ -786,7 +766,6 @@ __device__ __forceinline__ void verify_row(const KParams& P, Smem& sm, const int
             sm.slotP[tid] = a;
         }
         __syncthreads();
-#endif
         if (wid == 0) {
             double a0 = 0.0, a1 = 0.0;
             for (int s2 = lane; s2 < nslots; s2 += 64) {
@@ -935,17 +914,8 @@ __device__ __forceinline__ void verify_row(const KParams& P, Smem& sm, const int
             // ResiSpec needs the per-slot sums of R only after the first rejection
             const bool wantB = MODE == RS_MODE_RESISPEC && ii > 0;
             auto flush = [&](int slot) {
-#if RS_LANE_PARTIALS
                 sm.partA[lane][slot] = accA;
                 if (wantB) sm.partB[lane][slot] = accB;
-#else
-                const double wa = wave_sum((double)accA);
-                const double wb = wantB ? wave_sum((double)accB) : 0.0;
-                if (lane == 0) {
-                    sm.slotA[slot] = wa;
-                    sm.slotB[slot] = wb;
-                }
-#endif
                 accA = accB = 0.0f;
             };
             // does this slot hold a rejected token? (wave-uniform)
@@ -1049,7 +1019,6 @@ __device__ __forceinline__ void verify_row(const KParams& P, Smem& sm, const int
             }
         }
         __syncthreads();
-#if RS_LANE_PARTIALS
         if (tid < nslots) {
             double a = 0.0, c = 0.0;
 #pragma unroll 8
@@ -1062,7 +1031,6 @@ __device__ __forceinline__ void verify_row(const KParams& P, Smem& sm, const int
             sm.slotB[tid] = c;
         }
         __syncthreads();
-#endif
         if (wid == 0) {
             // per-lane sums over slots lane, lane+64, ... in a fixed order
             double A = 0.0, Bv = 0.0;
@@ -1560,16 +1528,10 @@ __global__ void __launch_bounds__(kBlock) __attribute__((amdgpu_waves_per_eu(4))
                     for (int e = 0; e < VEC; ++e) fa += exp2_fast(expo(t[u][e], c2h, c2l, K));
             },
             [&](int slot) {
-#if RS_LANE_PARTIALS
                 sm.partA[lane][slot] = fa;
-#else
-                const double a = wave_sum((double)fa);
-                if (lane == 0) sm.slotA[slot] = a;
-#endif
                 fa = 0.0f;
             });
         __syncthreads();
-#if RS_LANE_PARTIALS
         if (tid < nslots) {
             double a = 0.0;
 #pragma unroll 8
@@ -1577,7 +1539,6 @@ __global__ void __launch_bounds__(kBlock) __attribute__((amdgpu_waves_per_eu(4))
             sm.slotA[tid] = a;
         }
         __syncthreads();
-#endif
         if (wid == 0) {
             double a0 = 0.0;
             for (int s2 = lane; s2 < nslots; s2 += 64) a0 += sm.slotA[s2];
