@@ -21,13 +21,18 @@ import time
 
 ROOT = os.path.dirname(os.path.abspath(__file__))
 HBM_PEAK_GBPS = 8000.0
-KERNEL_SRC = os.path.join(ROOT, "paper_2608_24411_amd", "csrc", "resispec.hip")
+# the sources the row kernel is compiled from
+KERNEL_SRCS = [os.path.join(ROOT, "paper_2608_24411_amd", "csrc", f)
+               for f in ("resispec.hip", "common.h")]
 METRIC = "verified tree-node rows/s at V=128256 + achieved HBM GB/s (% of peak)"
 
 
 def kernel_source_hash():
-    with open(KERNEL_SRC, "rb") as f:
-        return hashlib.sha256(f.read()).hexdigest()
+    h = hashlib.sha256()
+    for path in KERNEL_SRCS:
+        with open(path, "rb") as f:
+            h.update(f.read())
+    return h.hexdigest()
 
 
 def measured_traffic(workload, mode):

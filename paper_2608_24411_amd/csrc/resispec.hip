@@ -40,269 +40,15 @@
 // the target row's unnormalised mass (the target normaliser is folded into the step
 // constants).
 //
-// A second kernel walks each tree from the root along accepted children.
-
-#include <hip/hip_runtime.h>
+// A second kernel walks each tree from the root along accepted children; a third
+// (the path-only schedule) verifies only the nodes each walk reaches.  The draft step
+// that precedes verification is in draft.hip; shared helpers are in common.h.
 
 #include <atomic>
-#include <cfloat>
-#include <cmath>
-#include <cstdint>
 
-#include "resispec.h"
+#include "common.h"
 
 namespace {
-
-#ifndef RS_BLOCK
-#define RS_BLOCK 512
-#endif
-constexpr int kBlock = RS_BLOCK;          // threads per row workgroup (all-nodes schedule)
-constexpr int kBlockWide = 1024;         // path schedule with few sequences: one workgroup per CU
-constexpr int kMaxWaves = kBlockWide / 64;
-constexpr int kMaxCand = RS_MAX_CANDIDATES;
-#ifndef RS_MAX_SLOTS
-#define RS_MAX_SLOTS 128
-#endif
-#ifndef RS_UNR16
-#define RS_UNR16 2
-#endif
-#ifndef RS_UNR32
-#define RS_UNR32 2
-#endif
-// Load policy.  Data whose last full use is the current pass is read with nontemporal
-// loads (about 12% more streaming bandwidth on gfx950): pass 1 of rows without
-// children and every rejection pass.  Pass 1 of a row with children uses ordinary loads,
-// so a rejection pass that follows soon after can still find part of the row in the
-// last-level cache.
-constexpr bool kNtPass1 = false;
-constexpr bool kNtRej = true;
-constexpr bool kNtLeaf = true;
-constexpr int kMaxSlots = RS_MAX_SLOTS;   // per-row slots (runs of chunks) with partial sums
-// A row's exponent reference is fixed before pass 1; sums outside [2^-kLow, inf) send the
-// row through an exact-maximum pass and a second pass 1.
-constexpr double kLowSum = 1.0 / 1048576.0;
-
-// ------------------------------------------------------------------ loads ----
-
-__device__ __forceinline__ float bf16_lo(uint32_t w) { return __uint_as_float(w << 16); }
-__device__ __forceinline__ float bf16_hi(uint32_t w) { return __uint_as_float(w & 0xffff0000u); }
-
-__device__ __forceinline__ float widen(float x) { return x; }
-__device__ __forceinline__ float widen(uint16_t h) { return __uint_as_float(((uint32_t)h) << 16); }
-
-// VEC consecutive elements starting at element idx, kept as raw words until used;
-// elements at or beyond V read as -inf, which makes them contribute exactly zero to
-// every sum below.
-// 16-byte load; NT: nontemporal (streamed past the caches' normal allocation)
-typedef unsigned int u32x4 __attribute__((ext_vector_type(4)));
-template <bool NT>
-__device__ __forceinline__ uint4 ld16(const void* p) {
-    if (NT) {
-        const u32x4 r = __builtin_nontemporal_load(reinterpret_cast<const u32x4*>(p));
-        return make_uint4(r.x, r.y, r.z, r.w);
-    }
-    return *reinterpret_cast<const uint4*>(p);
-}
-template <bool NT>
-__device__ __forceinline__ uint32_t ld4(const void* p) {
-    if (NT) return __builtin_nontemporal_load(reinterpret_cast<const uint32_t*>(p));
-    return *reinterpret_cast<const uint32_t*>(p);
-}
-template <bool NT>
-__device__ __forceinline__ uint32_t ld2(const void* p) {
-    if (NT) return __builtin_nontemporal_load(reinterpret_cast<const uint16_t*>(p));
-    return *reinterpret_cast<const uint16_t*>(p);
-}
-
-template <typename In, int VEC>
-struct Vec;
-
-template <>
-struct Vec<float, 4> {
-    using raw = uint4;
-    template <bool NT = false>
-    static __device__ __forceinline__ raw load(const float* __restrict__ row, int idx, int V) {
-        if (idx < V) return ld16<NT>(row + idx);
-        return make_uint4(0xff800000u, 0xff800000u, 0xff800000u, 0xff800000u);
-    }
-    template <bool NT = false>
-    static __device__ __forceinline__ raw load_full(const float* __restrict__ row, int idx) {
-        return ld16<NT>(row + idx);
-    }
-    static __device__ __forceinline__ void unpack(const raw& r, float (&v)[4]) {
-        v[0] = __uint_as_float(r.x); v[1] = __uint_as_float(r.y);
-        v[2] = __uint_as_float(r.z); v[3] = __uint_as_float(r.w);
-    }
-};
-
-template <>
-struct Vec<uint16_t, 8> {
-    using raw = uint4;
-    template <bool NT = false>
-    static __device__ __forceinline__ raw load(const uint16_t* __restrict__ row, int idx, int V) {
-        if (idx < V) return ld16<NT>(row + idx);
-        return make_uint4(0xff80ff80u, 0xff80ff80u, 0xff80ff80u, 0xff80ff80u);
-    }
-    template <bool NT = false>
-    static __device__ __forceinline__ raw load_full(const uint16_t* __restrict__ row, int idx) {
-        return ld16<NT>(row + idx);
-    }
-    static __device__ __forceinline__ void unpack(const raw& r, float (&v)[8]) {
-        v[0] = bf16_lo(r.x); v[1] = bf16_hi(r.x);
-        v[2] = bf16_lo(r.y); v[3] = bf16_hi(r.y);
-        v[4] = bf16_lo(r.z); v[5] = bf16_hi(r.z);
-        v[6] = bf16_lo(r.w); v[7] = bf16_hi(r.w);
-    }
-};
-
-template <>
-struct Vec<float, 1> {
-    using raw = uint32_t;
-    template <bool NT = false>
-    static __device__ __forceinline__ raw load(const float* __restrict__ row, int idx, int V) {
-        return idx < V ? ld4<NT>(row + idx) : 0xff800000u;
-    }
-    template <bool NT = false>
-    static __device__ __forceinline__ raw load_full(const float* __restrict__ row, int idx) {
-        return ld4<NT>(row + idx);
-    }
-    static __device__ __forceinline__ void unpack(const raw& r, float (&v)[1]) { v[0] = __uint_as_float(r); }
-};
-
-template <>
-struct Vec<uint16_t, 1> {
-    using raw = uint32_t;
-    template <bool NT = false>
-    static __device__ __forceinline__ raw load(const uint16_t* __restrict__ row, int idx, int V) {
-        return idx < V ? ld2<NT>(row + idx) << 16 : 0xff800000u;
-    }
-    template <bool NT = false>
-    static __device__ __forceinline__ raw load_full(const uint16_t* __restrict__ row, int idx) {
-        return ld2<NT>(row + idx) << 16;
-    }
-    static __device__ __forceinline__ void unpack(const raw& r, float (&v)[1]) { v[0] = __uint_as_float(r); }
-};
-
-// Unpacked elements of one vector (used outside the streaming passes).
-template <typename In, int VEC>
-__device__ __forceinline__ void load_vec(const In* __restrict__ row, int idx, int V, float (&v)[VEC]) {
-    Vec<In, VEC>::unpack(Vec<In, VEC>::load(row, idx, V), v);
-}
-
-// v_exp_f32: 2^x; results below the normal range flush to zero (they are more than
-// 2^-126 below the row maximum and carry no mass at fp32 resolution).
-__device__ __forceinline__ float exp2_fast(float x) { return __builtin_amdgcn_exp2f(x); }
-
-// exponent l * c2 + K with c2 = c2h + c2l (both > 0; see base_params)
-__device__ __forceinline__ float expo(float l, float c2h, float c2l, float K) {
-    return fmaf(l, c2l, fmaf(l, c2h, K));
-}
-
-// ------------------------------------------------------------- wave ops ----
-
-// Wave-wide reductions with DPP lane moves inside each 16-lane row (xor 1, xor 2,
-// half-row mirror, row mirror), then the four row results combined in a fixed order
-// from lanes 0, 16, 32, 48.  Every lane returns the same value.
-template <int CTRL>
-__device__ __forceinline__ int dpp_i(int v) {
-    return __builtin_amdgcn_update_dpp(0, v, CTRL, 0xF, 0xF, false);
-}
-template <int CTRL>
-__device__ __forceinline__ float dpp_f(float v) {
-    return __int_as_float(dpp_i<CTRL>(__float_as_int(v)));
-}
-template <int CTRL>
-__device__ __forceinline__ double dpp_d(double v) {
-    const int lo = dpp_i<CTRL>(__double2loint(v));
-    const int hi = dpp_i<CTRL>(__double2hiint(v));
-    return __hiloint2double(hi, lo);
-}
-constexpr int kDppXor1 = 0xB1, kDppXor2 = 0x4E, kDppHalfMirror = 0x141, kDppMirror = 0x140;
-
-__device__ __forceinline__ float readlane_f(float v, int l) {
-    return __int_as_float(__builtin_amdgcn_readlane(__float_as_int(v), l));
-}
-__device__ __forceinline__ double readlane_d(double v, int l) {
-    return __hiloint2double(__builtin_amdgcn_readlane(__double2hiint(v), l),
-                            __builtin_amdgcn_readlane(__double2loint(v), l));
-}
-
-__device__ __forceinline__ float wave_max(float v) {
-    v = fmaxf(v, dpp_f<kDppXor1>(v));
-    v = fmaxf(v, dpp_f<kDppXor2>(v));
-    v = fmaxf(v, dpp_f<kDppHalfMirror>(v));
-    v = fmaxf(v, dpp_f<kDppMirror>(v));
-    return fmaxf(fmaxf(readlane_f(v, 0), readlane_f(v, 16)), fmaxf(readlane_f(v, 32), readlane_f(v, 48)));
-}
-
-__device__ __forceinline__ double wave_sum(double v) {
-    v += dpp_d<kDppXor1>(v);
-    v += dpp_d<kDppXor2>(v);
-    v += dpp_d<kDppHalfMirror>(v);
-    v += dpp_d<kDppMirror>(v);
-    return (readlane_d(v, 0) + readlane_d(v, 16)) + (readlane_d(v, 32) + readlane_d(v, 48));
-}
-
-__device__ __forceinline__ double wave_incl_scan(double v, int lane) {
-#pragma unroll
-    for (int o = 1; o < 64; o <<= 1) {
-        const double n = __shfl_up(v, o, 64);
-        if (lane >= o) v += n;
-    }
-    return v;
-}
-
-// ------------------------------------------------------------ row state ----
-
-struct Smem {
-    int32_t status;
-    int32_t decision;     // -1 continue, >= 0 accepted candidate, -2 fault
-    int32_t next_slot;    // slot counter of the running sweep
-    int32_t nc;           // rows with more nodes than threads only
-    float ur;
-    double St, Sd;        // sums of exp2(l c2 + K)
-    int32_t wcount[kMaxWaves];
-    int32_t wbad[kMaxWaves];
-    int32_t cand_tok[kMaxCand];
-    int32_t cand_node[kMaxCand];
-    float cand_u[kMaxCand];
-    float cand_lt[kMaxCand];
-    float cand_ld[kMaxCand];
-    double cand_p[kMaxCand];
-    double cand_q[kMaxCand];
-    // rejection steps, in test order; fp32 copies are in target-mass units
-    int32_t st_x[kMaxCand + 1];
-    float st_c[kMaxCand + 1];       // ResiSpec: Z * dscale * St/Sd.  Standard: C * St/Sd
-    float st_a[kMaxCand + 1];       // ResiSpec: a
-    float st_i[kMaxCand + 1];       // ResiSpec: 1/Z
-    double st_zd[kMaxCand + 1], st_ad[kMaxCand + 1];
-    double st_ds[kMaxCand + 1];     // draft scale (without replacement)
-    double st_rx[kMaxCand + 1];     // R(x_i) of the tested candidate (normalised)
-    // standard residual after i + 1 rejections, collapsed:
-    //   R = max(p - C_i q, 0) / Tot_i,  C_i = C_{i-1} + Tot_{i-1} dscale_i
-    double st_C[kMaxCand + 1], st_tot[kMaxCand + 1];
-    // ResiSpec, first rejection: min(c Q, R) = 2^f0 exp2(min(aR - f0, aQ + e)) with
-    // log2 c = e + f0; kq0 = Kd + e (integer valued)
-    float st_f0, st_kq0;
-    double st_2f0;                  // 2^f0 (as v_exp_f32 gives it)
-    double rx0e;                    // the fp32 element value of R at x_0 (target units)
-    int32_t sx0;                    // slot holding x_0
-    double slotP[kMaxSlots];        // pass-1 slot totals of the target row
-    uint32_t hit_slots[kMaxSlots / 32];  // slots that hold a rejected token
-    // per-lane partials of every slot of the running pass ([lane][slot], padded so a
-    // wave's 64 stores hit 64 distinct banks), reduced after the pass in a fixed order
-    float partA[64][kMaxSlots + 1];
-    float partB[64][kMaxSlots + 1];
-    double slotA[kMaxSlots];
-    double slotB[kMaxSlots];
-    double slotT[kMaxSlots];
-    float wmax[2][kMaxWaves];
-    // draw
-    int32_t token;
-    double total;
-    // outcome of the row (path schedule)
-    int32_t res_child, res_tok, res_status;
-};
 
 struct KParams {
     const void* tgt;
@@ -345,13 +91,6 @@ __device__ long long* g_timing = nullptr;
     do {                 \
     } while (0)
 #endif
-
-// Exponent reference for a maximum m: an integer-valued float near -m * c2, so that
-// the fp32 exponents near the maximum are small and exactly offset, and a shift of
-// the reference by an integer (the first-rejection split of log2 c) stays exact.
-__device__ __forceinline__ float kref(float m, float c2h) {
-    return m > -FLT_MAX ? -ceilf(m * c2h) : 0.0f;
-}
 
 __device__ __forceinline__ void write_outcome(const KParams& P, int64_t row, int32_t child,
                                               int32_t tok, int32_t status) {
@@ -425,120 +164,6 @@ __device__ double scalar_residual(const Smem& sm, int i, double p, double q, int
         if (worep && x == sm.st_x[t]) removed = true;
     }
     return R;
-}
-
-// One chunk (UNR loads of 64 * VEC elements per row) starting at element c0 + lane * VEC;
-// chunks wholly below V load without per-lane bounds checks.
-template <typename In, int VEC, int UNR, bool PAIR, bool NT>
-__device__ __forceinline__ void load_chunk(const In* __restrict__ tg, const In* __restrict__ dg,
-                                           int c0, int V, typename Vec<In, VEC>::raw (&t)[UNR],
-                                           typename Vec<In, VEC>::raw (&d)[UNR]) {
-    using W = Vec<In, VEC>;
-    constexpr int CHUNK = 64 * VEC * UNR;
-    const int l0 = c0 + (threadIdx.x & 63) * VEC;
-    if (c0 + CHUNK <= V) {
-#pragma unroll
-        for (int u = 0; u < UNR; ++u) {
-            t[u] = W::template load_full<NT>(tg, l0 + u * 64 * VEC);
-            if (PAIR) d[u] = W::template load_full<NT>(dg, l0 + u * 64 * VEC);
-        }
-    } else {
-#pragma unroll
-        for (int u = 0; u < UNR; ++u) {
-            t[u] = W::template load<NT>(tg, l0 + u * 64 * VEC, V);
-            if (PAIR) d[u] = W::template load<NT>(dg, l0 + u * 64 * VEC, V);
-        }
-    }
-}
-
-// One pass over the row.  The row is cut into chunks of 64 * VEC * UNR elements (one
-// 128-bit load per lane and UNR) and runs of G chunks form slots.  Waves take slots
-// from a shared counter, so the eight waves of the block finish within about one chunk
-// of each other; a wave's first slot is its own index, so its first loads can be
-// issued before the counter is set (PRE = 1: its target part was loaded by the caller
-// into pre_t; PRE = 2: target and draft parts, into pre_t and pre_d).  Two register
-// sets alternate: the next chunk is loaded into one while the other is processed.
-// body(t, d, idx0, slot) gets the unpacked elements
-// of a chunk (element (u, e) has index idx0 + u * 64 * VEC + e); flush(slot) runs
-// after a slot's last chunk.  reverse: slots in descending order, chunks descending
-// inside a slot.
-template <typename In, int VEC, int UNR, bool PAIR, int PRE, bool NT, typename Body, typename Flush>
-__device__ __forceinline__ void wave_sweep(const In* __restrict__ tg, const In* __restrict__ dg,
-                                           int V, int G, int nslots, bool reverse,
-                                           const typename Vec<In, VEC>::raw (&pre_t)[UNR],
-                                           const typename Vec<In, VEC>::raw (&pre_d)[UNR],
-                                           int* counter, Body&& body, Flush&& flush) {
-    using W = Vec<In, VEC>;
-    using raw = typename W::raw;
-    constexpr int CHUNK = 64 * VEC * UNR;
-    const int lane = threadIdx.x & 63;
-    const int wid = threadIdx.x >> 6;
-    const int lane0 = lane * VEC;
-    // first element of chunk j of a slot (the same for every lane)
-    auto chunk_start = [&](int slot, int j) -> int {
-        return (slot * G + (reverse ? G - 1 - j : j)) * CHUNK;
-    };
-    int slot = wid < nslots ? (reverse ? nslots - 1 - wid : wid) : -1;
-    if (slot < 0) return;
-    // the counter is read one slot ahead, so its latency overlaps a chunk's work
-    auto take = [&]() -> int {
-        int v = 0;
-        if (lane == 0) v = atomicAdd(counter, 1);
-        v = __builtin_amdgcn_readfirstlane(v);
-        return v < nslots ? (reverse ? nslots - 1 - v : v) : -1;
-    };
-    int ahead = take();
-    auto advance = [&](int& s, int& j) {
-        if (++j == G) {
-            s = ahead;
-            j = 0;
-            if (s >= 0) ahead = take();
-        }
-    };
-    auto load = [&](int s, int j, raw (&t)[UNR], raw (&d)[UNR]) {
-        load_chunk<In, VEC, UNR, PAIR, NT>(tg, dg, chunk_start(s, j), V, t, d);
-    };
-    auto process = [&](const raw (&ct)[UNR], const raw (&cd)[UNR], int s, int j) {
-        float t[UNR][VEC], d[UNR][VEC];
-#pragma unroll
-        for (int u = 0; u < UNR; ++u) {
-            W::unpack(ct[u], t[u]);
-            if (PAIR) W::unpack(cd[u], d[u]);
-        }
-        body(t, d, chunk_start(s, j) + lane0, s);
-        if (j == G - 1) flush(s);
-    };
-    raw at[UNR], ad[UNR], bt[UNR], bd[UNR];
-    int sa = slot, ja = 0;
-    if (PRE >= 1) {
-#pragma unroll
-        for (int u = 0; u < UNR; ++u) at[u] = pre_t[u];
-        if (PAIR) {
-            if (PRE == 2) {
-#pragma unroll
-                for (int u = 0; u < UNR; ++u) ad[u] = pre_d[u];
-            } else {
-                const int c0 = chunk_start(sa, 0);
-#pragma unroll
-                for (int u = 0; u < UNR; ++u) ad[u] = W::template load<NT>(dg, c0 + lane0 + u * 64 * VEC, V);
-            }
-        }
-    } else {
-        load(sa, ja, at, ad);
-    }
-    for (;;) {
-        int sb = sa, jb = ja;
-        advance(sb, jb);
-        if (sb >= 0) load(sb, jb, bt, bd);
-        process(at, ad, sa, ja);
-        if (sb < 0) break;
-        sa = sb;
-        ja = jb;
-        advance(sa, ja);
-        if (sa >= 0) load(sa, ja, at, ad);
-        process(bt, bd, sb, jb);
-        if (sa < 0) break;
-    }
 }
 
 // ------------------------------------------------------------ row kernel ----
@@ -1379,397 +1004,6 @@ rs_path_kernel(const KParams P, int32_t max_depth, int32_t* __restrict__ out_tok
     }
 }
 
-// ------------------------------------------------------------ draft step ----
-//
-// The step before verification: every node's uniforms and the candidate tokens of
-// every node's children, drawn on the device.  Uniforms come from Philox4x32-10
-// (Salmon, Moraes, Dror and Shaw, SC'11): node n of sequence b takes counter
-// (n, b, offset low, offset high) under key (seed low, seed high); word 0 is its
-// u_accept, word 1 its u_resample and word 2 the uniform that draws the node's own
-// token from its parent's draft distribution.  Candidates are inverse-CDF draws in
-// vocabulary order from softmax(draft / T) (children in ascending node index); without
-// replacement each draw removes its token from the distribution before the next.
-
-__device__ __forceinline__ void philox4x32_10(uint32_t (&c)[4], uint32_t k0, uint32_t k1) {
-#pragma unroll
-    for (int r = 0; r < 10; ++r) {
-        if (r > 0) {
-            k0 += 0x9E3779B9u;
-            k1 += 0xBB67AE85u;
-        }
-        const uint32_t lo0 = 0xD2511F53u * c[0], hi0 = __umulhi(0xD2511F53u, c[0]);
-        const uint32_t lo1 = 0xCD9E8D57u * c[2], hi1 = __umulhi(0xCD9E8D57u, c[2]);
-        const uint32_t n0 = hi1 ^ c[1] ^ k0, n2 = hi0 ^ c[3] ^ k1;
-        c[0] = n0;
-        c[1] = lo1;
-        c[2] = n2;
-        c[3] = lo0;
-    }
-}
-
-__device__ __forceinline__ float u01(uint32_t w) { return (float)(w >> 8) * (1.0f / 16777216.0f); }
-
-struct DParams {
-    const void* dft;
-    const int32_t* parent;
-    int32_t* node_token;
-    float* ua;
-    float* ur;
-    int32_t* out_status;   // per sequence, may be NULL
-    int32_t B, N, V;
-    float c2h, c2l;
-    int32_t worep;
-    uint32_t seed_lo, seed_hi, off_lo, off_hi;
-    int32_t G, nslots;
-};
-
-template <typename In, int VEC, int UNR>
-__global__ void __launch_bounds__(kBlock) __attribute__((amdgpu_waves_per_eu(4))) rs_draft_kernel(const DParams P) {
-    __shared__ Smem sm;
-    constexpr int kWaves = kBlock / 64;
-    constexpr int CHUNK = 64 * VEC * UNR;
-    using W = Vec<In, VEC>;
-    const int tid = threadIdx.x, lane = tid & 63, wid = tid >> 6;
-    const int V = P.V, G = P.G, nslots = P.nslots;
-    const int32_t g = blockIdx.x;
-    const int32_t n = g / P.B, b = g - n * P.B;
-    const int64_t row = (int64_t)b * P.N + n;
-    const In* __restrict__ dg = reinterpret_cast<const In*>(P.dft) + row * V;
-
-    if (tid == 0) {
-        uint32_t c[4] = {(uint32_t)n, (uint32_t)b, P.off_lo, P.off_hi};
-        philox4x32_10(c, P.seed_lo, P.seed_hi);
-        P.ua[row] = u01(c[0]);
-        P.ur[row] = u01(c[1]);
-        if (n == 0) P.node_token[row] = -1;
-        sm.next_slot = kWaves;
-    }
-    // children of node n (ascending node index) and the uniforms that draw them; the
-    // draft row is only read when there are children
-    const int64_t sb = (int64_t)b * P.N;
-    int nc = 0, anybad = 0;
-    for (int base = 0; base < P.N; base += kBlock) {
-        const int m = base + tid;
-        bool holder = false;
-        int bad = 0;
-        if (m < P.N) {
-            const int32_t pm = P.parent[sb + m];
-            bad = (m == 0) ? (pm != -1) : (pm < 0 || pm >= m);
-            holder = m > n && pm == n;
-        }
-        const uint64_t cm = __ballot(holder);
-        const uint64_t bm = __ballot(bad);
-        if (lane == 0) {
-            sm.wcount[wid] = __popcll(cm);
-            sm.wbad[wid] = bm != 0;
-        }
-        __syncthreads();
-        int rank = nc + __popcll(cm & __lanemask_lt());
-        for (int w = 0; w < kWaves; ++w) {
-            rank += (w < wid) ? sm.wcount[w] : 0;
-            nc += sm.wcount[w];
-            anybad |= sm.wbad[w];
-        }
-        if (holder && rank < kMaxCand) {
-            uint32_t c[4] = {(uint32_t)m, (uint32_t)b, P.off_lo, P.off_hi};
-            philox4x32_10(c, P.seed_lo, P.seed_hi);
-            sm.cand_node[rank] = m;
-            sm.cand_u[rank] = u01(c[2]);
-        }
-        __syncthreads();
-    }
-    if (n == 0 && tid == 0 && P.out_status) P.out_status[b] = anybad ? RS_SEQ_BAD_TREE : RS_SEQ_OK;
-    if (anybad) {
-        // a malformed tree: every node's own row marks the node
-        if (n > 0 && tid == 0) P.node_token[row] = -1;
-        return;
-    }
-    if (nc > kMaxCand) {
-        // too many children to draw: all of them keep token -1
-        for (int m = n + 1 + tid; m < P.N; m += kBlock)
-            if (P.parent[sb + m] == n) P.node_token[sb + m] = -1;
-        return;
-    }
-    if (nc == 0) return;
-    // this wave's first chunk; its maximum fixes the row's exponent reference
-    typename W::raw pre[UNR];
-#pragma unroll
-    for (int u = 0; u < UNR; ++u) pre[u] = W::template load<true>(dg, wid * G * CHUNK + lane * VEC + u * 64 * VEC, V);
-    {
-        float mx = -FLT_MAX;
-#pragma unroll
-        for (int u = 0; u < UNR; ++u) {
-            float v[VEC];
-            W::unpack(pre[u], v);
-#pragma unroll
-            for (int e = 0; e < VEC; ++e) mx = fmaxf(mx, v[e]);
-        }
-        mx = wave_max(mx);
-        if (lane == 0) sm.wmax[0][wid] = mx;
-    }
-    __syncthreads();
-    const float c2h = P.c2h, c2l = P.c2l;
-
-    // ---- one pass: the draft row's sum of exp2 against a fixed reference, per slot
-    float K;
-    {
-        float m0 = -FLT_MAX;
-        for (int w = 0; w < kWaves; ++w) m0 = fmaxf(m0, sm.wmax[0][w]);
-        K = kref(m0, c2h);
-    }
-    double total = 0.0;
-    for (int attempt = 0;; ++attempt) {
-        float fa = 0.0f;
-        wave_sweep<In, VEC, UNR, false, 1, true>(dg, dg, V, G, nslots, false, pre, pre, &sm.next_slot,
-            [&](const float (&t)[UNR][VEC], const float (&)[UNR][VEC], int, int) {
-#pragma unroll
-                for (int u = 0; u < UNR; ++u)
-#pragma unroll
-                    for (int e = 0; e < VEC; ++e) fa += exp2_fast(expo(t[u][e], c2h, c2l, K));
-            },
-            [&](int slot) {
-                sm.partA[lane][slot] = fa;
-                fa = 0.0f;
-            });
-        __syncthreads();
-        if (tid < nslots) {
-            double a = 0.0;
-#pragma unroll 8
-            for (int l = 0; l < 64; ++l) a += (double)sm.partA[l][tid];
-            sm.slotA[tid] = a;
-        }
-        __syncthreads();
-        if (wid == 0) {
-            double a0 = 0.0;
-            for (int s2 = lane; s2 < nslots; s2 += 64) a0 += sm.slotA[s2];
-            const double s0 = wave_sum(a0);
-            if (lane == 0) {
-                sm.total = s0;
-                sm.decision = (s0 >= kLowSum && s0 < INFINITY) ? -1 : -3;
-                sm.next_slot = kWaves;
-            }
-        }
-        __syncthreads();
-        if (sm.decision != -3) {
-            total = sm.total;
-            break;
-        }
-        if (attempt == 1) {
-            // no usable distribution: the children keep token -1
-            if (tid < nc) P.node_token[sb + sm.cand_node[tid]] = -1;
-            return;
-        }
-        float mx = -FLT_MAX;
-        wave_sweep<In, VEC, UNR, false, 0, false>(dg, dg, V, G, nslots, false, pre, pre, &sm.next_slot,
-            [&](const float (&t)[UNR][VEC], const float (&)[UNR][VEC], int, int) {
-#pragma unroll
-                for (int u = 0; u < UNR; ++u)
-#pragma unroll
-                    for (int e = 0; e < VEC; ++e) mx = fmaxf(mx, t[u][e]);
-            },
-            [](int) {});
-        mx = wave_max(mx);
-        if (lane == 0) sm.wmax[0][wid] = mx;
-        __syncthreads();
-        float m0 = -FLT_MAX;
-        for (int w = 0; w < kWaves; ++w) m0 = fmaxf(m0, sm.wmax[0][w]);
-        K = kref(m0, c2h);
-        if (tid == 0) {
-            sm.decision = -1;
-            sm.next_slot = kWaves;
-        }
-        __syncthreads();
-    }
-    if (wid != 0) return;
-
-    // ---- the draws (wave 0): inverse CDF over the slot totals, then inside one slot
-    const bool worep = P.worep != 0;
-    const int R = G * VEC * UNR;          // elements of a slot per lane
-    double removed = 0.0;                 // mass drawn so far (without replacement)
-    for (int i = 0; i < nc; ++i) {
-        const double thr = (double)sm.cand_u[i] * (total - removed);
-        // removed tokens of each slot (lane j holds removed token j, j < i)
-        const int32_t rtok = (worep && lane < i) ? sm.cand_tok[lane] : -1;
-        const int rslot = rtok >= 0 ? (rtok / CHUNK) / G : -1;
-        const double rval = rtok >= 0 ? sm.cand_p[lane] : 0.0;
-        double Ts[4];
-        double own = 0.0;
-#pragma unroll
-        for (int q = 0; q < 4; ++q) {
-            const int s2 = 4 * lane + q;
-            double T = 0.0;
-            if (s2 < nslots) T = sm.slotA[s2];
-            Ts[q] = T;
-        }
-        // subtract removed masses slot by slot (at most i tokens, broadcast one by one)
-        if (worep) {
-            for (int j = 0; j < i; ++j) {
-                const int sj = __builtin_amdgcn_readlane(rslot, j);
-                const double vj = readlane_d(rval, j);
-#pragma unroll
-                for (int q = 0; q < 4; ++q)
-                    if (4 * lane + q == sj) Ts[q] -= vj;
-            }
-        }
-#pragma unroll
-        for (int q = 0; q < 4; ++q) {
-            Ts[q] = Ts[q] > 0.0 ? Ts[q] : 0.0;
-            own += Ts[q];
-        }
-        const double incl = wave_incl_scan(own, lane);
-        const double excl = incl - own;
-        uint64_t hit = __ballot(own > 0.0 && incl > thr);
-        int L = hit ? (__ffsll((unsigned long long)hit) - 1) : -1;
-        if (L < 0) {
-            const uint64_t pos = __ballot(own > 0.0);
-            L = pos ? 63 - __clzll((long long)pos) : 0;
-        }
-        int ks = -1;
-        double base = 0.0;
-        if (lane == L) {
-            double c = excl;
-            int lastpos = -1;
-            double lastbase = 0.0;
-#pragma unroll
-            for (int q = 0; q < 4; ++q) {
-                if (Ts[q] > 0.0) {
-                    if (ks < 0 && c + Ts[q] > thr) {
-                        ks = 4 * lane + q;
-                        base = c;
-                    }
-                    lastpos = 4 * lane + q;
-                    lastbase = c;
-                }
-                c += Ts[q];
-            }
-            if (ks < 0) {
-                ks = lastpos;
-                base = lastbase;
-            }
-        }
-        ks = __builtin_amdgcn_readlane(ks, L);
-        base = readlane_d(base, L);
-        int32_t tok = -1;
-        double tval = 0.0;
-        if (ks >= 0) {
-            // removed tokens inside slot ks (wave-uniform list, read one by one below)
-            const uint64_t rin = __ballot(rtok >= 0 && rslot == ks);
-            const int t0 = ks * G * CHUNK + lane * R;
-            auto value = [&](float l, int j) -> float {
-                float v = exp2_fast(expo(l, c2h, c2l, K));
-                uint64_t m = rin;
-                while (m) {
-                    const int jl = __ffsll((unsigned long long)m) - 1;
-                    m &= m - 1;
-                    if (j == __builtin_amdgcn_readlane(rtok, jl)) v = 0.0f;
-                }
-                return v;
-            };
-            constexpr int kRegRun = 32;
-            float vals[kRegRun];
-            double own2 = 0.0;
-            const bool inreg = R <= kRegRun;
-            if (inreg) {
-#pragma unroll
-                for (int c = 0; c < kRegRun; c += VEC) {
-                    float dv[VEC];
-                    if (c < R) load_vec<In, VEC>(dg, t0 + c, V, dv);
-#pragma unroll
-                    for (int e = 0; e < VEC; ++e) {
-                        const int j = t0 + c + e;
-                        const float v = (c < R && j < V) ? value(dv[e], j) : 0.0f;
-                        vals[c + e] = v;
-                        own2 += (double)v;
-                    }
-                }
-            } else {
-                for (int c = 0; c < R; c += VEC) {
-                    float dv[VEC];
-                    load_vec<In, VEC>(dg, t0 + c, V, dv);
-#pragma unroll
-                    for (int e = 0; e < VEC; ++e) {
-                        const int j = t0 + c + e;
-                        if (j < V) own2 += (double)value(dv[e], j);
-                    }
-                }
-            }
-            const double incl2 = wave_incl_scan(own2, lane);
-            const double excl2 = incl2 - own2;
-            const uint64_t hit2 = __ballot(own2 > 0.0 && base + incl2 > thr);
-            int L2 = hit2 ? (__ffsll((unsigned long long)hit2) - 1) : -1;
-            const bool fallback = L2 < 0;
-            if (fallback) {
-                const uint64_t pos = __ballot(own2 > 0.0);
-                L2 = pos ? 63 - __clzll((long long)pos) : -1;
-            }
-            float tv = 0.0f;
-            if (lane == L2) {
-                double acc = base + excl2;
-                int lastpos = -1;
-                float lastv = 0.0f;
-                if (inreg) {
-#pragma unroll
-                    for (int c = 0; c < kRegRun; ++c) {
-                        const float v = vals[c];
-                        const int j = t0 + c;
-                        if (tok < 0 && c < R && j < V) {
-                            if (v > 0.0f) {
-                                lastpos = j;
-                                lastv = v;
-                            }
-                            acc += (double)v;
-                            if (!fallback && v > 0.0f && acc > thr) {
-                                tok = j;
-                                tv = v;
-                            }
-                        }
-                    }
-                } else {
-                    for (int c = 0; c < R && tok < 0; c += VEC) {
-                        float dv[VEC];
-                        load_vec<In, VEC>(dg, t0 + c, V, dv);
-                        for (int e = 0; e < VEC; ++e) {
-                            const int j = t0 + c + e;
-                            if (j >= V) break;
-                            const float v = value(dv[e], j);
-                            if (v > 0.0f) {
-                                lastpos = j;
-                                lastv = v;
-                            }
-                            acc += (double)v;
-                            if (!fallback && v > 0.0f && acc > thr) {
-                                tok = j;
-                                tv = v;
-                                break;
-                            }
-                        }
-                    }
-                }
-                if (tok < 0) {
-                    tok = lastpos;
-                    tv = lastv;
-                }
-            }
-            if (L2 >= 0) {
-                tok = __builtin_amdgcn_readlane(tok, L2);
-                tval = (double)readlane_f(tv, L2);
-            }
-        }
-        if (lane == 0) {
-            P.node_token[sb + sm.cand_node[i]] = tok;
-            sm.cand_tok[i] = tok;
-            sm.cand_p[i] = tval;
-        }
-        if (tok < 0) {
-            // nothing left to draw from: the remaining children keep token -1
-            for (int i2 = i + 1 + lane; i2 < nc; i2 += 64) P.node_token[sb + sm.cand_node[i2]] = -1;
-            break;
-        }
-        if (worep) removed += tval;
-        __builtin_amdgcn_wave_barrier();
-    }
-}
-
 // ----------------------------------------------------------- walk kernel ----
 
 __global__ void rs_walk_kernel(const int32_t* __restrict__ node_child,
@@ -1825,8 +1059,6 @@ namespace {
 
 constexpr int kWalkBlock = 256;
 
-bool aligned16(const void* p) { return (reinterpret_cast<uintptr_t>(p) & 15u) == 0; }
-
 // compute units of the current device (queried once per device)
 int cu_count() {
     static std::atomic<int> cache[64];
@@ -1839,14 +1071,6 @@ int cu_count() {
         cache[dev].store(n, std::memory_order_relaxed);
     }
     return n;
-}
-
-rs_status check_params(const rs_params* prm) {
-    if (!prm) return RS_ERR_INVALID_ARG;
-    if (prm->mode != RS_MODE_RESISPEC && prm->mode != RS_MODE_SPECINFER) return RS_ERR_INVALID_ARG;
-    if (prm->logits_dtype != RS_F32 && prm->logits_dtype != RS_BF16) return RS_ERR_INVALID_ARG;
-    if (!(prm->temperature > 0.0f) || !std::isfinite(prm->temperature)) return RS_ERR_INVALID_ARG;
-    return RS_OK;
 }
 
 // Outputs of the path schedule (NULL: all-nodes schedule).
@@ -1897,18 +1121,6 @@ hipError_t launch_rows(const KParams& P, const rs_params* prm, bool vec, int64_t
     return launch_rows_m<RS_MODE_RESISPEC>(P, prm->logits_dtype, vec, nrows, path, s);
 }
 
-template <typename In, int VEC, int UNR>
-hipError_t launch_draft_t(DParams P, hipStream_t s) {
-    constexpr int64_t CHUNK = 64 * VEC * UNR;
-    const int64_t nch = ((int64_t)P.V + CHUNK - 1) / CHUNK;
-    const int64_t G = (nch + kMaxSlots - 1) / kMaxSlots;
-    P.G = (int32_t)G;
-    P.nslots = (int32_t)((nch + G - 1) / G);
-    hipLaunchKernelGGL((rs_draft_kernel<In, VEC, UNR>), dim3((unsigned)((int64_t)P.B * P.N)), dim3(kBlock), 0,
-                       s, P);
-    return hipGetLastError();
-}
-
 bool vector_ok(const void* t, const void* d, int64_t V, int dtype) {
     const int64_t esz = dtype == RS_BF16 ? 2 : 4;
     return ((V * esz) % 16 == 0) && aligned16(t) && aligned16(d);
@@ -1920,13 +1132,7 @@ KParams base_params(const void* t, const void* d, int64_t V, const rs_params* pr
     P.dft = d;
     P.V = (int32_t)V;
     P.T = prm->temperature;
-    // c2 = c2h + c2l with c2h strictly below c2, so c2l > 0: then a -inf logit gives
-    // the exponent -inf (never -inf + inf) and contributes exactly zero.
-    const double c2 = 1.4426950408889634 / (double)prm->temperature;
-    float c2h = (float)c2;
-    if ((double)c2h >= c2) c2h = std::nextafter(c2h, 0.0f);
-    P.c2h = c2h;
-    P.c2l = (float)(c2 - (double)c2h);
+    split_c2(prm->temperature, &P.c2h, &P.c2l);
     P.worep = prm->without_replacement ? 1 : 0;
     P.bonus = prm->bonus ? 1 : 0;
     return P;
@@ -2095,46 +1301,6 @@ rs_status resispec_verify_tree_path(const void* target_logits, const void* draft
     const PathOut path{B < 2 * cu_count() ? 1 : 0, max_depth, out_tokens, out_accepted_len,
                        out_status};
     return launch_rows(P, prm, vec, B, (hipStream_t)stream, &path) == hipSuccess ? RS_OK : RS_ERR_HIP;
-}
-
-rs_status resispec_draft_candidates(const void* draft_logits, const int32_t* parent, int32_t B,
-                                    int32_t N, int32_t V, const rs_params* prm, uint64_t seed,
-                                    uint64_t offset, int32_t* node_token, float* u_accept,
-                                    float* u_resample, int32_t* out_status, void* stream) {
-    const rs_status ps = check_params(prm);
-    if (ps != RS_OK) return ps;
-    if (B < 0 || N <= 0 || V <= 0) return RS_ERR_INVALID_ARG;
-    if (V > RS_MAX_VOCAB) return RS_ERR_UNSUPPORTED;
-    if ((int64_t)B * N > 0x7fffffffLL) return RS_ERR_UNSUPPORTED;
-    if (B == 0) return RS_OK;
-    if (!draft_logits || !parent || !node_token || !u_accept || !u_resample) return RS_ERR_INVALID_ARG;
-    const KParams base = base_params(draft_logits, draft_logits, V, prm);
-    DParams P{};
-    P.dft = draft_logits;
-    P.parent = parent;
-    P.node_token = node_token;
-    P.ua = u_accept;
-    P.ur = u_resample;
-    P.out_status = out_status;
-    P.B = B;
-    P.N = N;
-    P.V = V;
-    P.c2h = base.c2h;
-    P.c2l = base.c2l;
-    P.worep = prm->without_replacement ? 1 : 0;
-    P.seed_lo = (uint32_t)seed;
-    P.seed_hi = (uint32_t)(seed >> 32);
-    P.off_lo = (uint32_t)offset;
-    P.off_hi = (uint32_t)(offset >> 32);
-    const int64_t esz = prm->logits_dtype == RS_BF16 ? 2 : 4;
-    const bool vec = ((int64_t)V * esz) % 16 == 0 && aligned16(draft_logits);
-    const hipStream_t s = (hipStream_t)stream;
-    hipError_t e;
-    if (prm->logits_dtype == RS_BF16)
-        e = vec ? launch_draft_t<uint16_t, 8, RS_UNR16>(P, s) : launch_draft_t<uint16_t, 1, 4>(P, s);
-    else
-        e = vec ? launch_draft_t<float, 4, RS_UNR32>(P, s) : launch_draft_t<float, 1, 4>(P, s);
-    return e == hipSuccess ? RS_OK : RS_ERR_HIP;
 }
 
 rs_status resispec_verify_nodes(const void* target_logits, const void* draft_logits,
