@@ -205,13 +205,14 @@ __global__ void __launch_bounds__(kBlock) __attribute__((amdgpu_waves_per_eu(4))
         }
         __syncthreads();
     }
-    if (wid != 0) return;
-
-    // ---- the draws (wave 0): inverse CDF over the slot totals, then inside one slot
+    // ---- the draws: inverse CDF over the slot totals, then inside one slot.  Draws with
+    // replacement are independent and spread over the waves; without replacement each
+    // draw depends on the tokens before it and wave 0 takes them in order.
     const bool worep = P.worep != 0;
+    if (worep && wid != 0) return;
     const int R = G * VEC * UNR;          // elements of a slot per lane
     double removed = 0.0;                 // mass drawn so far (without replacement)
-    for (int i = 0; i < nc; ++i) {
+    for (int i = worep ? 0 : wid; i < nc; i += worep ? 1 : kWaves) {
         const double thr = (double)sm.cand_u[i] * (total - removed);
         // removed tokens of each slot (lane j holds removed token j, j < i)
         const int32_t rtok = (worep && lane < i) ? sm.cand_tok[lane] : -1;
@@ -385,7 +386,7 @@ __global__ void __launch_bounds__(kBlock) __attribute__((amdgpu_waves_per_eu(4))
             sm.cand_tok[i] = tok;
             sm.cand_p[i] = tval;
         }
-        if (tok < 0) {
+        if (tok < 0 && worep) {
             // nothing left to draw from: the remaining children keep token -1
             for (int i2 = i + 1 + lane; i2 < nc; i2 += 64) P.node_token[sb + sm.cand_node[i2]] = -1;
             break;
