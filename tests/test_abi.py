@@ -124,6 +124,31 @@ def test_argument_errors_return_before_launch(native):
     assert lib.resispec_verify_tree_debug(*args, 4, 5, 100, 2, ctypes.byref(ok), i32p, i32p, None,
                                           None, 0, None, None, None, None,
                                           None) == native.RS_ERR_INVALID_ARG
+    # path schedule: same argument rules, no workspace
+    assert lib.resispec_verify_tree_path(*args, 4, 0, 100, 2, ctypes.byref(ok), i32p, i32p, None,
+                                         None) == native.RS_ERR_INVALID_ARG
+    assert lib.resispec_verify_tree_path(*args, 4, 5, 100, -1, ctypes.byref(ok), i32p, i32p, None,
+                                         None) == native.RS_ERR_INVALID_ARG
+    assert lib.resispec_verify_tree_path(*args, 4, 5, (1 << 22) + 1, 2, ctypes.byref(ok), i32p,
+                                         i32p, None, None) == native.RS_ERR_UNSUPPORTED
+    assert lib.resispec_verify_tree_path(fake, fake, i32p, i32p, fake, fake, 4, 5, 100, 2,
+                                         ctypes.byref(_prm(native, T=0.0)), i32p, i32p, None,
+                                         None) == native.RS_ERR_INVALID_ARG
+    assert lib.resispec_verify_tree_path(None, None, None, None, None, None, 0, 5, 100, 2,
+                                         ctypes.byref(ok), None, None, None, None) == native.RS_OK
+    # draft step
+    f32p = fake
+    assert lib.resispec_draft_candidates(fake, i32p, 4, 5, 100, ctypes.byref(ok), 1, 0, None, f32p,
+                                         f32p, None, None) == native.RS_ERR_INVALID_ARG
+    assert lib.resispec_draft_candidates(fake, i32p, 4, 0, 100, ctypes.byref(ok), 1, 0, i32p,
+                                         f32p, f32p, None, None) == native.RS_ERR_INVALID_ARG
+    assert lib.resispec_draft_candidates(fake, i32p, 4, 5, (1 << 22) + 1, ctypes.byref(ok), 1, 0,
+                                         i32p, f32p, f32p, None, None) == native.RS_ERR_UNSUPPORTED
+    assert lib.resispec_draft_candidates(fake, i32p, 4, 5, 100, ctypes.byref(_prm(native, dtype=9)),
+                                         1, 0, i32p, f32p, f32p, None,
+                                         None) == native.RS_ERR_INVALID_ARG
+    assert lib.resispec_draft_candidates(None, None, 0, 5, 100, ctypes.byref(ok), 1, 0, None, None,
+                                         None, None, None) == native.RS_OK
 
 
 def test_product_path_has_no_oracle_dependency():

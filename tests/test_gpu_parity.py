@@ -336,3 +336,26 @@ def test_stream_ordering(gpu_lib):
             temperature=w["temperature"], max_depth=w["max_depth"], stream=s)
     s.synchronize()
     assert torch.equal(t, ref["tokens"]) and torch.equal(l, ref["accepted_len"])
+
+
+def test_max_vocab(gpu_lib):
+    """V = RS_MAX_VOCAB (2^22): slots of many chunks, draws that re-read a slot from
+    memory instead of registers; both schedules and the draft step."""
+    V = 1 << 22
+    g = torch.Generator(device="cuda").manual_seed(22)
+    par = torch.tensor([[-1, 0, 0, 1]], dtype=torch.int32, device="cuda").repeat(2, 1)
+    B, N = par.shape
+    t = (2.0 * torch.randn((B, N, V), generator=g, device="cuda")).to(torch.bfloat16)
+    d = (t.float() + torch.randn((B, N, V), generator=g, device="cuda")).to(torch.bfloat16)
+    tok, ua, ur, st = gpu_lib.resispec_draft_candidates(d, par, temperature=1.0, seed=4)
+    w = dict(target=t, draft=d, node_token=tok, parent=par, u_accept=ua, u_resample=ur,
+             temperature=1.0, without_replacement=False, max_depth=2)
+    h = host_tree(w)
+    for mode in MODES:
+        gpu = gpu_tree(gpu_lib, w, mode, debug=True)
+        compare_walk(gpu, oracle_walk(h, w, mode))
+        compare_nodes(gpu, h, w, mode)
+        t2, l2, s2 = gpu_lib.resispec_verify_tree_path(
+            t, d, tok, par, ua, ur, temperature=1.0, max_depth=2, mode=mode)
+        torch.cuda.synchronize()
+        assert torch.equal(t2, gpu["tokens"]) and torch.equal(l2, gpu["accepted_len"])
