@@ -267,6 +267,55 @@ struct Smem {
     int32_t res_child, res_tok, res_status;
 };
 
+// Per-slot sums of the lane partials of a pass, in a fixed order, so the totals are
+// bitwise reproducible whatever wave processed which slot.  Stage 1 (every thread):
+// thread t adds lanes [g*GS, g*GS + GS) of slot t % kMaxSlots, g = t / kMaxSlots, in
+// fp64 and parks the sum in rows g*GS and g*GS + 1 of that column as two 32-bit
+// halves (no other thread touches those cells).  Stage 2, after a barrier
+// (slot_group_sum): the NG group sums of one slot are added in group order.
+template <int BLK>
+struct SlotGroups {
+    static constexpr int NG = BLK / kMaxSlots;
+    static constexpr int GS = 64 / NG;
+    static_assert(NG >= 1 && NG * kMaxSlots == BLK && NG * GS == 64 && GS >= 2,
+                  "the block must split the 64 lanes into equal groups per slot");
+};
+
+__device__ __forceinline__ void park_double(float (&part)[64][kMaxSlots + 1], int r, int s, double v) {
+    const unsigned long long bits = (unsigned long long)__double_as_longlong(v);
+    part[r][s] = __uint_as_float((uint32_t)bits);
+    part[r + 1][s] = __uint_as_float((uint32_t)(bits >> 32));
+}
+
+template <int BLK>
+__device__ __forceinline__ void slot_sums_stage1(Smem& sm, int nslots, bool wantB) {
+    using SG = SlotGroups<BLK>;
+    const int s = threadIdx.x % kMaxSlots, g = threadIdx.x / kMaxSlots;
+    if (s >= nslots) return;
+    double a = 0.0, c = 0.0;
+#pragma unroll
+    for (int l = 0; l < SG::GS; ++l) a += (double)sm.partA[g * SG::GS + l][s];
+    if (wantB) {
+#pragma unroll
+        for (int l = 0; l < SG::GS; ++l) c += (double)sm.partB[g * SG::GS + l][s];
+    }
+    park_double(sm.partA, g * SG::GS, s, a);
+    if (wantB) park_double(sm.partB, g * SG::GS, s, c);
+}
+
+template <int BLK>
+__device__ __forceinline__ double slot_group_sum(const float (&part)[64][kMaxSlots + 1], int s) {
+    using SG = SlotGroups<BLK>;
+    double v = 0.0;
+#pragma unroll
+    for (int g = 0; g < SG::NG; ++g) {
+        const uint32_t lo = __float_as_uint(part[g * SG::GS][s]);
+        const uint32_t hi = __float_as_uint(part[g * SG::GS + 1][s]);
+        v += __longlong_as_double((long long)(((unsigned long long)hi << 32) | lo));
+    }
+    return v;
+}
+
 // Exponent reference for a maximum m: an integer-valued float near -m * c2, so that
 // the fp32 exponents near the maximum are small and exactly offset, and a shift of
 // the reference by an integer (the first-rejection split of log2 c) stays exact.

@@ -157,12 +157,9 @@ __global__ void __launch_bounds__(kBlock) __attribute__((amdgpu_waves_per_eu(4))
                 fa = 0.0f;
             });
         __syncthreads();
-        if (tid < nslots) {
-            double a = 0.0;
-#pragma unroll 8
-            for (int l = 0; l < 64; ++l) a += (double)sm.partA[l][tid];
-            sm.slotA[tid] = a;
-        }
+        slot_sums_stage1<kBlock>(sm, nslots, false);
+        __syncthreads();
+        if (tid < nslots) sm.slotA[tid] = slot_group_sum<kBlock>(sm.partA, tid);
         __syncthreads();
         if (wid == 0) {
             double a0 = 0.0;

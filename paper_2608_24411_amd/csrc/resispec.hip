@@ -195,8 +195,8 @@ __device__ __forceinline__ void verify_row(const KParams& P, Smem& sm, const int
     for (int u = 0; u < UNR; ++u) pre[u] = W::template load<kNtPass1>(tg, wid * G * CHUNK + lane * VEC + u * 64 * VEC, V);
 
     // ---- row description.  "Holder" threads own one candidate each: node, token and
-    // uniform now; the two logits of its token are gathered while pass 1 streams and
-    // written to shared memory after it.
+    // uniform, then the two logits of its token and their unnormalised masses, all
+    // written to shared memory before pass 1 starts.
     if (tid == 0) {
         sm.decision = -1;
         sm.next_slot = kWaves;
@@ -313,7 +313,7 @@ __device__ __forceinline__ void verify_row(const KParams& P, Smem& sm, const int
         return;
     }
     if (tid == 0) sm.status = RS_SEQ_OK;
-    // candidate logits: requested now, consumed after pass 1
+    // candidate logits (their latency overlaps the first chunk's)
     float hlt = 0.0f, hld = 0.0f;
     if (holder && hrank < kMaxCand && hx >= 0 && hx < V) {
         hlt = widen(tg[hx]);
@@ -334,6 +334,26 @@ __device__ __forceinline__ void verify_row(const KParams& P, Smem& sm, const int
         float m0 = -FLT_MAX;
         for (int w = 0; w < kWaves; ++w) m0 = fmaxf(m0, sm.wmax[0][w]);
         Kt = Kd = kref(m0, c2h);
+    }
+    // The candidates' unnormalised masses need only the exponent references: holders
+    // compute them (fp64) now, off the critical path after pass 1; the division by the
+    // sums follows the pass.  Rows that take the exact-maximum pass recompute them.
+    const double c2d = (double)c2h + (double)c2l;
+    const bool holders = P.flat || P.N <= kBlock;
+    bool refixed = false;
+    if (holder && hrank < kMaxCand) {
+        double pe = 0.0, qe = 0.0;
+        if (hx >= 0 && hx < V) {
+            pe = exp2((double)hlt * c2d + (double)Kt);
+            qe = exp2((double)hld * c2d + (double)Kd);
+        }
+        sm.cand_tok[hrank] = hx;
+        sm.cand_u[hrank] = hu;
+        sm.cand_node[hrank] = hnode;
+        sm.cand_lt[hrank] = hlt;
+        sm.cand_ld[hrank] = hld;
+        sm.cand_p[hrank] = pe;
+        sm.cand_q[hrank] = qe;
     }
     for (int attempt = 0;; ++attempt) {
         float fa = 0.0f, fc = 0.0f;   // this slot's lane partials
@@ -367,27 +387,16 @@ __device__ __forceinline__ void verify_row(const KParams& P, Smem& sm, const int
         if (attempt == 0) {
             RS_STAMP(row, 2);
 #ifdef RS_TIMING
-            if (lane == 0 && g_timing) g_timing[row * 16 + 8 + wid] = wall_clock64();   // per-wave end
+            if (lane == 0 && wid < 8 && g_timing) g_timing[row * 16 + 8 + wid] = wall_clock64();   // per-wave end (waves 0-7)
 #endif
-            if (holder && hrank < kMaxCand) {
-                sm.cand_tok[hrank] = hx;
-                sm.cand_u[hrank] = hu;
-                sm.cand_node[hrank] = hnode;
-                sm.cand_lt[hrank] = hlt;
-                sm.cand_ld[hrank] = hld;
-            }
         }
         __syncthreads();
+        slot_sums_stage1<BLK>(sm, nslots, internal);
+        __syncthreads();
         if (tid < nslots) {
-            double a = 0.0, c = 0.0;
-#pragma unroll 8
-            for (int l = 0; l < 64; ++l) a += (double)sm.partA[l][tid];
-            if (internal) {
-#pragma unroll 8
-                for (int l = 0; l < 64; ++l) c += (double)sm.partB[l][tid];
-            }
+            const double a = slot_group_sum<BLK>(sm.partA, tid);
             sm.slotA[tid] = a;
-            sm.slotB[tid] = c;
+            sm.slotB[tid] = internal ? slot_group_sum<BLK>(sm.partB, tid) : 0.0;
             sm.slotP[tid] = a;
         }
         __syncthreads();
@@ -443,6 +452,7 @@ __device__ __forceinline__ void verify_row(const KParams& P, Smem& sm, const int
             }
             Kt = kref(m0, c2h);
             Kd = kref(m1, c2h);
+            refixed = true;
             if (tid == 0) {
                 sm.decision = -1;
                 sm.next_slot = kWaves;
@@ -451,7 +461,6 @@ __device__ __forceinline__ void verify_row(const KParams& P, Smem& sm, const int
         }
     }
 
-    const double c2d = (double)c2h + (double)c2l;
     const double St = sm.St, Sd = sm.Sd;
     // draft mass in target units: q St / Sd, folded into the step constants
     const double q2t = internal ? St / Sd : 0.0;
@@ -461,8 +470,11 @@ __device__ __forceinline__ void verify_row(const KParams& P, Smem& sm, const int
         const int32_t x = sm.cand_tok[tid];
         double pc = 0.0, qc = 0.0;
         if (x >= 0 && x < V) {
-            pc = exp2((double)sm.cand_lt[tid] * c2d + (double)Kt) / St;
-            qc = exp2((double)sm.cand_ld[tid] * c2d + (double)Kd) / Sd;
+            const bool early = holders && !refixed;
+            const double pe = early ? sm.cand_p[tid] : exp2((double)sm.cand_lt[tid] * c2d + (double)Kt);
+            const double qe = early ? sm.cand_q[tid] : exp2((double)sm.cand_ld[tid] * c2d + (double)Kd);
+            pc = pe / St;
+            qc = qe / Sd;
         }
         sm.cand_p[tid] = pc;
         sm.cand_q[tid] = qc;
@@ -644,16 +656,14 @@ __device__ __forceinline__ void verify_row(const KParams& P, Smem& sm, const int
             }
         }
         __syncthreads();
-        if (tid < nslots) {
-            double a = 0.0, c = 0.0;
-#pragma unroll 8
-            for (int l = 0; l < 64; ++l) a += (double)sm.partA[l][tid];
-            if (MODE == RS_MODE_RESISPEC && i > 0) {
-#pragma unroll 8
-                for (int l = 0; l < 64; ++l) c += (double)sm.partB[l][tid];
+        {
+            const bool wantB = MODE == RS_MODE_RESISPEC && i > 0;
+            slot_sums_stage1<BLK>(sm, nslots, wantB);
+            __syncthreads();
+            if (tid < nslots) {
+                sm.slotA[tid] = slot_group_sum<BLK>(sm.partA, tid);
+                sm.slotB[tid] = wantB ? slot_group_sum<BLK>(sm.partB, tid) : 0.0;
             }
-            sm.slotA[tid] = a;
-            sm.slotB[tid] = c;
         }
         __syncthreads();
         if (wid == 0) {
