@@ -10,7 +10,9 @@ resident in HBM.  Prints one JSON line.
 The metric is verified tree-node rows per second (B * N / step time) at V = 128,256;
 `roofline.achieved` is the row kernel's algorithmic bytes (every target row once, the
 draft row of every node with children once, plus ids/uniforms/outcomes) divided by its
-average launch duration measured with HIP events on the launch stream.
+average launch duration measured with HIP events on the launch stream.  The read probe
+(libresispec_probe.so) measures the device's achievable read rate beside it:
+`roofline.frac_of_read_ceiling` is the achieved figure over the nontemporal stream rate.
 """
 import argparse
 import hashlib
@@ -76,6 +78,42 @@ def cpu_baseline(w, seconds, mode):
     return {"value": rows_done / t_used, "unit": "rows/s", "cores": 1, "kind": "oracle",
             "sample": "%d of %d sequences (%d node rows) of %s, every node evaluated, fp64, "
                       "one thread, %.1f s CPU" % (seqs, B, rows_done, w["cfg"]["name"], t_used)}
+
+
+def read_ceiling(torch, chunk=1 << 19, nbytes=4 << 30, reps=5):
+    """The device's achievable read bandwidth from the read probe library: a stream of
+    nbytes with ordinary and with nontemporal 16-byte loads (one chunk of `chunk` bytes
+    per 512-thread workgroup, about one bf16 row pair of the benchmarked workload), and a
+    stream followed by a reversed nontemporal re-read of every chunk (2 * nbytes read)."""
+    import ctypes
+    lib = ctypes.CDLL(os.path.join(ROOT, "paper_2608_24411_amd", "libresispec_probe.so"))
+    fn = lib.resispec_probe_read
+    fn.restype = ctypes.c_int
+    fn.argtypes = [ctypes.c_void_p, ctypes.c_int64, ctypes.c_int32, ctypes.c_int32,
+                   ctypes.c_int32, ctypes.c_void_p, ctypes.c_void_p]
+    src = torch.ones(nbytes // 4, dtype=torch.int32, device="cuda")
+    sink = torch.zeros(nbytes // chunk, dtype=torch.int32, device="cuda")
+    stream = ctypes.c_void_p(torch.cuda.current_stream().cuda_stream)
+    out = {"bytes": nbytes, "chunk_bytes": chunk}
+    for name, policy, passes in (("plain_stream_gbps", 0, 1), ("nt_stream_gbps", 1, 1),
+                                 ("plain_then_nt_reread_gbps", 0, 2)):
+        def run():
+            rc = fn(ctypes.c_void_p(src.data_ptr()), nbytes, chunk, policy, passes,
+                    ctypes.c_void_p(sink.data_ptr()), stream)
+            if rc != 0:
+                raise RuntimeError("resispec_probe_read failed (%d)" % rc)
+        run()
+        torch.cuda.synchronize()
+        e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+        e0.record()
+        for _ in range(reps):
+            run()
+        e1.record()
+        torch.cuda.synchronize()
+        out[name] = passes * nbytes / (e0.elapsed_time(e1) / reps * 1e-3) / 1e9
+    del src, sink
+    torch.cuda.empty_cache()
+    return out
 
 
 def time_mode(native, torch, w, mode, steps, warmup, settle, ws, out_tok, out_len, out_st):
@@ -197,6 +235,8 @@ def main():
     ap.add_argument("--no-other-mode", action="store_true")
     ap.add_argument("--no-path", action="store_true", help="skip the path-only schedule")
     ap.add_argument("--no-draft", action="store_true", help="skip the draft step")
+    ap.add_argument("--no-read-probe", action="store_true",
+                    help="skip the read-bandwidth probe (the measured ceiling)")
     ap.add_argument("--study", action="store_true",
                     help="only run the synthetic acceptance studies (not a benchmark)")
     ap.add_argument("--copy-probe", type=int, default=0, metavar="MIB",
@@ -343,8 +383,11 @@ def main():
         draft = {"kernel_ms": dms, "rows_per_s": B * N / (dms * 1e-3),
                  "alg_bytes_per_launch": d_bytes, "achieved_gbps": d_bytes / (dms * 1e-3) / 1e9}
 
+    probe = None if args.no_read_probe else read_ceiling(torch)
+
     r = results[args.mode]
     achieved = r["row_kernel_gbps"]
+    traffic = measured_traffic(w["cfg"]["name"], args.mode)
     out = {
         "metric": METRIC,
         "value": r["rows_per_s"],
@@ -364,9 +407,16 @@ def main():
                    "without_replacement": bool(w["without_replacement"])},
         "roofline": {"bound": "hbm", "achieved": achieved, "peak": HBM_PEAK_GBPS, "unit": "GB/s",
                      "frac": achieved / HBM_PEAK_GBPS,
-                     "traffic": measured_traffic(w["cfg"]["name"], args.mode),
+                     "traffic": traffic,
                      "kernel": "rs_row_kernel", "alg_bytes_per_launch": alg_bytes,
-                     "rows_target": rows_t, "rows_draft": rows_d},
+                     "rows_target": rows_t, "rows_draft": rows_d,
+                     # HBM traffic (counters) per second, against the measured read ceiling
+                     "traffic_gbps": (traffic / (r["row_kernel_ms"] * 1e-3) / 1e9
+                                      if traffic else None),
+                     "read_ceiling_gbps": probe["nt_stream_gbps"] if probe else None,
+                     "frac_of_read_ceiling": (achieved / probe["nt_stream_gbps"]
+                                              if probe else None)},
+        "read_probe": probe,
         "modes": results,
         "path_schedule": path,
         "draft_step": draft,

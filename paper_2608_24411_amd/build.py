@@ -1,4 +1,5 @@
-"""Build libresispec.so (gfx950) in-tree with hipcc."""
+"""Build libresispec.so and the benchmark's read probe libresispec_probe.so (gfx950) in-tree
+with hipcc."""
 import os
 import subprocess
 import sys
@@ -7,6 +8,9 @@ HERE = os.path.dirname(os.path.abspath(__file__))
 ROOT = os.path.dirname(HERE)
 SRCS = [os.path.join(HERE, "csrc", "resispec.hip"), os.path.join(HERE, "csrc", "draft.hip")]
 LIB = os.path.join(HERE, "libresispec.so")
+# the benchmark's read-bandwidth probe, a library of its own
+PROBE_SRCS = [os.path.join(HERE, "csrc", "probe.hip")]
+PROBE_LIB = os.path.join(HERE, "libresispec_probe.so")
 HIPCC = os.environ.get("HIPCC", "/opt/rocm/bin/hipcc")
 
 FLAGS = [
@@ -17,13 +21,18 @@ FLAGS = [
 ]
 
 
-def build(verbose: bool = False) -> str:
-    tmp = LIB + ".tmp%d" % os.getpid()
-    cmd = [HIPCC] + FLAGS + ["-I", os.path.join(ROOT, "include"), "-o", tmp] + SRCS
+def _compile(srcs, lib, verbose):
+    tmp = lib + ".tmp%d" % os.getpid()
+    cmd = [HIPCC] + FLAGS + ["-I", os.path.join(ROOT, "include"), "-o", tmp] + srcs
     if verbose:
         print(" ".join(cmd), flush=True)
     subprocess.run(cmd, check=True)
-    os.replace(tmp, LIB)
+    os.replace(tmp, lib)
+
+
+def build(verbose: bool = False) -> str:
+    _compile(SRCS, LIB, verbose)
+    _compile(PROBE_SRCS, PROBE_LIB, verbose)
     return LIB
 
 

@@ -159,3 +159,22 @@ def test_product_path_has_no_oracle_dependency():
             if fn.endswith((".py", ".hip", ".cpp", ".h")):
                 text = open(os.path.join(dirpath, fn)).read()
                 assert "oracle" not in text.lower(), os.path.join(dirpath, fn)
+
+
+def test_read_probe_library_rejects_bad_arguments():
+    """The benchmark's read probe (a library of its own) loads and checks its arguments
+    before any launch."""
+    lib = ctypes.CDLL(os.path.join(ROOT, "paper_2608_24411_amd", "libresispec_probe.so"))
+    fn = lib.resispec_probe_read
+    fn.restype = ctypes.c_int
+    fn.argtypes = [ctypes.c_void_p, ctypes.c_int64, ctypes.c_int32, ctypes.c_int32,
+                   ctypes.c_int32, ctypes.c_void_p, ctypes.c_void_p]
+    p = ctypes.c_void_p(4096)   # never dereferenced: every call below fails its checks
+    q = 1 << 15                 # the chunk quantum (32 KiB)
+    assert fn(None, 4 * q, q, 0, 1, p, None) == 1          # null source
+    assert fn(p, 4 * q, q, 0, 1, None, None) == 1          # null sink
+    assert fn(p, 0, q, 0, 1, p, None) == 1                 # empty buffer
+    assert fn(p, 4 * q, q + 16, 0, 1, p, None) == 1        # chunk not a multiple of 32 KiB
+    assert fn(p, 5 * q, 2 * q, 0, 1, p, None) == 1         # chunk does not divide the buffer
+    assert fn(p, 4 * q, q, 2, 1, p, None) == 1             # unknown load policy
+    assert fn(p, 4 * q, q, 0, 3, p, None) == 1             # unknown pass count
