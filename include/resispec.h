@@ -54,7 +54,8 @@ typedef enum {
     RS_OK = 0,
     RS_ERR_INVALID_ARG = 1,  /* NULL pointer, non-positive size, T <= 0, unknown mode/dtype */
     RS_ERR_WORKSPACE = 2,    /* workspace NULL or smaller than resispec_workspace_bytes() */
-    RS_ERR_UNSUPPORTED = 3,  /* size beyond RS_MAX_VOCAB / RS_MAX_CANDIDATES */
+    RS_ERR_UNSUPPORTED = 3,  /* size beyond RS_MAX_VOCAB / RS_MAX_CANDIDATES, or a row
+                                group that cannot run on this device */
     RS_ERR_HIP = 4           /* a HIP launch error */
 } rs_status;
 
@@ -67,7 +68,9 @@ typedef enum {
     RS_SEQ_BAD_TREE = 4,         /* parent[.,0] != -1 or parent[n] not in [0, n) */
     RS_SEQ_BAD_UNIFORM = 5,      /* a used uniform outside [0, 1) */
     RS_SEQ_DEPTH_EXCEEDED = 6,   /* accepted path longer than max_depth */
-    RS_SEQ_TOO_MANY_CHILDREN = 7 /* a node with more than RS_MAX_CANDIDATES children */
+    RS_SEQ_TOO_MANY_CHILDREN = 7, /* a node with more than RS_MAX_CANDIDATES children */
+    RS_SEQ_GROUP_TIMEOUT = 8     /* path schedule with row groups: the workgroups of a
+                                    sequence did not meet at a barrier within 20 ms */
 } rs_seq_status;
 
 typedef enum { RS_MODE_RESISPEC = 0, RS_MODE_SPECINFER = 1 } rs_mode;
@@ -152,6 +155,44 @@ rs_status resispec_verify_tree_path(const void* target_logits, const void* draft
                                     int32_t B, int32_t N, int32_t V, int32_t max_depth,
                                     const rs_params* prm, int32_t* out_tokens,
                                     int32_t* out_accepted_len, int32_t* out_status, void* stream);
+
+/*
+ * The path-only schedule with row groups, for batches too small to fill the device with
+ * one workgroup per sequence (same results as resispec_verify_tree_path and
+ * resispec_verify_tree, bit for bit).  Each sequence gets `group_size` 1024-thread
+ * workgroups that verify every row of its walk together: each sweeps its share of the
+ * row's slots in every pass, and after a pass they exchange their slots' totals through
+ * `workspace` and meet at a barrier (a counter in global memory; all workgroups of the
+ * launch are resident at once by a cooperative launch, and each wait is bounded: a
+ * sequence whose workgroups do not meet within 20 ms reports RS_SEQ_GROUP_TIMEOUT).
+ *   group_size      : 0 = automatic (as many members as the device holds at once, up to
+ *                     16 and to one per 16 slots of a row; 1 when that is under 2 or
+ *                     workspace is NULL), 1 = one workgroup per sequence,
+ *                     2..16 = that many (RS_ERR_UNSUPPORTED if B * group_size workgroups
+ *                     cannot be resident at once, if the batch takes the 512-thread
+ *                     schedule (B >= 2 per CU), or if a row has fewer slots than members)
+ *   workspace       : device buffer of at least resispec_path_workspace_bytes(B) bytes,
+ *                     16-byte aligned, caller-owned; its counters are zeroed by the call
+ *                     itself (on `stream`) before the verification kernel; NULL allowed
+ *                     when group_size is 0 or 1.  Calls that overlap on one workspace race.
+ * Other arguments, outputs and statuses as resispec_verify_tree_path.
+ */
+rs_status resispec_verify_tree_path_group(const void* target_logits, const void* draft_logits,
+                                          const int32_t* node_token, const int32_t* parent,
+                                          const float* u_accept, const float* u_resample,
+                                          int32_t B, int32_t N, int32_t V, int32_t max_depth,
+                                          const rs_params* prm, int32_t* out_tokens,
+                                          int32_t* out_accepted_len, int32_t* out_status,
+                                          int32_t group_size, void* workspace,
+                                          size_t workspace_bytes, void* stream);
+
+/* Workspace bytes resispec_verify_tree_path_group needs for B sequences (0 if B <= 0). */
+size_t resispec_path_workspace_bytes(int32_t B);
+
+/* The group size resispec_verify_tree_path_group chooses with group_size = 0 for B
+ * sequences of V-element rows (16-byte aligned rows assumed), on the current device;
+ * -1 for invalid arguments.  Host only: launches nothing. */
+int32_t resispec_path_group_size(int32_t B, int32_t V, const rs_params* prm);
 
 /*
  * The draft step that precedes verification (Preliminary: candidates are drawn from the

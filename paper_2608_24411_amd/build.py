@@ -1,6 +1,7 @@
 """Build libresispec.so and the benchmark's read probe libresispec_probe.so (gfx950) in-tree
 with hipcc."""
 import os
+import re
 import subprocess
 import sys
 
@@ -21,12 +22,47 @@ FLAGS = [
 ]
 
 
+def _spills(report):
+    """Functions whose registers spill to scratch memory, from the compiler's resource
+    remarks: [(name, vgpr_spills, scratch_bytes_per_lane)]."""
+    bad, name, scratch = [], None, 0
+    for line in report.splitlines():
+        m = re.search(r"Function Name: (\S+)", line)
+        if m:
+            name, scratch = m.group(1), 0
+            continue
+        m = re.search(r"ScratchSize \[bytes/lane\]: (\d+)", line)
+        if m:
+            scratch = int(m.group(1))
+            continue
+        m = re.search(r"VGPRs Spill: (\d+)", line)
+        if m and name and (int(m.group(1)) > 0 or scratch > 0):
+            bad.append((name, int(m.group(1)), scratch))
+    return bad
+
+
 def _compile(srcs, lib, verbose):
     tmp = lib + ".tmp%d" % os.getpid()
-    cmd = [HIPCC] + FLAGS + ["-I", os.path.join(ROOT, "include"), "-o", tmp] + srcs
+    cmd = ([HIPCC] + FLAGS + ["-Rpass-analysis=kernel-resource-usage", "-I",
+                              os.path.join(ROOT, "include"), "-o", tmp] + srcs)
     if verbose:
         print(" ".join(cmd), flush=True)
-    subprocess.run(cmd, check=True)
+    r = subprocess.run(cmd, capture_output=True, text=True)
+    other = [l for l in r.stderr.splitlines()
+             if "kernel-resource-usage" not in l and "packed-fp32-ops" not in l and l.strip()]
+    if r.returncode != 0:
+        sys.stderr.write("\n".join(other) + "\n")
+        raise subprocess.CalledProcessError(r.returncode, cmd)
+    if verbose and other:
+        print("\n".join(other), flush=True)
+    # A register spilled inside a branch that only some lanes take is stored for those
+    # lanes alone; a value that other lanes still hold would come back from stale
+    # scratch.  Every kernel is built to fit its registers, and the build checks it.
+    bad = _spills(r.stderr)
+    if bad:
+        os.remove(tmp)
+        raise RuntimeError("registers spill to scratch in: " +
+                           ", ".join("%s (%d VGPRs, %d B/lane)" % b for b in bad))
     os.replace(tmp, lib)
 
 

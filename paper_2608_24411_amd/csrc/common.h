@@ -20,8 +20,7 @@ namespace {
 #define RS_BLOCK 512
 #endif
 constexpr int kBlock = RS_BLOCK;          // threads per row workgroup (all-nodes schedule)
-constexpr int kBlockWide = 1024;         // path schedule with few sequences: one workgroup per CU
-constexpr int kMaxWaves = kBlockWide / 64;
+constexpr int kMaxWaves = 16;            // waves per workgroup at most
 constexpr int kMaxCand = RS_MAX_CANDIDATES;
 #ifndef RS_MAX_SLOTS
 #define RS_MAX_SLOTS 128
@@ -263,15 +262,16 @@ struct Smem {
     // draw
     int32_t token;
     double total;
+    int32_t group_ok;               // the last barrier of a row group completed in time
     // outcome of the row (path schedule)
     int32_t res_child, res_tok, res_status;
 };
 
 // Per-slot sums of the lane partials of a pass, in a fixed order, so the totals are
-// bitwise reproducible whatever wave processed which slot.  Stage 1 (every thread):
-// thread t adds lanes [g*GS, g*GS + GS) of slot t % kMaxSlots, g = t / kMaxSlots, in
-// fp64 and parks the sum in rows g*GS and g*GS + 1 of that column as two 32-bit
-// halves (no other thread touches those cells).  Stage 2, after a barrier
+// bitwise reproducible whatever wave processed which slot.  Stage 1 (every thread, for
+// the slots in [s_lo, s_hi)): thread t adds lanes [g*GS, g*GS + GS) of slot
+// t % kMaxSlots, g = t / kMaxSlots, in fp64 and parks the sum in rows g*GS and
+// g*GS + 1 of that column as two 32-bit halves (no other thread touches those cells).  Stage 2, after a barrier
 // (slot_group_sum): the NG group sums of one slot are added in group order.
 template <int BLK>
 struct SlotGroups {
@@ -288,10 +288,10 @@ __device__ __forceinline__ void park_double(float (&part)[64][kMaxSlots + 1], in
 }
 
 template <int BLK>
-__device__ __forceinline__ void slot_sums_stage1(Smem& sm, int nslots, bool wantB) {
+__device__ __forceinline__ void slot_sums_stage1(Smem& sm, int s_lo, int s_hi, bool wantB) {
     using SG = SlotGroups<BLK>;
     const int s = threadIdx.x % kMaxSlots, g = threadIdx.x / kMaxSlots;
-    if (s >= nslots) return;
+    if (s < s_lo || s >= s_hi) return;
     double a = 0.0, c = 0.0;
 #pragma unroll
     for (int l = 0; l < SG::GS; ++l) a += (double)sm.partA[g * SG::GS + l][s];
@@ -357,10 +357,11 @@ __device__ __forceinline__ void load_chunk(const In* __restrict__ tg, const In* 
 // body(t, d, idx0, slot) gets the unpacked elements
 // of a chunk (element (u, e) has index idx0 + u * 64 * VEC + e); flush(slot) runs
 // after a slot's last chunk.  reverse: slots in descending order, chunks descending
-// inside a slot.
+// inside a slot.  The sweep covers slots [sbase, sbase + nslots) of the row (a share of
+// them when several workgroups verify one row; the waves' first slots are sbase + w).
 template <typename In, int VEC, int UNR, bool PAIR, int PRE, bool NT, typename Body, typename Flush>
 __device__ __forceinline__ void wave_sweep(const In* __restrict__ tg, const In* __restrict__ dg,
-                                           int V, int G, int nslots, bool reverse,
+                                           int V, int G, int nslots, int sbase, bool reverse,
                                            const typename Vec<In, VEC>::raw (&pre_t)[UNR],
                                            const typename Vec<In, VEC>::raw (&pre_d)[UNR],
                                            int* counter, Body&& body, Flush&& flush) {
@@ -374,14 +375,14 @@ __device__ __forceinline__ void wave_sweep(const In* __restrict__ tg, const In* 
     auto chunk_start = [&](int slot, int j) -> int {
         return (slot * G + (reverse ? G - 1 - j : j)) * CHUNK;
     };
-    int slot = wid < nslots ? (reverse ? nslots - 1 - wid : wid) : -1;
+    int slot = wid < nslots ? sbase + (reverse ? nslots - 1 - wid : wid) : -1;
     if (slot < 0) return;
     // the counter is read one slot ahead, so its latency overlaps a chunk's work
     auto take = [&]() -> int {
         int v = 0;
         if (lane == 0) v = atomicAdd(counter, 1);
         v = __builtin_amdgcn_readfirstlane(v);
-        return v < nslots ? (reverse ? nslots - 1 - v : v) : -1;
+        return v < nslots ? sbase + (reverse ? nslots - 1 - v : v) : -1;
     };
     int ahead = take();
     auto advance = [&](int& s, int& j) {

@@ -145,7 +145,7 @@ __global__ void __launch_bounds__(kBlock) __attribute__((amdgpu_waves_per_eu(4))
     double total = 0.0;
     for (int attempt = 0;; ++attempt) {
         float fa = 0.0f;
-        wave_sweep<In, VEC, UNR, false, 1, true>(dg, dg, V, G, nslots, false, pre, pre, &sm.next_slot,
+        wave_sweep<In, VEC, UNR, false, 1, true>(dg, dg, V, G, nslots, 0, false, pre, pre, &sm.next_slot,
             [&](const float (&t)[UNR][VEC], const float (&)[UNR][VEC], int, int) {
 #pragma unroll
                 for (int u = 0; u < UNR; ++u)
@@ -157,7 +157,7 @@ __global__ void __launch_bounds__(kBlock) __attribute__((amdgpu_waves_per_eu(4))
                 fa = 0.0f;
             });
         __syncthreads();
-        slot_sums_stage1<kBlock>(sm, nslots, false);
+        slot_sums_stage1<kBlock>(sm, 0, nslots, false);
         __syncthreads();
         if (tid < nslots) sm.slotA[tid] = slot_group_sum<kBlock>(sm.partA, tid);
         __syncthreads();
@@ -182,7 +182,7 @@ __global__ void __launch_bounds__(kBlock) __attribute__((amdgpu_waves_per_eu(4))
             return;
         }
         float mx = -FLT_MAX;
-        wave_sweep<In, VEC, UNR, false, 0, false>(dg, dg, V, G, nslots, false, pre, pre, &sm.next_slot,
+        wave_sweep<In, VEC, UNR, false, 0, false>(dg, dg, V, G, nslots, 0, false, pre, pre, &sm.next_slot,
             [&](const float (&t)[UNR][VEC], const float (&)[UNR][VEC], int, int) {
 #pragma unroll
                 for (int u = 0; u < UNR; ++u)

@@ -171,9 +171,98 @@ __device__ double scalar_residual(const Smem& sm, int i, double p, double q, int
 // Verification of one node row by the whole workgroup: node n of sequence b (row
 // b * N + n; flat rows: b = row, n = 0).  emit(child, token, status) is called by
 // thread 0 once, with the node's outcome.
-template <typename In, int VEC, int UNR, int MODE, int BLK, typename Emit>
+// Workgroups that verify one row together (the path schedule with few sequences, one
+// workgroup per CU): member w of S sweeps slots [w * nslots / S, (w + 1) * nslots / S)
+// in every pass; after a pass the members publish their slots' totals in global memory
+// and meet at a barrier, then all continue from the same totals in the same order, so
+// each decision is taken identically by every member.  S = 1: one workgroup per row.
+struct RowGroup {
+    int32_t S, w;      // members, this member
+    uint32_t* ctr;     // arrivals at this sequence's barriers (zero before the launch)
+    double* xbuf;      // [2 (barrier parity)][2 (first sum, second sum)][kMaxSlots]
+    float* xmax;       // [S][2]: the members' maxima of the target and draft rows
+    uint32_t epoch;    // barriers passed so far (the same count in every member)
+};
+
+// per-sequence workspace of a row group: counter, slot totals, maxima
+constexpr int64_t kGroupStride = 4608;
+constexpr int64_t kGroupXbuf = 256;
+constexpr int64_t kGroupXmax = kGroupXbuf + 2 * 2 * kMaxSlots * (int64_t)sizeof(double);
+constexpr int32_t kMaxGroup = 16;
+static_assert(kGroupXmax + 2 * kMaxGroup * (int64_t)sizeof(float) <= kGroupStride, "group workspace layout");
+
+// Barrier of a row group with a time limit (20 ms of the 100 MHz wall clock): false if
+// the other members did not arrive in time, so every workgroup ends whatever happens
+// to the others (the row then reports RS_SEQ_GROUP_TIMEOUT).
+constexpr uint64_t kGroupWaitTicks = 2000000ull;
+
+__device__ __forceinline__ bool group_barrier(Smem& sm, RowGroup& g) {
+    __syncthreads();
+    ++g.epoch;
+    if (threadIdx.x == 0) {
+        __threadfence();   // this member's published totals before its arrival
+        atomicAdd(g.ctr, 1u);
+        const uint32_t target = g.epoch * (uint32_t)g.S;
+        const uint64_t t0 = (uint64_t)wall_clock64();
+        int ok = 1;
+        while (__hip_atomic_load(g.ctr, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT) < target) {
+            __builtin_amdgcn_s_sleep(2);
+            if ((uint64_t)wall_clock64() - t0 > kGroupWaitTicks) {
+                ok = 0;
+                break;
+            }
+        }
+        __threadfence();   // the other members' totals after their arrivals
+        sm.group_ok = ok;
+    }
+    __syncthreads();
+    return sm.group_ok != 0;
+}
+
+// Slot totals of the pass just swept (this workgroup's slots [s0, s0 + nl)): summed in
+// shared memory, then, in a row group, published and gathered, so that on return
+// slotA / slotB (and slotP if keepP) hold the totals of every slot of the row.
+// False if a group barrier timed out.
+template <int BLK, bool SPLIT>
+__device__ __forceinline__ bool pass_totals(Smem& sm, RowGroup& grp, int nslots, int s0, int nl,
+                                            bool wantB, bool keepP) {
+    const int tid = threadIdx.x;
+    slot_sums_stage1<BLK>(sm, s0, s0 + nl, wantB);
+    __syncthreads();
+    if (!SPLIT || grp.S == 1) {
+        if (tid < nslots) {
+            const double a = slot_group_sum<BLK>(sm.partA, tid);
+            sm.slotA[tid] = a;
+            sm.slotB[tid] = wantB ? slot_group_sum<BLK>(sm.partB, tid) : 0.0;
+            if (keepP) sm.slotP[tid] = a;
+        }
+        __syncthreads();
+        return true;
+    }
+    // the buffer of the coming barrier (parity): no member still reads it, since that
+    // needs the barrier before it, which every member has passed
+    double* xa = grp.xbuf + (size_t)((grp.epoch + 1) & 1u) * 2 * kMaxSlots;
+    double* xb = xa + kMaxSlots;
+    if (tid < nl) {
+        const int s = s0 + tid;
+        xa[s] = slot_group_sum<BLK>(sm.partA, s);
+        if (wantB) xb[s] = slot_group_sum<BLK>(sm.partB, s);
+    }
+    const bool ok = group_barrier(sm, grp);
+    if (tid < nslots) {
+        const double a = __hip_atomic_load(&xa[tid], __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+        sm.slotA[tid] = a;
+        sm.slotB[tid] = wantB ? __hip_atomic_load(&xb[tid], __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT) : 0.0;
+        if (keepP) sm.slotP[tid] = a;
+    }
+    __syncthreads();
+    return ok;
+}
+
+template <typename In, int VEC, int UNR, int MODE, int BLK, bool SPLIT, typename Emit>
 __device__ __forceinline__ void verify_row(const KParams& P, Smem& sm, const int64_t row,
-                                           const int32_t b, const int32_t n, Emit&& emit) {
+                                           const int32_t b, const int32_t n, Emit&& emit,
+                                           RowGroup& grp) {
     constexpr int kBlock = BLK;
     constexpr int kWaves = BLK / 64;
     const int tid = threadIdx.x;
@@ -182,6 +271,12 @@ __device__ __forceinline__ void verify_row(const KParams& P, Smem& sm, const int
     const int V = P.V;
     constexpr int CHUNK = 64 * VEC * UNR;
     const int G = P.G, nslots = P.nslots;
+    // this workgroup's slots: all of them, or its share in a row group
+    int s0 = 0, nl = nslots;
+    if (SPLIT && grp.S > 1) {
+        s0 = (int)((int64_t)nslots * grp.w / grp.S);
+        nl = (int)((int64_t)nslots * (grp.w + 1) / grp.S) - s0;
+    }
 
     const In* __restrict__ tg = reinterpret_cast<const In*>(P.tgt) + row * V;
     const In* __restrict__ dg = reinterpret_cast<const In*>(P.dft) + row * V;
@@ -189,10 +284,10 @@ __device__ __forceinline__ void verify_row(const KParams& P, Smem& sm, const int
     RS_STAMP(row, 0);
     using W = Vec<In, VEC>;
     // This wave's first target chunk is requested before anything else, so its latency
-    // overlaps the row description below (the first slot of wave w is slot w).
+    // overlaps the row description below (the first slot of wave w is slot s0 + w).
     typename W::raw pre[UNR];
 #pragma unroll
-    for (int u = 0; u < UNR; ++u) pre[u] = W::template load<kNtPass1>(tg, wid * G * CHUNK + lane * VEC + u * 64 * VEC, V);
+    for (int u = 0; u < UNR; ++u) pre[u] = W::template load<kNtPass1>(tg, (s0 + wid) * G * CHUNK + lane * VEC + u * 64 * VEC, V);
 
     // ---- row description.  "Holder" threads own one candidate each: node, token and
     // uniform, then the two logits of its token and their unnormalised masses, all
@@ -203,18 +298,23 @@ __device__ __forceinline__ void verify_row(const KParams& P, Smem& sm, const int
         sm.ur = P.flat ? P.ur_flat[row] : P.ur[row];
     }
     for (int w = tid; w < kMaxSlots / 32; w += kBlock) sm.hit_slots[w] = 0u;
-    // maxima of the chunks just requested: they fix the row's exponent reference
+    // The maximum of the row's first chunk fixes the row's exponent reference, the same
+    // in every schedule and in every member of a row group (wave 0 requested that chunk
+    // above unless its workgroup's slots start later).
     auto publish_premax = [&]() {
+        if (wid != 0) return;
         float mx = -FLT_MAX;
 #pragma unroll
         for (int u = 0; u < UNR; ++u) {
+            typename W::raw r = pre[u];
+            if (SPLIT && s0 != 0) r = W::template load<false>(tg, lane * VEC + u * 64 * VEC, V);
             float v[VEC];
-            W::unpack(pre[u], v);
+            W::unpack(r, v);
 #pragma unroll
             for (int e = 0; e < VEC; ++e) mx = fmaxf(mx, v[e]);
         }
         mx = wave_max(mx);
-        if (lane == 0) sm.wmax[0][wid] = mx;
+        if (lane == 0) sm.wmax[0][0] = mx;
     };
     bool holder = false;
     int32_t hx = 0, hnode = 0, hrank = 0;
@@ -325,16 +425,12 @@ __device__ __forceinline__ void verify_row(const KParams& P, Smem& sm, const int
     const float c2h = P.c2h, c2l = P.c2l;
 
     // ---- pass 1: softmax statistics.  Both rows are summed against one exponent
-    // reference K, fixed from the maxima of the first chunks, so element values do not
+    // reference K, fixed from the maximum of the row's first chunk, so element values do not
     // depend on which wave read which chunk; per-lane partials of every slot go to shared
     // memory and are reduced in a fixed order.  A row whose sums overflow, or come out
     // below kLowSum, takes an exact-maximum pass and is summed again.
     float Kt, Kd;
-    {
-        float m0 = -FLT_MAX;
-        for (int w = 0; w < kWaves; ++w) m0 = fmaxf(m0, sm.wmax[0][w]);
-        Kt = Kd = kref(m0, c2h);
-    }
+    Kt = Kd = kref(sm.wmax[0][0], c2h);
     // The candidates' unnormalised masses need only the exponent references: holders
     // compute them (fp64) now, off the critical path after pass 1; the division by the
     // sums follows the pass.  Rows that take the exact-maximum pass recompute them.
@@ -363,7 +459,7 @@ __device__ __forceinline__ void verify_row(const KParams& P, Smem& sm, const int
             fa = fc = 0.0f;
         };
         if (internal) {
-            wave_sweep<In, VEC, UNR, true, 1, kNtPass1>(tg, dg, V, G, nslots, false, pre, pre, &sm.next_slot,
+            wave_sweep<In, VEC, UNR, true, 1, kNtPass1>(tg, dg, V, G, nl, s0, false, pre, pre, &sm.next_slot,
                 [&](const float (&t)[UNR][VEC], const float (&d)[UNR][VEC], int, int) {
 #pragma unroll
                     for (int u = 0; u < UNR; ++u)
@@ -375,7 +471,7 @@ __device__ __forceinline__ void verify_row(const KParams& P, Smem& sm, const int
                 },
                 flush);
         } else {
-            wave_sweep<In, VEC, UNR, false, 1, kNtLeaf>(tg, dg, V, G, nslots, false, pre, pre, &sm.next_slot,
+            wave_sweep<In, VEC, UNR, false, 1, kNtLeaf>(tg, dg, V, G, nl, s0, false, pre, pre, &sm.next_slot,
                 [&](const float (&t)[UNR][VEC], const float (&)[UNR][VEC], int, int) {
 #pragma unroll
                     for (int u = 0; u < UNR; ++u)
@@ -391,15 +487,11 @@ __device__ __forceinline__ void verify_row(const KParams& P, Smem& sm, const int
 #endif
         }
         __syncthreads();
-        slot_sums_stage1<BLK>(sm, nslots, internal);
-        __syncthreads();
-        if (tid < nslots) {
-            const double a = slot_group_sum<BLK>(sm.partA, tid);
-            sm.slotA[tid] = a;
-            sm.slotB[tid] = internal ? slot_group_sum<BLK>(sm.partB, tid) : 0.0;
-            sm.slotP[tid] = a;
+        if (!pass_totals<BLK, SPLIT>(sm, grp, nslots, s0, nl, internal, true)) {
+            if (tid == 0) emit(-1, -1, RS_SEQ_GROUP_TIMEOUT);
+            zero_residual_row(P, row);
+            return;
         }
-        __syncthreads();
         if (wid == 0) {
             double a0 = 0.0, a1 = 0.0;
             for (int s2 = lane; s2 < nslots; s2 += 64) {
@@ -427,7 +519,7 @@ __device__ __forceinline__ void verify_row(const KParams& P, Smem& sm, const int
         // exact maxima of both rows, then the references are taken from them
         {
             float mx = -FLT_MAX, my = -FLT_MAX;
-            wave_sweep<In, VEC, UNR, true, 0, kNtPass1>(tg, dg, V, G, nslots, false, pre, pre, &sm.next_slot,
+            wave_sweep<In, VEC, UNR, true, 0, kNtPass1>(tg, dg, V, G, nl, s0, false, pre, pre, &sm.next_slot,
                 [&](const float (&t)[UNR][VEC], const float (&d)[UNR][VEC], int, int) {
 #pragma unroll
                     for (int u = 0; u < UNR; ++u)
@@ -449,6 +541,22 @@ __device__ __forceinline__ void verify_row(const KParams& P, Smem& sm, const int
             for (int w = 0; w < kWaves; ++w) {
                 m0 = fmaxf(m0, sm.wmax[0][w]);
                 m1 = fmaxf(m1, sm.wmax[1][w]);
+            }
+            if (SPLIT && grp.S > 1) {   // the maxima of the whole row, from every member
+                if (tid == 0) {
+                    grp.xmax[2 * grp.w] = m0;
+                    grp.xmax[2 * grp.w + 1] = m1;
+                }
+                if (!group_barrier(sm, grp)) {
+                    if (tid == 0) emit(-1, -1, RS_SEQ_GROUP_TIMEOUT);
+                    zero_residual_row(P, row);
+                    return;
+                }
+                m0 = m1 = -FLT_MAX;
+                for (int q = 0; q < grp.S; ++q) {
+                    m0 = fmaxf(m0, __hip_atomic_load(&grp.xmax[2 * q], __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT));
+                    m1 = fmaxf(m1, __hip_atomic_load(&grp.xmax[2 * q + 1], __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT));
+                }
             }
             Kt = kref(m0, c2h);
             Kd = kref(m1, c2h);
@@ -562,7 +670,7 @@ __device__ __forceinline__ void verify_row(const KParams& P, Smem& sm, const int
             };
             if (MODE == RS_MODE_SPECINFER) {
                 // A = max(R - C_i Q, 0)
-                wave_sweep<In, VEC, UNR, true, 0, kNtRej>(tg, dg, V, G, nslots, reverse, pre, pre, &sm.next_slot,
+                wave_sweep<In, VEC, UNR, true, 0, kNtRej>(tg, dg, V, G, nl, s0, reverse, pre, pre, &sm.next_slot,
                     [&](const float (&t)[UNR][VEC], const float (&d)[UNR][VEC], int, int) {
                         float fa = 0.0f;
 #pragma unroll
@@ -580,7 +688,7 @@ __device__ __forceinline__ void verify_row(const KParams& P, Smem& sm, const int
                 // first rejection: A = min(c Q, R) / 2^f0 = exp2(min(aR - f0, aQ + e)), one
                 // exponential per element; the sum of R over j != x_0 is 1 - R(x_0)
                 const float f0 = sm.st_f0, kq0 = sm.st_kq0;
-                wave_sweep<In, VEC, UNR, true, 0, kNtRej>(tg, dg, V, G, nslots, reverse, pre, pre, &sm.next_slot,
+                wave_sweep<In, VEC, UNR, true, 0, kNtRej>(tg, dg, V, G, nl, s0, reverse, pre, pre, &sm.next_slot,
                     [&](const float (&t)[UNR][VEC], const float (&d)[UNR][VEC], int idx0, int slot) {
                         float v[UNR][VEC];
 #pragma unroll
@@ -605,7 +713,7 @@ __device__ __forceinline__ void verify_row(const KParams& P, Smem& sm, const int
                     },
                     flush);
             } else {
-                wave_sweep<In, VEC, UNR, true, 0, kNtRej>(tg, dg, V, G, nslots, reverse, pre, pre, &sm.next_slot,
+                wave_sweep<In, VEC, UNR, true, 0, kNtRej>(tg, dg, V, G, nl, s0, reverse, pre, pre, &sm.next_slot,
                     [&](const float (&t)[UNR][VEC], const float (&d)[UNR][VEC], int idx0, int slot) {
                         const bool hit = slot_hit(slot);
                         float R[UNR][VEC], Q[UNR][VEC];
@@ -656,16 +764,11 @@ __device__ __forceinline__ void verify_row(const KParams& P, Smem& sm, const int
             }
         }
         __syncthreads();
-        {
-            const bool wantB = MODE == RS_MODE_RESISPEC && i > 0;
-            slot_sums_stage1<BLK>(sm, nslots, wantB);
-            __syncthreads();
-            if (tid < nslots) {
-                sm.slotA[tid] = slot_group_sum<BLK>(sm.partA, tid);
-                sm.slotB[tid] = wantB ? slot_group_sum<BLK>(sm.partB, tid) : 0.0;
-            }
+        if (!pass_totals<BLK, SPLIT>(sm, grp, nslots, s0, nl, MODE == RS_MODE_RESISPEC && i > 0, false)) {
+            if (tid == 0) emit(-1, -1, RS_SEQ_GROUP_TIMEOUT);
+            zero_residual_row(P, row);
+            return;
         }
-        __syncthreads();
         if (wid == 0) {
             // per-lane sums over slots lane, lane+64, ... in a fixed order
             double A = 0.0, Bv = 0.0;
@@ -951,36 +1054,64 @@ __global__ void __launch_bounds__(kBlock) __attribute__((amdgpu_waves_per_eu(4))
         b = g - n * P.B;
         row = (int64_t)b * P.N + n;
     }
-    verify_row<In, VEC, UNR, MODE, kBlock>(P, sm, row, b, n, [&](int32_t child, int32_t tok, int32_t st) {
+    RowGroup solo{1, 0, nullptr, nullptr, nullptr, 0u};
+    verify_row<In, VEC, UNR, MODE, kBlock, false>(P, sm, row, b, n, [&](int32_t child, int32_t tok, int32_t st) {
         write_outcome(P, row, child, tok, st);
-    });
+    }, solo);
 }
 
-// Path-only schedule: one workgroup per sequence walks its own tree from the root and
-// verifies only the nodes it reaches (each node's outcome depends on that node's rows
-// and uniforms alone, so the result equals the all-nodes schedule followed by the walk).
-template <typename In, int VEC, int UNR, int MODE, int BLK>
-__global__ void __launch_bounds__(BLK) __attribute__((amdgpu_waves_per_eu(4)))
+// Row groups of the path schedule: S members per sequence (workgroups b * S .. b * S +
+// S - 1) and the workspace that holds each sequence's group state (kGroupStride bytes
+// per sequence).  S = 1 needs no workspace.
+struct GroupArgs {
+    int32_t S;
+    char* ws;
+};
+
+// Path-only schedule: a sequence's workgroup (or row group) walks its own tree from the
+// root and verifies only the nodes it reaches (each node's outcome depends on that
+// node's rows and uniforms alone, so the result equals the all-nodes schedule followed
+// by the walk, bit for bit: rows are cut into the same chunks and slots, and summed in
+// the same order).  Member 0 of a group writes the outputs.  The walk keeps its state
+// live across every row, so these workgroups take up to 256 registers per lane (two
+// waves per SIMD, one workgroup per CU) and nothing is spilled.
+constexpr int kPathBlock = 512;
+
+template <typename In, int VEC, int UNR, int MODE>
+__global__ void __launch_bounds__(kPathBlock) __attribute__((amdgpu_waves_per_eu(2)))
 rs_path_kernel(const KParams P, int32_t max_depth, int32_t* __restrict__ out_tokens,
-               int32_t* __restrict__ out_len, int32_t* __restrict__ out_status) {
-    constexpr int kBlock = BLK;
+               int32_t* __restrict__ out_len, int32_t* __restrict__ out_status, const GroupArgs ga) {
+    constexpr int kBlock = kPathBlock;
     __shared__ Smem sm;
     const int tid = threadIdx.x;
-    const int32_t b = blockIdx.x;
+    const int32_t S = ga.S;
+    const int32_t b = (int32_t)(blockIdx.x / (uint32_t)S);
+    const int32_t member = (int32_t)blockIdx.x - b * S;
+    RowGroup grp{S, member, nullptr, nullptr, nullptr, 0u};
+    if (S > 1) {
+        char* base = ga.ws + (int64_t)b * kGroupStride;
+        grp.ctr = reinterpret_cast<uint32_t*>(base);
+        grp.xbuf = reinterpret_cast<double*>(base + kGroupXbuf);
+        grp.xmax = reinterpret_cast<float*>(base + kGroupXmax);
+    }
+    const bool lead = member == 0;
     const int32_t N = P.N;
     const int64_t W = (int64_t)max_depth + 1;
     int32_t* out = out_tokens + (int64_t)b * W;
-    for (int64_t i = tid; i < W; i += kBlock) out[i] = -1;
+    if (lead)
+        for (int64_t i = tid; i < W; i += kBlock) out[i] = -1;
     int32_t n = 0, len = 0, status = RS_SEQ_OK;
     for (int32_t steps = 0; steps <= N; ++steps) {
-        verify_row<In, VEC, UNR, MODE, BLK>(P, sm, (int64_t)b * N + n, b, n,
-                                       [&](int32_t child, int32_t tok, int32_t st) {
+        verify_row<In, VEC, UNR, MODE, kBlock, true>(P, sm, (int64_t)b * N + n, b, n,
+                                                     [&](int32_t child, int32_t tok, int32_t st) {
             sm.res_child = child;
             sm.res_tok = tok;
             sm.res_status = st;
-        });
+        }, grp);
         __syncthreads();
-        const int32_t st = sm.res_status, c = sm.res_child, t = sm.res_tok;
+        const int32_t st = __builtin_amdgcn_readfirstlane(sm.res_status);
+        const int32_t c = __builtin_amdgcn_readfirstlane(sm.res_child);
+        const int32_t t = __builtin_amdgcn_readfirstlane(sm.res_tok);
         __syncthreads();   // the next row rewrites the shared state
         if (st != RS_SEQ_OK) {
             status = st;
@@ -995,23 +1126,30 @@ rs_path_kernel(const KParams P, int32_t max_depth, int32_t* __restrict__ out_tok
                 status = RS_SEQ_DEPTH_EXCEEDED;
                 break;
             }
-            if (tid == 0) out[len] = P.node_token[(int64_t)b * N + c];
+            if (lead && tid == 0) out[len] = P.node_token[(int64_t)b * N + c];
             ++len;
             n = c;
             continue;
         }
-        if (t >= 0 && tid == 0) out[len] = t;
+        if (t >= 0 && lead && tid == 0) out[len] = t;
         break;
     }
     if (status != RS_SEQ_OK) {
         __syncthreads();
-        for (int64_t i = tid; i < W; i += kBlock) out[i] = -1;
+        if (lead)
+            for (int64_t i = tid; i < W; i += kBlock) out[i] = -1;
         len = -1;
     }
-    if (tid == 0) {
+    if (lead && tid == 0) {
         out_len[b] = len;
         if (out_status) out_status[b] = status;
     }
+}
+
+// The arrival counters of the row groups start at zero in every launch.
+__global__ void rs_group_reset(char* __restrict__ ws, int32_t B) {
+    const int64_t b = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;
+    if (b < B) *reinterpret_cast<uint32_t*>(ws + b * kGroupStride) = 0u;
 }
 
 // ----------------------------------------------------------- walk kernel ----
@@ -1085,47 +1223,110 @@ int cu_count() {
 
 // Outputs of the path schedule (NULL: all-nodes schedule).
 struct PathOut {
-    int wide;            // 1024-thread workgroups (few sequences: one per CU)
     int32_t max_depth;
     int32_t* out_tokens;
     int32_t* out_len;
     int32_t* out_status;
+    int32_t group;       // members per sequence: 0 automatic, 1 one workgroup, >= 2 that many
+    char* ws;            // row-group workspace (kGroupStride bytes per sequence) or null
+    int dry_run;         // only resolve the group size
+    int32_t used_group;  // out: members per sequence
+    int unsupported;     // out: the requested group size cannot run on this device
 };
 
-template <typename In, int VEC, int UNR, int MODE>
-hipError_t launch_rows_t(KParams P, int64_t nrows, const PathOut* path, hipStream_t s) {
+// chunks of 64 * VEC * UNR elements, grouped into at most kMaxSlots slots of G chunks
+template <int VEC, int UNR>
+void set_slots(KParams& P) {
     constexpr int64_t CHUNK = 64 * VEC * UNR;
     const int64_t nch = ((int64_t)P.V + CHUNK - 1) / CHUNK;
     const int64_t G = (nch + kMaxSlots - 1) / kMaxSlots;
     P.G = (int32_t)G;
     P.nslots = (int32_t)((nch + G - 1) / G);
-    if (path && path->wide) {
-        hipLaunchKernelGGL((rs_path_kernel<In, VEC, UNR, MODE, kBlockWide>), dim3((unsigned)P.B),
-                           dim3(kBlockWide), 0, s, P, path->max_depth, path->out_tokens,
-                           path->out_len, path->out_status);
-    } else if (path) {
-        hipLaunchKernelGGL((rs_path_kernel<In, VEC, UNR, MODE, kBlock>), dim3((unsigned)P.B),
-                           dim3(kBlock), 0, s, P, path->max_depth, path->out_tokens, path->out_len,
-                           path->out_status);
-    } else {
-        hipLaunchKernelGGL((rs_row_kernel<In, VEC, UNR, MODE>), dim3((unsigned)nrows), dim3(kBlock), 0, s, P);
-    }
+}
+
+template <typename In, int VEC, int UNR, int MODE>
+hipError_t launch_row_kernel(KParams P, int64_t nrows, hipStream_t s) {
+    set_slots<VEC, UNR>(P);
+    hipLaunchKernelGGL((rs_row_kernel<In, VEC, UNR, MODE>), dim3((unsigned)nrows), dim3(kBlock), 0, s, P);
     return hipGetLastError();
 }
 
-template <int MODE>
-hipError_t launch_rows_m(const KParams& P, int dtype, bool vec, int64_t nrows, const PathOut* path,
-                         hipStream_t s) {
-    if (dtype == RS_BF16) {
-        return vec ? launch_rows_t<uint16_t, 8, RS_UNR16, MODE>(P, nrows, path, s)
-                   : launch_rows_t<uint16_t, 1, 4, MODE>(P, nrows, path, s);
+// Members per sequence: all B * S workgroups must be resident at once (cooperative
+// launch), and each member keeps at least one slot (one per wave when chosen
+// automatically).
+template <typename In, int VEC, int UNR, int MODE>
+int32_t resolve_group(const KParams& P, const PathOut* path) {
+    if (path->group == 1 || (path->group == 0 && !path->ws)) return 1;
+    if (!path->ws) return -1;
+    int dev = 0, coop = 0, per_cu = 0;
+    if (hipGetDevice(&dev) != hipSuccess ||
+        hipDeviceGetAttribute(&coop, hipDeviceAttributeCooperativeLaunch, dev) != hipSuccess)
+        coop = 0;
+    if (coop && hipOccupancyMaxActiveBlocksPerMultiprocessor(
+                    &per_cu, reinterpret_cast<const void*>(rs_path_kernel<In, VEC, UNR, MODE>),
+                    kPathBlock, 0) != hipSuccess)
+        per_cu = 0;
+    const int64_t cap = coop ? (int64_t)per_cu * cu_count() : 0;
+    int64_t smax = (int64_t)kMaxGroup;
+    if (cap / P.B < smax) smax = cap / P.B;
+    if (path->group == 0) {
+        if (P.nslots / (kPathBlock / 64) < smax) smax = P.nslots / (kPathBlock / 64);
+        return smax >= 2 ? (int32_t)smax : 1;
     }
-    return vec ? launch_rows_t<float, 4, RS_UNR32, MODE>(P, nrows, path, s)
-               : launch_rows_t<float, 1, 4, MODE>(P, nrows, path, s);
+    if (P.nslots < smax) smax = P.nslots;
+    return path->group <= smax ? path->group : -1;
 }
 
+template <typename In, int VEC, int UNR, int MODE>
+hipError_t launch_path_kernel(KParams P, PathOut* path, hipStream_t s) {
+    set_slots<VEC, UNR>(P);
+    const int32_t S = resolve_group<In, VEC, UNR, MODE>(P, path);
+    path->used_group = S;
+    if (S < 1) {
+        path->unsupported = 1;
+        return hipErrorInvalidConfiguration;
+    }
+    if (path->dry_run) return hipSuccess;
+    if (S == 1) {
+        hipLaunchKernelGGL((rs_path_kernel<In, VEC, UNR, MODE>), dim3((unsigned)P.B), dim3(kPathBlock), 0, s,
+                           P, path->max_depth, path->out_tokens, path->out_len, path->out_status,
+                           GroupArgs{1, nullptr});
+        return hipGetLastError();
+    }
+    // a row group per sequence: counters zeroed, then every workgroup resident at once
+    hipLaunchKernelGGL(rs_group_reset, dim3((unsigned)((P.B + 255) / 256)), dim3(256), 0, s, path->ws, P.B);
+    const hipError_t e = hipGetLastError();
+    if (e != hipSuccess) return e;
+    KParams kp = P;
+    int32_t md = path->max_depth;
+    int32_t* ot = path->out_tokens;
+    int32_t* ol = path->out_len;
+    int32_t* os = path->out_status;
+    GroupArgs ga{S, path->ws};
+    void* args[] = {&kp, &md, &ot, &ol, &os, &ga};
+    return hipLaunchCooperativeKernel(reinterpret_cast<const void*>(rs_path_kernel<In, VEC, UNR, MODE>),
+                                      dim3((unsigned)((int64_t)P.B * S)), dim3(kPathBlock), args, 0, s);
+}
+
+template <int MODE>
+hipError_t launch_rows_m(const KParams& P, int dtype, bool vec, int64_t nrows, PathOut* path,
+                         hipStream_t s) {
+    if (path) {
+        if (dtype == RS_BF16)
+            return vec ? launch_path_kernel<uint16_t, 8, RS_UNR16, MODE>(P, path, s)
+                       : launch_path_kernel<uint16_t, 1, 4, MODE>(P, path, s);
+        return vec ? launch_path_kernel<float, 4, RS_UNR32, MODE>(P, path, s)
+                   : launch_path_kernel<float, 1, 4, MODE>(P, path, s);
+    }
+    if (dtype == RS_BF16) {
+        return vec ? launch_row_kernel<uint16_t, 8, RS_UNR16, MODE>(P, nrows, s)
+                   : launch_row_kernel<uint16_t, 1, 4, MODE>(P, nrows, s);
+    }
+    return vec ? launch_row_kernel<float, 4, RS_UNR32, MODE>(P, nrows, s)
+               : launch_row_kernel<float, 1, 4, MODE>(P, nrows, s);
+}
 hipError_t launch_rows(const KParams& P, const rs_params* prm, bool vec, int64_t nrows, hipStream_t s,
-                       const PathOut* path = nullptr) {
+                       PathOut* path = nullptr) {
     if (prm->mode == RS_MODE_SPECINFER)
         return launch_rows_m<RS_MODE_SPECINFER>(P, prm->logits_dtype, vec, nrows, path, s);
     return launch_rows_m<RS_MODE_RESISPEC>(P, prm->logits_dtype, vec, nrows, path, s);
@@ -1294,23 +1495,74 @@ rs_status resispec_verify_tree(const void* target_logits, const void* draft_logi
                      ws_array(workspace, rows, 2), nullptr, (hipStream_t)stream);
 }
 
+static rs_status verify_tree_path_impl(const void* target_logits, const void* draft_logits,
+                                       const int32_t* node_token, const int32_t* parent,
+                                       const float* u_accept, const float* u_resample, int32_t B,
+                                       int32_t N, int32_t V, int32_t max_depth, const rs_params* prm,
+                                       int32_t* out_tokens, int32_t* out_accepted_len,
+                                       int32_t* out_status, int32_t group_size, void* workspace,
+                                       size_t workspace_bytes, void* stream) {
+    const rs_status as = check_tree_args(target_logits, draft_logits, node_token, parent, u_accept,
+                                         u_resample, B, N, V, max_depth, prm, out_tokens,
+                                         out_accepted_len);
+    if (as != RS_OK) return as;
+    if (group_size < 0 || group_size > kMaxGroup) return RS_ERR_INVALID_ARG;
+    if (workspace && (workspace_bytes < resispec_path_workspace_bytes(B) || !aligned16(workspace)))
+        return RS_ERR_WORKSPACE;
+    if (group_size >= 2 && !workspace) return RS_ERR_WORKSPACE;
+    if (B == 0) return RS_OK;
+    const KParams P = tree_params(target_logits, draft_logits, node_token, parent, u_accept,
+                                  u_resample, B, N, V, prm, nullptr, nullptr, nullptr, nullptr);
+    const bool vec = vector_ok(target_logits, draft_logits, V, prm->logits_dtype);
+    PathOut path{max_depth, out_tokens, out_accepted_len, out_status, group_size,
+                 static_cast<char*>(workspace), 0, 1, 0};
+    const hipError_t e = launch_rows(P, prm, vec, B, (hipStream_t)stream, &path);
+    if (path.unsupported) return RS_ERR_UNSUPPORTED;
+    return e == hipSuccess ? RS_OK : RS_ERR_HIP;
+}
+
 rs_status resispec_verify_tree_path(const void* target_logits, const void* draft_logits,
                                     const int32_t* node_token, const int32_t* parent,
                                     const float* u_accept, const float* u_resample, int32_t B,
                                     int32_t N, int32_t V, int32_t max_depth, const rs_params* prm,
                                     int32_t* out_tokens, int32_t* out_accepted_len,
                                     int32_t* out_status, void* stream) {
-    const rs_status as = check_tree_args(target_logits, draft_logits, node_token, parent, u_accept,
-                                         u_resample, B, N, V, max_depth, prm, out_tokens,
-                                         out_accepted_len);
-    if (as != RS_OK || B == 0) return as;
-    const KParams P = tree_params(target_logits, draft_logits, node_token, parent, u_accept,
-                                  u_resample, B, N, V, prm, nullptr, nullptr, nullptr, nullptr);
-    const bool vec = vector_ok(target_logits, draft_logits, V, prm->logits_dtype);
-    // with fewer sequences than two per CU, give each sequence a whole CU
-    const PathOut path{B < 2 * cu_count() ? 1 : 0, max_depth, out_tokens, out_accepted_len,
-                       out_status};
-    return launch_rows(P, prm, vec, B, (hipStream_t)stream, &path) == hipSuccess ? RS_OK : RS_ERR_HIP;
+    return verify_tree_path_impl(target_logits, draft_logits, node_token, parent, u_accept,
+                                 u_resample, B, N, V, max_depth, prm, out_tokens, out_accepted_len,
+                                 out_status, 1, nullptr, 0, stream);
+}
+
+rs_status resispec_verify_tree_path_group(const void* target_logits, const void* draft_logits,
+                                          const int32_t* node_token, const int32_t* parent,
+                                          const float* u_accept, const float* u_resample,
+                                          int32_t B, int32_t N, int32_t V, int32_t max_depth,
+                                          const rs_params* prm, int32_t* out_tokens,
+                                          int32_t* out_accepted_len, int32_t* out_status,
+                                          int32_t group_size, void* workspace,
+                                          size_t workspace_bytes, void* stream) {
+    return verify_tree_path_impl(target_logits, draft_logits, node_token, parent, u_accept,
+                                 u_resample, B, N, V, max_depth, prm, out_tokens, out_accepted_len,
+                                 out_status, group_size, workspace, workspace_bytes, stream);
+}
+
+size_t resispec_path_workspace_bytes(int32_t B) {
+    if (B <= 0) return 0;
+    return (size_t)B * (size_t)kGroupStride;
+}
+
+int32_t resispec_path_group_size(int32_t B, int32_t V, const rs_params* prm) {
+    if (B <= 0 || V <= 0 || !prm || (prm->logits_dtype != RS_F32 && prm->logits_dtype != RS_BF16) ||
+        (prm->mode != RS_MODE_RESISPEC && prm->mode != RS_MODE_SPECINFER))
+        return -1;
+    KParams P{};
+    P.B = B;
+    P.V = V;
+    char probe = 0;   // any non-null workspace: the answer does not depend on it
+    PathOut path{0, nullptr, nullptr, nullptr, 0, &probe, 1, 1, 0};
+    // 16-byte aligned rows take the vector kernels
+    const bool vec = (prm->logits_dtype == RS_BF16) ? (V % 8 == 0) : (V % 4 == 0);
+    if (launch_rows(P, prm, vec, B, nullptr, &path) != hipSuccess) return -1;
+    return path.used_group;
 }
 
 rs_status resispec_verify_nodes(const void* target_logits, const void* draft_logits,

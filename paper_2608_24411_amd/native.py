@@ -22,7 +22,8 @@ MODES = {"resispec": RS_MODE_RESISPEC, "specinfer": RS_MODE_SPECINFER}
 
 # Every symbol include/resispec.h declares.
 EXPORTS = ("resispec_verify", "resispec_verify_tree", "resispec_verify_tree_path",
-           "resispec_draft_candidates",
+           "resispec_verify_tree_path_group", "resispec_path_workspace_bytes",
+           "resispec_path_group_size", "resispec_draft_candidates",
            "resispec_verify_nodes", "resispec_walk",
            "resispec_workspace_bytes", "resispec_validate_tree_host",
            "resispec_verify_tree_debug", "resispec_status_string", "resispec_abi_version")
@@ -53,6 +54,13 @@ def _load():
     lib.resispec_verify_tree_path.argtypes = [P, P, P, P, P, P, i32, i32, i32, i32, prm, P, P, P,
                                               P]
     lib.resispec_verify_tree_path.restype = i32
+    lib.resispec_verify_tree_path_group.argtypes = [P, P, P, P, P, P, i32, i32, i32, i32, prm, P,
+                                                    P, P, i32, P, sz, P]
+    lib.resispec_verify_tree_path_group.restype = i32
+    lib.resispec_path_workspace_bytes.argtypes = [i32]
+    lib.resispec_path_workspace_bytes.restype = sz
+    lib.resispec_path_group_size.argtypes = [i32, i32, prm]
+    lib.resispec_path_group_size.restype = i32
     lib.resispec_draft_candidates.argtypes = [P, P, i32, i32, i32, prm, ctypes.c_uint64,
                                               ctypes.c_uint64, P, P, P, P, P]
     lib.resispec_draft_candidates.restype = i32
@@ -272,6 +280,56 @@ def resispec_verify_tree_path(target_logits, draft_logits, node_token, parent, u
         _dev(out_tokens, torch.int32, "out_tokens"),
         _dev(out_accepted_len, torch.int32, "out_accepted_len"),
         _dev(out_status, torch.int32, "out_status"), _stream(stream))
+    _check(st)
+    return out_tokens, out_accepted_len, out_status
+
+
+def resispec_path_workspace_bytes(B: int) -> int:
+    return lib.resispec_path_workspace_bytes(int(B))
+
+
+def resispec_path_group_size(B: int, V: int, *, dtype, mode="resispec") -> int:
+    """Members per sequence the grouped path schedule picks by itself (dtype: "bf16" or
+    "f32"); -1 for invalid arguments."""
+    prm = RsParams(MODES[mode], RS_BF16 if dtype == "bf16" else RS_F32, 1.0, 0, 1)
+    return lib.resispec_path_group_size(int(B), int(V), ctypes.byref(prm))
+
+
+def resispec_verify_tree_path_group(target_logits, draft_logits, node_token, parent, u_accept,
+                                    u_resample, *, temperature, max_depth, mode="resispec",
+                                    without_replacement=False, bonus=True, group_size=0,
+                                    workspace=None, out_tokens=None, out_accepted_len=None,
+                                    out_status=None, stream=None):
+    """Path-only schedule with row groups (group_size workgroups per sequence, 0 =
+    automatic); same results as resispec_verify_tree_path.  Returns (tokens [B,
+    max_depth+1], accepted_len [B], status [B])."""
+    import torch
+    B, N, V = _tree_common(target_logits, draft_logits, node_token, parent, u_accept, u_resample,
+                           max_depth)
+    dev = target_logits.device
+    if out_tokens is None:
+        out_tokens = torch.empty((B, max_depth + 1), dtype=torch.int32, device=dev)
+    if out_accepted_len is None:
+        out_accepted_len = torch.empty(B, dtype=torch.int32, device=dev)
+    if out_status is None:
+        out_status = torch.empty(B, dtype=torch.int32, device=dev)
+    if workspace is None:
+        workspace = torch.empty(max(1, resispec_path_workspace_bytes(B)), dtype=torch.uint8,
+                                device=dev)
+    _shape(out_tokens, (B, max_depth + 1), "out_tokens")
+    _shape(out_accepted_len, (B,), "out_accepted_len")
+    _shape(out_status, (B,), "out_status")
+    prm = _params(target_logits, temperature, mode, without_replacement, bonus)
+    st = lib.resispec_verify_tree_path_group(
+        _dev(target_logits, target_logits.dtype, "target_logits"),
+        _dev(draft_logits, target_logits.dtype, "draft_logits"),
+        _dev(node_token, torch.int32, "node_token"), _dev(parent, torch.int32, "parent"),
+        _dev(u_accept, torch.float32, "u_accept"), _dev(u_resample, torch.float32, "u_resample"),
+        B, N, V, int(max_depth), ctypes.byref(prm),
+        _dev(out_tokens, torch.int32, "out_tokens"),
+        _dev(out_accepted_len, torch.int32, "out_accepted_len"),
+        _dev(out_status, torch.int32, "out_status"), int(group_size),
+        _dev(workspace, torch.uint8, "workspace"), workspace.numel(), _stream(stream))
     _check(st)
     return out_tokens, out_accepted_len, out_status
 

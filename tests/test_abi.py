@@ -136,6 +136,26 @@ def test_argument_errors_return_before_launch(native):
                                          None) == native.RS_ERR_INVALID_ARG
     assert lib.resispec_verify_tree_path(None, None, None, None, None, None, 0, 5, 100, 2,
                                          ctypes.byref(ok), None, None, None, None) == native.RS_OK
+    # path schedule with row groups: group size and workspace are checked before launch
+    pg = lib.resispec_verify_tree_path_group
+    pws = native.resispec_path_workspace_bytes(4)
+    assert pws > 0 and native.resispec_path_workspace_bytes(0) == 0
+    wsp = ctypes.c_void_p(0x10000)
+    for g in (-1, 17):
+        assert pg(*args, 4, 5, 100, 2, ctypes.byref(ok), i32p, i32p, None, g, wsp, pws,
+                  None) == native.RS_ERR_INVALID_ARG
+    assert pg(*args, 4, 5, 100, 2, ctypes.byref(ok), i32p, i32p, None, 2, None, 0,
+              None) == native.RS_ERR_WORKSPACE                     # members need a workspace
+    assert pg(*args, 4, 5, 100, 2, ctypes.byref(ok), i32p, i32p, None, 0, wsp, pws - 1,
+              None) == native.RS_ERR_WORKSPACE                     # too small
+    assert pg(*args, 4, 5, 100, 2, ctypes.byref(ok), i32p, i32p, None, 0,
+              ctypes.c_void_p(0x10008), pws, None) == native.RS_ERR_WORKSPACE   # misaligned
+    assert pg(*args, 4, 0, 100, 2, ctypes.byref(ok), i32p, i32p, None, 0, wsp, pws,
+              None) == native.RS_ERR_INVALID_ARG
+    assert pg(None, None, None, None, None, None, 0, 5, 100, 2, ctypes.byref(ok), None, None,
+              None, 0, None, 0, None) == native.RS_OK
+    assert lib.resispec_path_group_size(0, 100, ctypes.byref(ok)) == -1
+    assert lib.resispec_path_group_size(4, 100, ctypes.byref(_prm(native, dtype=5))) == -1
     # draft step
     f32p = fake
     assert lib.resispec_draft_candidates(fake, i32p, 4, 5, 100, ctypes.byref(ok), 1, 0, None, f32p,

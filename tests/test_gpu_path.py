@@ -29,7 +29,13 @@ def path_tree(native, w, mode, max_depth=None, bonus=True):
 
 def same(a, b):
     for k in ("tokens", "accepted_len", "status"):
-        assert torch.equal(a[k], b[k]), k
+        if not torch.equal(a[k], b[k]):
+            x, y = a[k].cpu().numpy(), b[k].cpu().numpy()
+            rows = sorted(set(int(i) for i in np.argwhere(x != y)[:, 0]))
+            for r in rows[:5]:
+                _log("mismatch", k, "seq", r, "path", x[r].tolist(), "reference", y[r].tolist(),
+                     "| status", a["status"][r].item(), b["status"][r].item())
+            raise AssertionError("%s differs on %d sequences" % (k, len(rows)))
 
 
 CASES = [(1, dict(B=8)), (2, dict(B=4)), (3, dict(B=3)), (4, dict(B=8)),
@@ -101,3 +107,84 @@ def test_path_side_stream(gpu_lib):
             stream=s)
     s.synchronize()
     assert torch.equal(t, ref["tokens"]) and torch.equal(l, ref["accepted_len"])
+
+
+# ---- row groups: several workgroups per sequence (resispec_verify_tree_path_group)
+
+def group_tree(native, w, mode, group, max_depth=None, bonus=True, workspace=None):
+    md = w["max_depth"] if max_depth is None else max_depth
+    t, l, s = native.resispec_verify_tree_path_group(
+        w["target"], w["draft"], w["node_token"], w["parent"], w["u_accept"], w["u_resample"],
+        temperature=w["temperature"], max_depth=md, mode=mode,
+        without_replacement=w["without_replacement"], bonus=bonus, group_size=group,
+        workspace=workspace)
+    torch.cuda.synchronize()
+    return {"tokens": t, "accepted_len": l, "status": s}
+
+
+@pytest.mark.parametrize("cfg,over", CASES, ids=[f"cfg{c}-{o}" for c, o in CASES])
+@pytest.mark.parametrize("mode", MODES)
+def test_path_groups_equal_path(gpu_lib, cfg, over, mode):
+    """Every group size gives the one-workgroup path's results bit for bit (ragged
+    vocabularies and the unaligned kernels included), and the oracle's walk."""
+    w = synth.make_workload(cfg, device="cuda", **over)
+    ref = path_tree(gpu_lib, w, mode)
+    for g in (2, 3, 5, 0):
+        _log("path group", cfg, over, mode, g)
+        same(group_tree(gpu_lib, w, mode, g), ref)
+    compare_walk(ref, oracle_walk(host_tree(w), w, mode))
+
+
+def test_path_groups_full_size(gpu_lib):
+    """The benchmarked configuration with the automatic group size, twice in a row on
+    one workspace (its counters are reset by every call)."""
+    w = synth.make_workload(2, device="cuda")
+    B = w["B"]
+    ws = torch.empty(gpu_lib.resispec_path_workspace_bytes(B), dtype=torch.uint8, device="cuda")
+    g = gpu_lib.resispec_path_group_size(B, w["V"], dtype="bf16")
+    _log("path group full size, automatic group", g)
+    assert g >= 1
+    for mode in MODES:
+        ref = gpu_tree(gpu_lib, w, mode)
+        for _ in range(2):
+            p = group_tree(gpu_lib, w, mode, 0, workspace=ws)
+            same(p, ref)
+        assert (p["status"].cpu().numpy() == 0).all()
+
+
+def test_path_groups_fallback_and_faults(gpu_lib):
+    """The exact-maximum pass (maxima exchanged between members) and faults met on the
+    walk, with a group of 4."""
+    w = synth.make_workload(2, device="cuda", B=3, V=40000)
+    w["target"][:, 3, 39990] = 200.0
+    w["target"][1, 0, 39000] = 150.0
+    for mode in MODES:
+        _log("path group fallback", mode)
+        same(group_tree(gpu_lib, w, mode, 4), gpu_tree(gpu_lib, w, mode))
+    ws = dict(w)
+    ws["draft"] = (w["draft"].float() - 60.0).to(w["draft"].dtype)
+    for mode in MODES:
+        same(group_tree(gpu_lib, ws, mode, 4), gpu_tree(gpu_lib, ws, mode))
+    f = synth.make_workload(1, device="cuda", B=6, V=3001)
+    f["u_accept"][2, 1:5] = 0.999
+    f["node_token"][3, 2] = 3001
+    f["parent"][4, 7] = 9
+    f["u_resample"][5, :] = 1.0
+    for mode in MODES:
+        for bonus in (True, False):
+            _log("path group faults", mode, bonus)
+            same(group_tree(gpu_lib, f, mode, 3, bonus=bonus), path_tree(gpu_lib, f, mode, bonus=bonus))
+        same(group_tree(gpu_lib, f, mode, 2, max_depth=1), path_tree(gpu_lib, f, mode, max_depth=1))
+
+
+def test_path_groups_unsupported(gpu_lib):
+    """More members than a row has slots, or than the device holds at once: an error
+    before anything runs."""
+    w = synth.make_workload(4, device="cuda", B=3, V=512)    # one slot per row
+    with pytest.raises(Exception):
+        group_tree(gpu_lib, w, "resispec", 2)
+    big = synth.make_workload(1, device="cuda", B=400, V=8192)   # 16 slots, 400 x 16 > device
+    with pytest.raises(Exception):
+        group_tree(gpu_lib, big, "resispec", 16)
+    # automatic: falls back to one workgroup per sequence
+    same(group_tree(gpu_lib, w, "resispec", 0), path_tree(gpu_lib, w, "resispec"))
