@@ -307,9 +307,16 @@ def main():
         pargs = (w["target"], w["draft"], w["node_token"], w["parent"], w["u_accept"],
                  w["u_resample"])
 
+        # row groups where the batch leaves CUs free (the group size the library picks)
+        pws = torch.empty(max(1, native.resispec_path_workspace_bytes(B)), dtype=torch.uint8,
+                          device="cuda")
+        group = native.resispec_path_group_size(B, V, dtype="bf16" if esz == 2 else "f32",
+                                                mode=args.mode)
+
         def pstep():
-            native.resispec_verify_tree_path(*pargs, out_tokens=out_tok, out_accepted_len=out_len,
-                                             out_status=out_st, **kw)
+            native.resispec_verify_tree_path_group(*pargs, out_tokens=out_tok,
+                                                   out_accepted_len=out_len, out_status=out_st,
+                                                   group_size=0, workspace=pws, **kw)
         t_end = time.perf_counter() + args.settle_ms * 1e-3
         while time.perf_counter() < t_end:
             pstep()
@@ -339,7 +346,7 @@ def main():
                 if child[b, n] < 0:
                     break
                 n = child[b, n]
-        path = {"ms_per_step": 1e3 * pwall, "sequences_per_s": B / pwall,
+        path = {"ms_per_step": 1e3 * pwall, "group_size": group, "sequences_per_s": B / pwall,
                 "rows_verified_per_step": int(plens.sum() + B),
                 "alg_bytes_per_step": int(pbytes),
                 "achieved_gbps": pbytes / pwall / 1e9,

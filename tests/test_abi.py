@@ -198,3 +198,22 @@ def test_read_probe_library_rejects_bad_arguments():
     assert fn(p, 5 * q, 2 * q, 0, 1, p, None) == 1         # chunk does not divide the buffer
     assert fn(p, 4 * q, q, 2, 1, p, None) == 1             # unknown load policy
     assert fn(p, 4 * q, q, 0, 3, p, None) == 1             # unknown pass count
+
+
+def test_build_rejects_register_spills():
+    """The build's check of the compiler's resource remarks finds spilling functions."""
+    from paper_2608_24411_amd import build
+    report = "\n".join([
+        "x.hip:1:1: remark: Function Name: k_ok [-Rpass-analysis=kernel-resource-usage]",
+        "x.hip:1:1: remark:     VGPRs: 120 [-Rpass-analysis=kernel-resource-usage]",
+        "x.hip:1:1: remark:     ScratchSize [bytes/lane]: 0 [-Rpass-analysis=kernel-resource-usage]",
+        "x.hip:1:1: remark:     SGPRs Spill: 30 [-Rpass-analysis=kernel-resource-usage]",
+        "x.hip:1:1: remark:     VGPRs Spill: 0 [-Rpass-analysis=kernel-resource-usage]",
+        "x.hip:9:1: remark: Function Name: k_bad [-Rpass-analysis=kernel-resource-usage]",
+        "x.hip:9:1: remark:     ScratchSize [bytes/lane]: 204 [-Rpass-analysis=kernel-resource-usage]",
+        "x.hip:9:1: remark:     VGPRs Spill: 50 [-Rpass-analysis=kernel-resource-usage]",
+        "x.hip:12:1: remark: Function Name: k_stack [-Rpass-analysis=kernel-resource-usage]",
+        "x.hip:12:1: remark:     ScratchSize [bytes/lane]: 16 [-Rpass-analysis=kernel-resource-usage]",
+        "x.hip:12:1: remark:     VGPRs Spill: 0 [-Rpass-analysis=kernel-resource-usage]",
+    ])
+    assert build._spills(report) == [("k_bad", 50, 204), ("k_stack", 0, 16)]
