@@ -298,23 +298,26 @@ __device__ __forceinline__ void verify_row(const KParams& P, Smem& sm, const int
         sm.ur = P.flat ? P.ur_flat[row] : P.ur[row];
     }
     for (int w = tid; w < kMaxSlots / 32; w += kBlock) sm.hit_slots[w] = 0u;
-    // The maximum of the row's first chunk fixes the row's exponent reference, the same
-    // in every schedule and in every member of a row group (wave 0 requested that chunk
-    // above unless its workgroup's slots start later).
+    // The maximum over the first chunks of the first slots (chunk w * G for wave w) fixes
+    // the row's exponent reference, the same in every schedule and in every member of a
+    // row group: each wave requested its chunk above, except in members whose slots start
+    // later, which load those chunks' target parts here.  Elements past the row's end
+    // do not count.
     auto publish_premax = [&]() {
-        if (wid != 0) return;
         float mx = -FLT_MAX;
 #pragma unroll
         for (int u = 0; u < UNR; ++u) {
+            const int idx = wid * G * CHUNK + lane * VEC + u * 64 * VEC;
             typename W::raw r = pre[u];
-            if (SPLIT && s0 != 0) r = W::template load<false>(tg, lane * VEC + u * 64 * VEC, V);
+            if (SPLIT && s0 != 0) r = W::template load<false>(tg, idx, V);
             float v[VEC];
             W::unpack(r, v);
 #pragma unroll
-            for (int e = 0; e < VEC; ++e) mx = fmaxf(mx, v[e]);
+            for (int e = 0; e < VEC; ++e)
+                if (idx + e < V) mx = fmaxf(mx, v[e]);
         }
         mx = wave_max(mx);
-        if (lane == 0) sm.wmax[0][0] = mx;
+        if (lane == 0) sm.wmax[0][wid] = mx;
     };
     bool holder = false;
     int32_t hx = 0, hnode = 0, hrank = 0;
@@ -425,12 +428,16 @@ __device__ __forceinline__ void verify_row(const KParams& P, Smem& sm, const int
     const float c2h = P.c2h, c2l = P.c2l;
 
     // ---- pass 1: softmax statistics.  Both rows are summed against one exponent
-    // reference K, fixed from the maximum of the row's first chunk, so element values do not
+    // reference K, fixed from the maxima of the first chunks, so element values do not
     // depend on which wave read which chunk; per-lane partials of every slot go to shared
     // memory and are reduced in a fixed order.  A row whose sums overflow, or come out
     // below kLowSum, takes an exact-maximum pass and is summed again.
     float Kt, Kd;
-    Kt = Kd = kref(sm.wmax[0][0], c2h);
+    {
+        float m0 = -FLT_MAX;
+        for (int w = 0; w < kWaves; ++w) m0 = fmaxf(m0, sm.wmax[0][w]);
+        Kt = Kd = kref(m0, c2h);
+    }
     // The candidates' unnormalised masses need only the exponent references: holders
     // compute them (fp64) now, off the critical path after pass 1; the division by the
     // sums follows the pass.  Rows that take the exact-maximum pass recompute them.
@@ -929,35 +936,37 @@ __device__ __forceinline__ void verify_row(const KParams& P, Smem& sm, const int
         // the slot's elements: lane l takes a contiguous run of R = G * VEC * UNR
         const int R = G * VEC * UNR;
         const int t0 = ks * G * CHUNK + lane * R;
-        constexpr int kRegRun = 32;
-        float vals[kRegRun];
         double own2 = 0.0;
-        const bool inreg = R <= kRegRun;
-        if (inreg) {
-#pragma unroll
-            for (int c = 0; c < kRegRun; c += VEC) {
-                float tv[VEC], dv[VEC];
-                if (c < R) {
-                    load_vec<In, VEC>(tg, t0 + c, V, tv);
-                    if (internal) load_vec<In, VEC>(dg, t0 + c, V, dv);
+        // The run's values are staged in the lane's row of the pass partials (idle during
+        // the draw) when the run fits there; one chunk's loads stay in flight ahead of the
+        // arithmetic.  A rolled loop keeps the kernel's code small: fully unrolled, the
+        // value code of every element made the kernel larger than the instruction cache.
+        const bool staged = R <= kMaxSlots;
+        {
+            float tv[VEC], dv[VEC];
+            load_vec<In, VEC>(tg, t0, V, tv);
+            if (internal) load_vec<In, VEC>(dg, t0, V, dv);
+#pragma unroll 1
+            for (int c = 0; c < R; c += VEC) {
+                float tn[VEC], dn[VEC];
+                const bool more = c + VEC < R;
+                if (more) {
+                    load_vec<In, VEC>(tg, t0 + c + VEC, V, tn);
+                    if (internal) load_vec<In, VEC>(dg, t0 + c + VEC, V, dn);
                 }
 #pragma unroll
                 for (int e = 0; e < VEC; ++e) {
                     const int j = t0 + c + e;
-                    const float v = (c < R && j < V) ? final_value(tv[e], internal ? dv[e] : 0.0f, j) : 0.0f;
-                    vals[c + e] = v;
+                    const float v = j < V ? final_value(tv[e], internal ? dv[e] : 0.0f, j) : 0.0f;
+                    if (staged) sm.partA[lane][c + e] = v;
                     own2 += (double)v;
                 }
-            }
-        } else {
-            for (int c = 0; c < R; c += VEC) {
-                float tv[VEC], dv[VEC];
-                load_vec<In, VEC>(tg, t0 + c, V, tv);
-                if (internal) load_vec<In, VEC>(dg, t0 + c, V, dv);
+                if (more) {
 #pragma unroll
-                for (int e = 0; e < VEC; ++e) {
-                    const int j = t0 + c + e;
-                    if (j < V) own2 += (double)final_value(tv[e], internal ? dv[e] : 0.0f, j);
+                    for (int e = 0; e < VEC; ++e) {
+                        tv[e] = tn[e];
+                        if (internal) dv[e] = dn[e];
+                    }
                 }
             }
         }
@@ -973,16 +982,15 @@ __device__ __forceinline__ void verify_row(const KParams& P, Smem& sm, const int
         if (lane == L2) {
             double acc = base + excl2;
             int tok = -1, lastpos = -1;
-            if (inreg) {
-#pragma unroll
-                for (int c = 0; c < kRegRun; ++c) {
-                    const float v = vals[c];
+            if (staged) {
+#pragma unroll 1
+                for (int c = 0; c < R && tok < 0; ++c) {
                     const int j = t0 + c;
-                    if (tok < 0 && c < R && j < V) {
-                        if (v > 0.0f) lastpos = j;
-                        acc += (double)v;
-                        if (!fallback && v > 0.0f && acc > thr) tok = j;
-                    }
+                    if (j >= V) break;
+                    const float v = sm.partA[lane][c];
+                    if (v > 0.0f) lastpos = j;
+                    acc += (double)v;
+                    if (!fallback && v > 0.0f && acc > thr) tok = j;
                 }
             } else {
                 for (int c = 0; c < R && tok < 0; c += VEC) {
