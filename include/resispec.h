@@ -186,6 +186,13 @@ rs_status resispec_verify_tree_path_group(const void* target_logits, const void*
                                           int32_t group_size, void* workspace,
                                           size_t workspace_bytes, void* stream);
 
+/* Testing hook: the time limit of every row-group barrier in later launches of this
+ * process, in ticks of the device's 100 MHz wall clock (default 2,000,000 = 20 ms;
+ * UINT64_MAX restores the default).  A small limit makes groups report
+ * RS_SEQ_GROUP_TIMEOUT instead of waiting, which is how the tests exercise that path.
+ * Not for concurrent use with launches on other threads.  Always RS_OK. */
+rs_status resispec_debug_set_group_wait(uint64_t ticks);
+
 /* Workspace bytes resispec_verify_tree_path_group needs for B sequences (0 if B <= 0). */
 size_t resispec_path_workspace_bytes(int32_t B);
 

@@ -182,6 +182,7 @@ struct RowGroup {
     double* xbuf;      // [2 (barrier parity)][2 (first sum, second sum)][kMaxSlots]
     float* xmax;       // [S][2]: the members' maxima of the target and draft rows
     uint32_t epoch;    // barriers passed so far (the same count in every member)
+    uint64_t wait;     // time limit of one barrier, in ticks of the 100 MHz wall clock
 };
 
 // per-sequence workspace of a row group: counter, slot totals, maxima
@@ -191,9 +192,10 @@ constexpr int64_t kGroupXmax = kGroupXbuf + 2 * 2 * kMaxSlots * (int64_t)sizeof(
 constexpr int32_t kMaxGroup = 16;
 static_assert(kGroupXmax + 2 * kMaxGroup * (int64_t)sizeof(float) <= kGroupStride, "group workspace layout");
 
-// Barrier of a row group with a time limit (20 ms of the 100 MHz wall clock): false if
-// the other members did not arrive in time, so every workgroup ends whatever happens
-// to the others (the row then reports RS_SEQ_GROUP_TIMEOUT).
+// Barrier of a row group with a time limit (20 ms of the 100 MHz wall clock unless a
+// test sets another): false if the other members did not arrive in time, so every
+// workgroup ends whatever happens to the others (the row then reports
+// RS_SEQ_GROUP_TIMEOUT).
 constexpr uint64_t kGroupWaitTicks = 2000000ull;
 
 __device__ __forceinline__ bool group_barrier(Smem& sm, RowGroup& g) {
@@ -207,7 +209,7 @@ __device__ __forceinline__ bool group_barrier(Smem& sm, RowGroup& g) {
         int ok = 1;
         while (__hip_atomic_load(g.ctr, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT) < target) {
             __builtin_amdgcn_s_sleep(2);
-            if ((uint64_t)wall_clock64() - t0 > kGroupWaitTicks) {
+            if ((uint64_t)wall_clock64() - t0 > g.wait) {
                 ok = 0;
                 break;
             }
@@ -1062,7 +1064,7 @@ __global__ void __launch_bounds__(kBlock) __attribute__((amdgpu_waves_per_eu(4))
         b = g - n * P.B;
         row = (int64_t)b * P.N + n;
     }
-    RowGroup solo{1, 0, nullptr, nullptr, nullptr, 0u};
+    RowGroup solo{1, 0, nullptr, nullptr, nullptr, 0u, kGroupWaitTicks};
     verify_row<In, VEC, UNR, MODE, kBlock, false>(P, sm, row, b, n, [&](int32_t child, int32_t tok, int32_t st) {
         write_outcome(P, row, child, tok, st);
     }, solo);
@@ -1074,6 +1076,7 @@ __global__ void __launch_bounds__(kBlock) __attribute__((amdgpu_waves_per_eu(4))
 struct GroupArgs {
     int32_t S;
     char* ws;
+    uint64_t wait;   // barrier time limit (ticks)
 };
 
 // Path-only schedule: a sequence's workgroup (or row group) walks its own tree from the
@@ -1095,7 +1098,7 @@ rs_path_kernel(const KParams P, int32_t max_depth, int32_t* __restrict__ out_tok
     const int32_t S = ga.S;
     const int32_t b = (int32_t)(blockIdx.x / (uint32_t)S);
     const int32_t member = (int32_t)blockIdx.x - b * S;
-    RowGroup grp{S, member, nullptr, nullptr, nullptr, 0u};
+    RowGroup grp{S, member, nullptr, nullptr, nullptr, 0u, ga.wait};
     if (S > 1) {
         char* base = ga.ws + (int64_t)b * kGroupStride;
         grp.ctr = reinterpret_cast<uint32_t*>(base);
@@ -1230,6 +1233,9 @@ int cu_count() {
 }
 
 // Outputs of the path schedule (NULL: all-nodes schedule).
+// time limit of row-group barriers for the next launches (a testing hook sets it)
+std::atomic<uint64_t> g_group_wait{kGroupWaitTicks};
+
 struct PathOut {
     int32_t max_depth;
     int32_t* out_tokens;
@@ -1298,7 +1304,7 @@ hipError_t launch_path_kernel(KParams P, PathOut* path, hipStream_t s) {
     if (S == 1) {
         hipLaunchKernelGGL((rs_path_kernel<In, VEC, UNR, MODE>), dim3((unsigned)P.B), dim3(kPathBlock), 0, s,
                            P, path->max_depth, path->out_tokens, path->out_len, path->out_status,
-                           GroupArgs{1, nullptr});
+                           GroupArgs{1, nullptr, kGroupWaitTicks});
         return hipGetLastError();
     }
     // a row group per sequence: counters zeroed, then every workgroup resident at once
@@ -1310,7 +1316,7 @@ hipError_t launch_path_kernel(KParams P, PathOut* path, hipStream_t s) {
     int32_t* ot = path->out_tokens;
     int32_t* ol = path->out_len;
     int32_t* os = path->out_status;
-    GroupArgs ga{S, path->ws};
+    GroupArgs ga{S, path->ws, g_group_wait.load(std::memory_order_relaxed)};
     void* args[] = {&kp, &md, &ot, &ol, &os, &ga};
     return hipLaunchCooperativeKernel(reinterpret_cast<const void*>(rs_path_kernel<In, VEC, UNR, MODE>),
                                       dim3((unsigned)((int64_t)P.B * S)), dim3(kPathBlock), args, 0, s);
@@ -1551,6 +1557,11 @@ rs_status resispec_verify_tree_path_group(const void* target_logits, const void*
     return verify_tree_path_impl(target_logits, draft_logits, node_token, parent, u_accept,
                                  u_resample, B, N, V, max_depth, prm, out_tokens, out_accepted_len,
                                  out_status, group_size, workspace, workspace_bytes, stream);
+}
+
+rs_status resispec_debug_set_group_wait(uint64_t ticks) {
+    g_group_wait.store(ticks == UINT64_MAX ? kGroupWaitTicks : ticks, std::memory_order_relaxed);
+    return RS_OK;
 }
 
 size_t resispec_path_workspace_bytes(int32_t B) {

@@ -23,7 +23,8 @@ MODES = {"resispec": RS_MODE_RESISPEC, "specinfer": RS_MODE_SPECINFER}
 # Every symbol include/resispec.h declares.
 EXPORTS = ("resispec_verify", "resispec_verify_tree", "resispec_verify_tree_path",
            "resispec_verify_tree_path_group", "resispec_path_workspace_bytes",
-           "resispec_path_group_size", "resispec_draft_candidates",
+           "resispec_path_group_size", "resispec_debug_set_group_wait",
+           "resispec_draft_candidates",
            "resispec_verify_nodes", "resispec_walk",
            "resispec_workspace_bytes", "resispec_validate_tree_host",
            "resispec_verify_tree_debug", "resispec_status_string", "resispec_abi_version")
@@ -61,6 +62,8 @@ def _load():
     lib.resispec_path_workspace_bytes.restype = sz
     lib.resispec_path_group_size.argtypes = [i32, i32, prm]
     lib.resispec_path_group_size.restype = i32
+    lib.resispec_debug_set_group_wait.argtypes = [ctypes.c_uint64]
+    lib.resispec_debug_set_group_wait.restype = i32
     lib.resispec_draft_candidates.argtypes = [P, P, i32, i32, i32, prm, ctypes.c_uint64,
                                               ctypes.c_uint64, P, P, P, P, P]
     lib.resispec_draft_candidates.restype = i32
@@ -293,6 +296,13 @@ def resispec_path_group_size(B: int, V: int, *, dtype, mode="resispec") -> int:
     "f32"); -1 for invalid arguments."""
     prm = RsParams(MODES[mode], RS_BF16 if dtype == "bf16" else RS_F32, 1.0, 0, 1)
     return lib.resispec_path_group_size(int(B), int(V), ctypes.byref(prm))
+
+
+def resispec_debug_set_group_wait(ticks=None) -> None:
+    """Testing hook: time limit of row-group barriers in later launches (ticks of the
+    100 MHz device clock); None restores the default (20 ms)."""
+    _check(lib.resispec_debug_set_group_wait(ctypes.c_uint64((1 << 64) - 1 if ticks is None
+                                                            else int(ticks))))
 
 
 def resispec_verify_tree_path_group(target_logits, draft_logits, node_token, parent, u_accept,

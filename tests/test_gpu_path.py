@@ -188,3 +188,29 @@ def test_path_groups_unsupported(gpu_lib):
         group_tree(gpu_lib, big, "resispec", 16)
     # automatic: falls back to one workgroup per sequence
     same(group_tree(gpu_lib, w, "resispec", 0), path_tree(gpu_lib, w, "resispec"))
+
+
+def test_path_groups_barrier_time_limit(gpu_lib):
+    """Forced from the host (testing hook): with a barrier time limit of zero ticks the
+    members of a row group do not wait for each other.  Every workgroup still ends; a
+    sequence either reports RS_SEQ_GROUP_TIMEOUT (8) with its outputs at -1, or finishes
+    with the reference result (a barrier passes only once every member has published its
+    totals).  The default limit restores normal results."""
+    w = synth.make_workload(2, device="cuda", B=4, V=40000)
+    ref = path_tree(gpu_lib, w, "resispec")
+    try:
+        gpu_lib.resispec_debug_set_group_wait(0)
+        g = group_tree(gpu_lib, w, "resispec", 4)
+    finally:
+        gpu_lib.resispec_debug_set_group_wait(None)
+    st = g["status"].cpu().numpy()
+    _log("statuses with a zero time limit", st.tolist())
+    assert set(st.tolist()) <= {0, 8}
+    late = st == 8
+    assert (g["accepted_len"].cpu().numpy()[late] == -1).all()
+    assert (g["tokens"].cpu().numpy()[late] == -1).all()
+    done = ~late
+    assert np.array_equal(g["tokens"].cpu().numpy()[done], ref["tokens"].cpu().numpy()[done])
+    assert np.array_equal(g["accepted_len"].cpu().numpy()[done],
+                          ref["accepted_len"].cpu().numpy()[done])
+    same(group_tree(gpu_lib, w, "resispec", 4), ref)
