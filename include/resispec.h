@@ -159,12 +159,14 @@ rs_status resispec_verify_tree_path(const void* target_logits, const void* draft
 /*
  * The path-only schedule with row groups, for batches too small to fill the device with
  * one workgroup per sequence (same results as resispec_verify_tree_path and
- * resispec_verify_tree, bit for bit).  Each sequence gets `group_size` 1024-thread
+ * resispec_verify_tree, bit for bit).  Each sequence gets `group_size` 512-thread
  * workgroups that verify every row of its walk together: each sweeps its share of the
  * row's slots in every pass, and after a pass they exchange their slots' totals through
- * `workspace` and meet at a barrier (a counter in global memory; all workgroups of the
- * launch are resident at once by a cooperative launch, and each wait is bounded: a
- * sequence whose workgroups do not meet within 20 ms reports RS_SEQ_GROUP_TIMEOUT).
+ * `workspace` and meet at a barrier (a counter in global memory).  The group forms only
+ * when all its workgroups have started within 20 us of the first; otherwise the first to
+ * give up waiting does the sequence alone (same results).  Every wait is bounded: a
+ * formed group whose workgroups do not meet within 20 ms at a barrier reports
+ * RS_SEQ_GROUP_TIMEOUT.
  *   group_size      : 0 = automatic (as many members as the device holds at once, up to
  *                     16 and to one per 16 slots of a row; 1 when that is under 2 or
  *                     workspace is NULL), 1 = one workgroup per sequence,
@@ -186,12 +188,50 @@ rs_status resispec_verify_tree_path_group(const void* target_logits, const void*
                                           int32_t group_size, void* workspace,
                                           size_t workspace_bytes, void* stream);
 
-/* Testing hook: the time limit of every row-group barrier in later launches of this
- * process, in ticks of the device's 100 MHz wall clock (default 2,000,000 = 20 ms;
- * UINT64_MAX restores the default).  A small limit makes groups report
- * RS_SEQ_GROUP_TIMEOUT instead of waiting, which is how the tests exercise that path.
+/*
+ * resispec_verify_tree with row groups, for batches of few rows (same results, bit for
+ * bit): every node row gets `group_size` 512-thread workgroups that verify it together,
+ * exchanging slot totals through the workspace at bounded barriers like the path
+ * schedule's row groups (a group that does not form within 20 us is done by one of its
+ * workgroups alone; RS_SEQ_GROUP_TIMEOUT after 20 ms at a barrier), then the walk runs
+ * as in resispec_verify_tree.
+ *   group_size : 0 = automatic (at most one workgroup per CU for B * N rows, up to 4
+ *                members per row, one per 8 slots of a row and one per 64 KiB of a row's
+ *                logits; 1 = the ordinary one-workgroup row kernel when that is under 2),
+ *                1 = the ordinary kernel,
+ *                2..16 = that many (RS_ERR_UNSUPPORTED if B * N * group_size workgroups
+ *                cannot be resident at once or a row has fewer slots than members)
+ *   workspace  : device buffer of at least resispec_tree_group_workspace_bytes(B, N)
+ *                bytes, 16-byte aligned, caller-owned (node outcomes, then one group
+ *                state per row; its counters are zeroed by the call itself on `stream`).
+ *                Calls that overlap on one workspace race.
+ * Other arguments, outputs and statuses as resispec_verify_tree.
+ */
+rs_status resispec_verify_tree_group(const void* target_logits, const void* draft_logits,
+                                     const int32_t* node_token, const int32_t* parent,
+                                     const float* u_accept, const float* u_resample, int32_t B,
+                                     int32_t N, int32_t V, int32_t max_depth, const rs_params* prm,
+                                     int32_t* out_tokens, int32_t* out_accepted_len,
+                                     int32_t* out_status, int32_t group_size, void* workspace,
+                                     size_t workspace_bytes, void* stream);
+
+/* Workspace bytes resispec_verify_tree_group needs (0 if B <= 0 or N <= 0). */
+size_t resispec_tree_group_workspace_bytes(int32_t B, int32_t N);
+
+/* The group size resispec_verify_tree_group chooses with group_size = 0 for B * N rows
+ * of V elements (16-byte aligned rows assumed), on the current device; -1 for invalid
+ * arguments.  Host only: launches nothing. */
+int32_t resispec_tree_group_size(int32_t B, int32_t N, int32_t V, const rs_params* prm);
+
+/* Testing hook: the time limits of row groups in later launches of this process, in
+ * ticks of the device's 100 MHz wall clock; UINT64_MAX restores a default.
+ *   barrier_ticks   : every barrier of a formed group (default 2,000,000 = 20 ms); a
+ *                     small limit makes groups report RS_SEQ_GROUP_TIMEOUT instead of
+ *                     waiting, which is how the tests exercise that path
+ *   formation_ticks : the wait for a group's workgroups to start (default 2,000 = 20 us);
+ *                     0 makes nearly every group fall back to one workgroup
  * Not for concurrent use with launches on other threads.  Always RS_OK. */
-rs_status resispec_debug_set_group_wait(uint64_t ticks);
+rs_status resispec_debug_set_group_waits(uint64_t barrier_ticks, uint64_t formation_ticks);
 
 /* Workspace bytes resispec_verify_tree_path_group needs for B sequences (0 if B <= 0). */
 size_t resispec_path_workspace_bytes(int32_t B);

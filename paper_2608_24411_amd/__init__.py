@@ -7,7 +7,8 @@ seeded synthetic workloads.  The binding is loaded on first use of an entry poin
 
 _API = ("resispec_verify", "resispec_verify_tree", "resispec_verify_tree_path",
         "resispec_verify_tree_path_group", "resispec_path_workspace_bytes",
-        "resispec_path_group_size", "resispec_debug_set_group_wait", "resispec_draft_candidates",
+        "resispec_path_group_size", "resispec_debug_set_group_waits", "resispec_verify_tree_group",
+        "resispec_tree_group_workspace_bytes", "resispec_tree_group_size", "resispec_draft_candidates",
         "resispec_verify_tree_debug",
         "resispec_workspace_bytes", "resispec_validate_tree_host", "resispec_status_string",
         "resispec_abi_version")

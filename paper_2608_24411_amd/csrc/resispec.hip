@@ -185,11 +185,15 @@ struct RowGroup {
     uint64_t wait;     // time limit of one barrier, in ticks of the 100 MHz wall clock
 };
 
-// per-sequence workspace of a row group: counter, slot totals, maxima
+// per-sequence (or per-row) workspace of a row group: barrier counter, formation
+// arrivals and state (each on its own 64-byte line), slot totals, maxima
 constexpr int64_t kGroupStride = 4608;
+constexpr int64_t kGroupArrive = 64;
+constexpr int64_t kGroupState = 128;
 constexpr int64_t kGroupXbuf = 256;
 constexpr int64_t kGroupXmax = kGroupXbuf + 2 * 2 * kMaxSlots * (int64_t)sizeof(double);
 constexpr int32_t kMaxGroup = 16;
+constexpr int32_t kAutoRowGroup = 4;   // automatic members per row, all-nodes schedule
 static_assert(kGroupXmax + 2 * kMaxGroup * (int64_t)sizeof(float) <= kGroupStride, "group workspace layout");
 
 // Barrier of a row group with a time limit (20 ms of the 100 MHz wall clock unless a
@@ -197,6 +201,46 @@ static_assert(kGroupXmax + 2 * kMaxGroup * (int64_t)sizeof(float) <= kGroupStrid
 // workgroup ends whatever happens to the others (the row then reports
 // RS_SEQ_GROUP_TIMEOUT).
 constexpr uint64_t kGroupWaitTicks = 2000000ull;
+
+// Group formation, before a group's first row.  Members are launched as ordinary
+// workgroups, so they need not all be resident at once: each counts its arrival, and
+// the last to arrive marks the group formed.  A member that sees no such mark within
+// the formation limit (20 us unless a test sets another) claims the group's work for
+// itself, and members that find it claimed leave.  The state moves once, from open to
+// formed or claimed: when formed, every member is running and reaches every barrier.
+// Returns 1 (formed: work as member w of S), 2 (claimed: do all of it alone) or 0
+// (leave).
+constexpr uint32_t kFormOpen = 0u, kFormed = 1u, kFormClaimed = 2u;
+constexpr uint64_t kFormWaitTicks = 2000ull;
+
+__device__ __forceinline__ int form_group(Smem& sm, const RowGroup& g, char* base, uint64_t wait) {
+    if (threadIdx.x == 0) {
+        uint32_t* arrive = reinterpret_cast<uint32_t*>(base + kGroupArrive);
+        uint32_t* state = reinterpret_cast<uint32_t*>(base + kGroupState);
+        if (atomicAdd(arrive, 1u) + 1u == (uint32_t)g.S) atomicCAS(state, kFormOpen, kFormed);
+        const uint64_t t0 = (uint64_t)wall_clock64();
+        int res;
+        for (;;) {
+            const uint32_t st = __hip_atomic_load(state, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+            if (st != kFormOpen) {
+                res = st == kFormed ? 1 : 0;
+                break;
+            }
+            if ((uint64_t)wall_clock64() - t0 > wait) {
+                const uint32_t old = atomicCAS(state, kFormOpen, kFormClaimed);
+                res = old == kFormOpen ? 2 : (old == kFormed ? 1 : 0);
+                break;
+            }
+            __builtin_amdgcn_s_sleep(2);
+        }
+        __threadfence();
+        sm.group_ok = res;
+    }
+    __syncthreads();
+    const int res = __builtin_amdgcn_readfirstlane(sm.group_ok);
+    __syncthreads();   // group_ok is reused by the barriers
+    return res;
+}
 
 __device__ __forceinline__ bool group_barrier(Smem& sm, RowGroup& g) {
     __syncthreads();
@@ -1076,7 +1120,8 @@ __global__ void __launch_bounds__(kBlock) __attribute__((amdgpu_waves_per_eu(4))
 struct GroupArgs {
     int32_t S;
     char* ws;
-    uint64_t wait;   // barrier time limit (ticks)
+    uint64_t wait;       // barrier time limit (ticks)
+    uint64_t form_wait;  // formation time limit (ticks)
 };
 
 // Path-only schedule: a sequence's workgroup (or row group) walks its own tree from the
@@ -1099,13 +1144,20 @@ rs_path_kernel(const KParams P, int32_t max_depth, int32_t* __restrict__ out_tok
     const int32_t b = (int32_t)(blockIdx.x / (uint32_t)S);
     const int32_t member = (int32_t)blockIdx.x - b * S;
     RowGroup grp{S, member, nullptr, nullptr, nullptr, 0u, ga.wait};
+    bool lead = member == 0;
     if (S > 1) {
         char* base = ga.ws + (int64_t)b * kGroupStride;
         grp.ctr = reinterpret_cast<uint32_t*>(base);
         grp.xbuf = reinterpret_cast<double*>(base + kGroupXbuf);
         grp.xmax = reinterpret_cast<float*>(base + kGroupXmax);
+        const int form = form_group(sm, grp, base, ga.form_wait);
+        if (form == 0) return;   // another member does this sequence's walk alone
+        if (form == 2) {         // this member does it alone: every slot, no barriers
+            grp.S = 1;
+            grp.w = 0;
+            lead = true;
+        }
     }
-    const bool lead = member == 0;
     const int32_t N = P.N;
     const int64_t W = (int64_t)max_depth + 1;
     int32_t* out = out_tokens + (int64_t)b * W;
@@ -1157,10 +1209,54 @@ rs_path_kernel(const KParams P, int32_t max_depth, int32_t* __restrict__ out_tok
     }
 }
 
-// The arrival counters of the row groups start at zero in every launch.
-__global__ void rs_group_reset(char* __restrict__ ws, int32_t B) {
+// The arrival counters of the row groups start at zero in every launch (one group state
+// of kGroupStride bytes per sequence or per row).
+__global__ void rs_group_reset(char* __restrict__ ws, int32_t count) {
     const int64_t b = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;
-    if (b < B) *reinterpret_cast<uint32_t*>(ws + b * kGroupStride) = 0u;
+    if (b < count) {
+        char* base = ws + b * kGroupStride;
+        *reinterpret_cast<uint32_t*>(base) = 0u;
+        *reinterpret_cast<uint32_t*>(base + kGroupArrive) = 0u;
+        *reinterpret_cast<uint32_t*>(base + kGroupState) = 0u;
+    }
+}
+
+// All-nodes schedule with row groups, for batches of few rows: S workgroups per node row
+// (workgroups g * S .. g * S + S - 1 verify row g of the node-major order, with the
+// row group of g at ws + g * kGroupStride).  The same chunks, slots and summation order
+// as the row kernel, so the outcomes are identical; member 0 writes them.
+template <typename In, int VEC, int UNR, int MODE>
+__global__ void __launch_bounds__(kPathBlock) __attribute__((amdgpu_waves_per_eu(2)))
+rs_rowgroup_kernel(const KParams P, const GroupArgs ga) {
+    __shared__ Smem sm;
+    const int32_t S = ga.S;
+    const int32_t g = (int32_t)(blockIdx.x / (uint32_t)S);
+    const int32_t member = (int32_t)blockIdx.x - g * S;
+    int64_t row;
+    int32_t b, n;
+    if (P.flat) {
+        row = g;
+        b = g;
+        n = 0;
+    } else {
+        n = g / P.B;
+        b = g - n * P.B;
+        row = (int64_t)b * P.N + n;
+    }
+    char* base = ga.ws + (int64_t)g * kGroupStride;
+    RowGroup grp{S, member, reinterpret_cast<uint32_t*>(base), reinterpret_cast<double*>(base + kGroupXbuf),
+                 reinterpret_cast<float*>(base + kGroupXmax), 0u, ga.wait};
+    bool lead = member == 0;
+    const int form = form_group(sm, grp, base, ga.form_wait);
+    if (form == 0) return;   // another member does this row alone
+    if (form == 2) {         // this member does it alone: every slot, no barriers
+        grp.S = 1;
+        grp.w = 0;
+        lead = true;
+    }
+    verify_row<In, VEC, UNR, MODE, kPathBlock, true>(P, sm, row, b, n, [&](int32_t child, int32_t tok, int32_t st) {
+        if (lead) write_outcome(P, row, child, tok, st);
+    }, grp);
 }
 
 // ----------------------------------------------------------- walk kernel ----
@@ -1233,8 +1329,10 @@ int cu_count() {
 }
 
 // Outputs of the path schedule (NULL: all-nodes schedule).
-// time limit of row-group barriers for the next launches (a testing hook sets it)
+// time limits of row-group barriers and formation for the next launches (a testing hook
+// sets them)
 std::atomic<uint64_t> g_group_wait{kGroupWaitTicks};
+std::atomic<uint64_t> g_form_wait{kFormWaitTicks};
 
 struct PathOut {
     int32_t max_depth;
@@ -1265,22 +1363,18 @@ hipError_t launch_row_kernel(KParams P, int64_t nrows, hipStream_t s) {
     return hipGetLastError();
 }
 
-// Members per sequence: all B * S workgroups must be resident at once (cooperative
-// launch), and each member keeps at least one slot (one per wave when chosen
-// automatically).
+// Members per sequence: at most as many workgroups as the device holds at once (a group
+// whose members do not all start in time is done by one of them alone), and each member
+// keeps at least one slot (one per wave when chosen automatically).
 template <typename In, int VEC, int UNR, int MODE>
 int32_t resolve_group(const KParams& P, const PathOut* path) {
     if (path->group == 1 || (path->group == 0 && !path->ws)) return 1;
     if (!path->ws) return -1;
-    int dev = 0, coop = 0, per_cu = 0;
-    if (hipGetDevice(&dev) != hipSuccess ||
-        hipDeviceGetAttribute(&coop, hipDeviceAttributeCooperativeLaunch, dev) != hipSuccess)
-        coop = 0;
-    if (coop && hipOccupancyMaxActiveBlocksPerMultiprocessor(
-                    &per_cu, reinterpret_cast<const void*>(rs_path_kernel<In, VEC, UNR, MODE>),
-                    kPathBlock, 0) != hipSuccess)
+    int per_cu = 0;
+    if (hipOccupancyMaxActiveBlocksPerMultiprocessor(
+            &per_cu, reinterpret_cast<const void*>(rs_path_kernel<In, VEC, UNR, MODE>), kPathBlock, 0) != hipSuccess)
         per_cu = 0;
-    const int64_t cap = coop ? (int64_t)per_cu * cu_count() : 0;
+    const int64_t cap = (int64_t)per_cu * cu_count();
     int64_t smax = (int64_t)kMaxGroup;
     if (cap / P.B < smax) smax = cap / P.B;
     if (path->group == 0) {
@@ -1304,7 +1398,7 @@ hipError_t launch_path_kernel(KParams P, PathOut* path, hipStream_t s) {
     if (S == 1) {
         hipLaunchKernelGGL((rs_path_kernel<In, VEC, UNR, MODE>), dim3((unsigned)P.B), dim3(kPathBlock), 0, s,
                            P, path->max_depth, path->out_tokens, path->out_len, path->out_status,
-                           GroupArgs{1, nullptr, kGroupWaitTicks});
+                           GroupArgs{1, nullptr, kGroupWaitTicks, kFormWaitTicks});
         return hipGetLastError();
     }
     // a row group per sequence: counters zeroed, then every workgroup resident at once
@@ -1316,10 +1410,80 @@ hipError_t launch_path_kernel(KParams P, PathOut* path, hipStream_t s) {
     int32_t* ot = path->out_tokens;
     int32_t* ol = path->out_len;
     int32_t* os = path->out_status;
-    GroupArgs ga{S, path->ws, g_group_wait.load(std::memory_order_relaxed)};
-    void* args[] = {&kp, &md, &ot, &ol, &os, &ga};
-    return hipLaunchCooperativeKernel(reinterpret_cast<const void*>(rs_path_kernel<In, VEC, UNR, MODE>),
-                                      dim3((unsigned)((int64_t)P.B * S)), dim3(kPathBlock), args, 0, s);
+    const GroupArgs ga{S, path->ws, g_group_wait.load(std::memory_order_relaxed),
+                       g_form_wait.load(std::memory_order_relaxed)};
+    hipLaunchKernelGGL((rs_path_kernel<In, VEC, UNR, MODE>), dim3((unsigned)((int64_t)P.B * S)), dim3(kPathBlock),
+                       0, s, kp, md, ot, ol, os, ga);
+    return hipGetLastError();
+}
+
+// Row groups of the all-nodes schedule: the resolved size (1: the row kernel itself, no
+// workspace used), -1 when the requested size cannot run.
+struct RowGroupLaunch {
+    int32_t group;       // members per row: 0 automatic, 1 one workgroup, >= 2 that many
+    char* ws;            // nrows * kGroupStride bytes or null
+    int dry_run;
+    int32_t used_group;  // out
+    int unsupported;     // out
+};
+
+template <typename In, int VEC, int UNR, int MODE>
+hipError_t launch_rowgroups(KParams P, int64_t nrows, RowGroupLaunch* rg, hipStream_t s) {
+    set_slots<VEC, UNR>(P);
+    int32_t S = 1;
+    if (rg->group >= 2 || (rg->group == 0 && rg->ws)) {
+        int per_cu = 0;
+        if (hipOccupancyMaxActiveBlocksPerMultiprocessor(
+                &per_cu, reinterpret_cast<const void*>(rs_rowgroup_kernel<In, VEC, UNR, MODE>), kPathBlock, 0) !=
+            hipSuccess)
+            per_cu = 0;
+        const int64_t cap = (int64_t)per_cu * cu_count();
+        int64_t smax = (int64_t)kMaxGroup;
+        if (cap / nrows < smax) smax = cap / nrows;
+        if (rg->group == 0) {
+            // measured: beyond one workgroup per CU, four members per row or below 64 KiB
+            // of a row per member, the barriers cost more than the split passes save
+            if (kAutoRowGroup < smax) smax = kAutoRowGroup;
+            const int64_t by_bytes = (int64_t)P.V * (int64_t)sizeof(In) / 65536;
+            if (by_bytes < smax) smax = by_bytes;
+            if ((int64_t)cu_count() / nrows < smax) smax = (int64_t)cu_count() / nrows;
+            if (P.nslots / (kPathBlock / 64) < smax) smax = P.nslots / (kPathBlock / 64);
+            S = smax >= 2 ? (int32_t)smax : 1;
+        } else {
+            if (P.nslots < smax) smax = P.nslots;
+            S = (rg->group <= smax && rg->ws) ? rg->group : -1;
+        }
+    }
+    rg->used_group = S;
+    if (S < 1) {
+        rg->unsupported = 1;
+        return hipErrorInvalidConfiguration;
+    }
+    if (rg->dry_run) return hipSuccess;
+    if (S == 1) {
+        hipLaunchKernelGGL((rs_row_kernel<In, VEC, UNR, MODE>), dim3((unsigned)nrows), dim3(kBlock), 0, s, P);
+        return hipGetLastError();
+    }
+    hipLaunchKernelGGL(rs_group_reset, dim3((unsigned)((nrows + 255) / 256)), dim3(256), 0, s, rg->ws,
+                       (int32_t)nrows);
+    const hipError_t e = hipGetLastError();
+    if (e != hipSuccess) return e;
+    KParams kp = P;
+    const GroupArgs ga{S, rg->ws, g_group_wait.load(std::memory_order_relaxed),
+                       g_form_wait.load(std::memory_order_relaxed)};
+    hipLaunchKernelGGL((rs_rowgroup_kernel<In, VEC, UNR, MODE>), dim3((unsigned)(nrows * S)), dim3(kPathBlock), 0,
+                       s, kp, ga);
+    return hipGetLastError();
+}
+
+template <int MODE>
+hipError_t launch_rowgroups_m(const KParams& P, int dtype, bool vec, int64_t nrows, RowGroupLaunch* rg,
+                              hipStream_t s) {
+    if (dtype == RS_BF16)
+        return vec ? launch_rowgroups<uint16_t, 8, RS_UNR16, MODE>(P, nrows, rg, s)
+                   : launch_rowgroups<uint16_t, 1, 4, MODE>(P, nrows, rg, s);
+    return vec ? launch_rowgroups<float, 4, RS_UNR32, MODE>(P, nrows, rg, s)
+               : launch_rowgroups<float, 1, 4, MODE>(P, nrows, rg, s);
 }
 
 template <int MODE>
@@ -1509,6 +1673,63 @@ rs_status resispec_verify_tree(const void* target_logits, const void* draft_logi
                      ws_array(workspace, rows, 2), nullptr, (hipStream_t)stream);
 }
 
+size_t resispec_tree_group_workspace_bytes(int32_t B, int32_t N) {
+    if (B <= 0 || N <= 0) return 0;
+    const int64_t rows = (int64_t)B * N;
+    return node_arrays_bytes(rows) + (size_t)rows * (size_t)kGroupStride;
+}
+
+rs_status resispec_verify_tree_group(const void* target_logits, const void* draft_logits,
+                                     const int32_t* node_token, const int32_t* parent,
+                                     const float* u_accept, const float* u_resample, int32_t B,
+                                     int32_t N, int32_t V, int32_t max_depth, const rs_params* prm,
+                                     int32_t* out_tokens, int32_t* out_accepted_len,
+                                     int32_t* out_status, int32_t group_size, void* workspace,
+                                     size_t workspace_bytes, void* stream) {
+    const rs_status as = check_tree_args(target_logits, draft_logits, node_token, parent, u_accept,
+                                         u_resample, B, N, V, max_depth, prm, out_tokens,
+                                         out_accepted_len);
+    if (as != RS_OK) return as;
+    if (group_size < 0 || group_size > kMaxGroup) return RS_ERR_INVALID_ARG;
+    if (B == 0) return RS_OK;
+    if (!workspace || workspace_bytes < resispec_tree_group_workspace_bytes(B, N) || !aligned16(workspace))
+        return RS_ERR_WORKSPACE;
+    const int64_t rows = (int64_t)B * N;
+    int32_t* nc = ws_array(workspace, rows, 0);
+    int32_t* nt = ws_array(workspace, rows, 1);
+    int32_t* ns = ws_array(workspace, rows, 2);
+    const KParams P = tree_params(target_logits, draft_logits, node_token, parent, u_accept,
+                                  u_resample, B, N, V, prm, nc, nt, ns, nullptr);
+    const bool vec = vector_ok(target_logits, draft_logits, V, prm->logits_dtype);
+    RowGroupLaunch rg{group_size, static_cast<char*>(workspace) + node_arrays_bytes(rows), 0, 1, 0};
+    const hipStream_t s = (hipStream_t)stream;
+    const hipError_t e = prm->mode == RS_MODE_SPECINFER
+                             ? launch_rowgroups_m<RS_MODE_SPECINFER>(P, prm->logits_dtype, vec, rows, &rg, s)
+                             : launch_rowgroups_m<RS_MODE_RESISPEC>(P, prm->logits_dtype, vec, rows, &rg, s);
+    if (rg.unsupported) return RS_ERR_UNSUPPORTED;
+    if (e != hipSuccess) return RS_ERR_HIP;
+    return launch_walk(nc, nt, ns, node_token, B, N, max_depth, out_tokens, out_accepted_len,
+                       out_status, s) == hipSuccess ? RS_OK : RS_ERR_HIP;
+}
+
+int32_t resispec_tree_group_size(int32_t B, int32_t N, int32_t V, const rs_params* prm) {
+    if (B <= 0 || N <= 0 || V <= 0 || !prm || (prm->logits_dtype != RS_F32 && prm->logits_dtype != RS_BF16) ||
+        (prm->mode != RS_MODE_RESISPEC && prm->mode != RS_MODE_SPECINFER))
+        return -1;
+    KParams P{};
+    P.B = B;
+    P.N = N;
+    P.V = V;
+    char probe = 0;   // any non-null workspace: the answer does not depend on it
+    RowGroupLaunch rg{0, &probe, 1, 1, 0};
+    const bool vec = (prm->logits_dtype == RS_BF16) ? (V % 8 == 0) : (V % 4 == 0);
+    const int64_t rows = (int64_t)B * N;
+    const hipError_t e = prm->mode == RS_MODE_SPECINFER
+                             ? launch_rowgroups_m<RS_MODE_SPECINFER>(P, prm->logits_dtype, vec, rows, &rg, nullptr)
+                             : launch_rowgroups_m<RS_MODE_RESISPEC>(P, prm->logits_dtype, vec, rows, &rg, nullptr);
+    return e == hipSuccess ? rg.used_group : -1;
+}
+
 static rs_status verify_tree_path_impl(const void* target_logits, const void* draft_logits,
                                        const int32_t* node_token, const int32_t* parent,
                                        const float* u_accept, const float* u_resample, int32_t B,
@@ -1559,8 +1780,9 @@ rs_status resispec_verify_tree_path_group(const void* target_logits, const void*
                                  out_status, group_size, workspace, workspace_bytes, stream);
 }
 
-rs_status resispec_debug_set_group_wait(uint64_t ticks) {
-    g_group_wait.store(ticks == UINT64_MAX ? kGroupWaitTicks : ticks, std::memory_order_relaxed);
+rs_status resispec_debug_set_group_waits(uint64_t barrier_ticks, uint64_t formation_ticks) {
+    g_group_wait.store(barrier_ticks == UINT64_MAX ? kGroupWaitTicks : barrier_ticks, std::memory_order_relaxed);
+    g_form_wait.store(formation_ticks == UINT64_MAX ? kFormWaitTicks : formation_ticks, std::memory_order_relaxed);
     return RS_OK;
 }
 

@@ -23,7 +23,9 @@ MODES = {"resispec": RS_MODE_RESISPEC, "specinfer": RS_MODE_SPECINFER}
 # Every symbol include/resispec.h declares.
 EXPORTS = ("resispec_verify", "resispec_verify_tree", "resispec_verify_tree_path",
            "resispec_verify_tree_path_group", "resispec_path_workspace_bytes",
-           "resispec_path_group_size", "resispec_debug_set_group_wait",
+           "resispec_path_group_size", "resispec_debug_set_group_waits",
+           "resispec_verify_tree_group", "resispec_tree_group_workspace_bytes",
+           "resispec_tree_group_size",
            "resispec_draft_candidates",
            "resispec_verify_nodes", "resispec_walk",
            "resispec_workspace_bytes", "resispec_validate_tree_host",
@@ -62,8 +64,15 @@ def _load():
     lib.resispec_path_workspace_bytes.restype = sz
     lib.resispec_path_group_size.argtypes = [i32, i32, prm]
     lib.resispec_path_group_size.restype = i32
-    lib.resispec_debug_set_group_wait.argtypes = [ctypes.c_uint64]
-    lib.resispec_debug_set_group_wait.restype = i32
+    lib.resispec_debug_set_group_waits.argtypes = [ctypes.c_uint64, ctypes.c_uint64]
+    lib.resispec_debug_set_group_waits.restype = i32
+    lib.resispec_verify_tree_group.argtypes = [P, P, P, P, P, P, i32, i32, i32, i32, prm, P, P, P,
+                                               i32, P, sz, P]
+    lib.resispec_verify_tree_group.restype = i32
+    lib.resispec_tree_group_workspace_bytes.argtypes = [i32, i32]
+    lib.resispec_tree_group_workspace_bytes.restype = sz
+    lib.resispec_tree_group_size.argtypes = [i32, i32, i32, prm]
+    lib.resispec_tree_group_size.restype = i32
     lib.resispec_draft_candidates.argtypes = [P, P, i32, i32, i32, prm, ctypes.c_uint64,
                                               ctypes.c_uint64, P, P, P, P, P]
     lib.resispec_draft_candidates.restype = i32
@@ -298,11 +307,64 @@ def resispec_path_group_size(B: int, V: int, *, dtype, mode="resispec") -> int:
     return lib.resispec_path_group_size(int(B), int(V), ctypes.byref(prm))
 
 
-def resispec_debug_set_group_wait(ticks=None) -> None:
-    """Testing hook: time limit of row-group barriers in later launches (ticks of the
-    100 MHz device clock); None restores the default (20 ms)."""
-    _check(lib.resispec_debug_set_group_wait(ctypes.c_uint64((1 << 64) - 1 if ticks is None
-                                                            else int(ticks))))
+def resispec_tree_group_workspace_bytes(B: int, N: int) -> int:
+    return lib.resispec_tree_group_workspace_bytes(int(B), int(N))
+
+
+def resispec_tree_group_size(B: int, N: int, V: int, *, dtype, mode="resispec") -> int:
+    """Members per row the grouped all-nodes schedule picks by itself (dtype: "bf16" or
+    "f32"); -1 for invalid arguments."""
+    prm = RsParams(MODES[mode], RS_BF16 if dtype == "bf16" else RS_F32, 1.0, 0, 1)
+    return lib.resispec_tree_group_size(int(B), int(N), int(V), ctypes.byref(prm))
+
+
+def resispec_verify_tree_group(target_logits, draft_logits, node_token, parent, u_accept,
+                               u_resample, *, temperature, max_depth, mode="resispec",
+                               without_replacement=False, bonus=True, group_size=0,
+                               workspace=None, out_tokens=None, out_accepted_len=None,
+                               out_status=None, stream=None):
+    """All-nodes verification with row groups (group_size workgroups per node row, 0 =
+    automatic); same results as resispec_verify_tree.  Returns (tokens [B, max_depth+1],
+    accepted_len [B], status [B])."""
+    import torch
+    B, N, V = _tree_common(target_logits, draft_logits, node_token, parent, u_accept, u_resample,
+                           max_depth)
+    dev = target_logits.device
+    if out_tokens is None:
+        out_tokens = torch.empty((B, max_depth + 1), dtype=torch.int32, device=dev)
+    if out_accepted_len is None:
+        out_accepted_len = torch.empty(B, dtype=torch.int32, device=dev)
+    if out_status is None:
+        out_status = torch.empty(B, dtype=torch.int32, device=dev)
+    if workspace is None:
+        workspace = torch.empty(max(1, resispec_tree_group_workspace_bytes(B, N)),
+                                dtype=torch.uint8, device=dev)
+    _shape(out_tokens, (B, max_depth + 1), "out_tokens")
+    _shape(out_accepted_len, (B,), "out_accepted_len")
+    _shape(out_status, (B,), "out_status")
+    prm = _params(target_logits, temperature, mode, without_replacement, bonus)
+    st = lib.resispec_verify_tree_group(
+        _dev(target_logits, target_logits.dtype, "target_logits"),
+        _dev(draft_logits, target_logits.dtype, "draft_logits"),
+        _dev(node_token, torch.int32, "node_token"), _dev(parent, torch.int32, "parent"),
+        _dev(u_accept, torch.float32, "u_accept"), _dev(u_resample, torch.float32, "u_resample"),
+        B, N, V, int(max_depth), ctypes.byref(prm),
+        _dev(out_tokens, torch.int32, "out_tokens"),
+        _dev(out_accepted_len, torch.int32, "out_accepted_len"),
+        _dev(out_status, torch.int32, "out_status"), int(group_size),
+        _dev(workspace, torch.uint8, "workspace"), workspace.numel(), _stream(stream))
+    _check(st)
+    return out_tokens, out_accepted_len, out_status
+
+
+def resispec_debug_set_group_waits(barrier=None, formation=None) -> None:
+    """Testing hook: time limits of row groups in later launches (ticks of the 100 MHz
+    device clock): `barrier` for every barrier of a formed group, `formation` for its
+    workgroups to start.  None restores a default (20 ms, 20 us)."""
+    none = (1 << 64) - 1
+    _check(lib.resispec_debug_set_group_waits(
+        ctypes.c_uint64(none if barrier is None else int(barrier)),
+        ctypes.c_uint64(none if formation is None else int(formation))))
 
 
 def resispec_verify_tree_path_group(target_logits, draft_logits, node_token, parent, u_accept,

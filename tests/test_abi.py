@@ -154,6 +154,21 @@ def test_argument_errors_return_before_launch(native):
               None) == native.RS_ERR_INVALID_ARG
     assert pg(None, None, None, None, None, None, 0, 5, 100, 2, ctypes.byref(ok), None, None,
               None, 0, None, 0, None) == native.RS_OK
+    # all-nodes schedule with row groups
+    tg = lib.resispec_verify_tree_group
+    tws = native.resispec_tree_group_workspace_bytes(4, 5)
+    assert tws > native.resispec_workspace_bytes(4, 5)
+    assert native.resispec_tree_group_workspace_bytes(0, 5) == 0
+    for g in (-1, 17):
+        assert tg(*args, 4, 5, 100, 2, ctypes.byref(ok), i32p, i32p, None, g, wsp, tws,
+                  None) == native.RS_ERR_INVALID_ARG
+    assert tg(*args, 4, 5, 100, 2, ctypes.byref(ok), i32p, i32p, None, 0, None, 0,
+              None) == native.RS_ERR_WORKSPACE
+    assert tg(*args, 4, 5, 100, 2, ctypes.byref(ok), i32p, i32p, None, 0, wsp, tws - 1,
+              None) == native.RS_ERR_WORKSPACE
+    assert tg(None, None, None, None, None, None, 0, 5, 100, 2, ctypes.byref(ok), None, None,
+              None, 0, None, 0, None) == native.RS_OK
+    assert lib.resispec_tree_group_size(0, 5, 100, ctypes.byref(ok)) == -1
     assert lib.resispec_path_group_size(0, 100, ctypes.byref(ok)) == -1
     assert lib.resispec_path_group_size(4, 100, ctypes.byref(_prm(native, dtype=5))) == -1
     # draft step

@@ -199,10 +199,10 @@ def test_path_groups_barrier_time_limit(gpu_lib):
     w = synth.make_workload(2, device="cuda", B=4, V=40000)
     ref = path_tree(gpu_lib, w, "resispec")
     try:
-        gpu_lib.resispec_debug_set_group_wait(0)
+        gpu_lib.resispec_debug_set_group_waits(barrier=0)
         g = group_tree(gpu_lib, w, "resispec", 4)
     finally:
-        gpu_lib.resispec_debug_set_group_wait(None)
+        gpu_lib.resispec_debug_set_group_waits()
     st = g["status"].cpu().numpy()
     _log("statuses with a zero time limit", st.tolist())
     assert set(st.tolist()) <= {0, 8}
@@ -214,3 +214,21 @@ def test_path_groups_barrier_time_limit(gpu_lib):
     assert np.array_equal(g["accepted_len"].cpu().numpy()[done],
                           ref["accepted_len"].cpu().numpy()[done])
     same(group_tree(gpu_lib, w, "resispec", 4), ref)
+
+
+def test_path_groups_formation_fallback(gpu_lib):
+    """Forced from the host (testing hook): with a formation limit of zero ticks nearly
+    every group is given up and its sequence done by one workgroup alone; formed or not,
+    every sequence gets the one-workgroup path's results, in every mode, and the default
+    limit restores normal grouping."""
+    w = synth.make_workload(2, device="cuda", B=6, V=40000)
+    for mode in MODES:
+        ref = path_tree(gpu_lib, w, mode)
+        try:
+            gpu_lib.resispec_debug_set_group_waits(formation=0)
+            for g in (2, 4, 0):
+                _log("path group with a zero formation limit", mode, g)
+                same(group_tree(gpu_lib, w, mode, g), ref)
+        finally:
+            gpu_lib.resispec_debug_set_group_waits()
+        same(group_tree(gpu_lib, w, mode, 4), ref)
