@@ -303,6 +303,18 @@ __device__ __forceinline__ void slot_sums_stage1(Smem& sm, int s_lo, int s_hi, b
     if (wantB) park_double(sm.partB, g * SG::GS, s, c);
 }
 
+// Stage 1 over one array of partials only (kernels with a single sum per slot).
+template <int BLK>
+__device__ __forceinline__ void slot_sums_stage1_one(float (&part)[64][kMaxSlots + 1], int s_lo, int s_hi) {
+    using SG = SlotGroups<BLK>;
+    const int s = threadIdx.x % kMaxSlots, g = threadIdx.x / kMaxSlots;
+    if (s < s_lo || s >= s_hi) return;
+    double a = 0.0;
+#pragma unroll
+    for (int l = 0; l < SG::GS; ++l) a += (double)part[g * SG::GS + l][s];
+    park_double(part, g * SG::GS, s, a);
+}
+
 template <int BLK>
 __device__ __forceinline__ double slot_group_sum(const float (&part)[64][kMaxSlots + 1], int s) {
     using SG = SlotGroups<BLK>;

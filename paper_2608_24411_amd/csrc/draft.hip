@@ -48,9 +48,28 @@ struct DParams {
     int32_t G, nslots;
 };
 
+// The draft kernel's shared state: one sum per slot, so 35 KB instead of the
+// verification kernels' 77 KB.  When a row's draws leave one wave running (draws without
+// replacement, or a single child), the other waves' registers and this small LDS let a
+// further row's workgroup start on the CU.
+struct DraftSmem {
+    int32_t decision;
+    int32_t next_slot;
+    double total;
+    int32_t wcount[kMaxWaves];
+    int32_t wbad[kMaxWaves];
+    int32_t cand_tok[kMaxCand];
+    int32_t cand_node[kMaxCand];
+    float cand_u[kMaxCand];
+    double cand_p[kMaxCand];
+    float wmax[2][kMaxWaves];
+    double slotA[kMaxSlots];
+    float partA[64][kMaxSlots + 1];
+};
+
 template <typename In, int VEC, int UNR>
 __global__ void __launch_bounds__(kBlock) __attribute__((amdgpu_waves_per_eu(4))) rs_draft_kernel(const DParams P) {
-    __shared__ Smem sm;
+    __shared__ DraftSmem sm;
     constexpr int kWaves = kBlock / 64;
     constexpr int CHUNK = 64 * VEC * UNR;
     using W = Vec<In, VEC>;
@@ -157,7 +176,7 @@ __global__ void __launch_bounds__(kBlock) __attribute__((amdgpu_waves_per_eu(4))
                 fa = 0.0f;
             });
         __syncthreads();
-        slot_sums_stage1<kBlock>(sm, 0, nslots, false);
+        slot_sums_stage1_one<kBlock>(sm.partA, 0, nslots);
         __syncthreads();
         if (tid < nslots) sm.slotA[tid] = slot_group_sum<kBlock>(sm.partA, tid);
         __syncthreads();
