@@ -237,6 +237,8 @@ struct Smem {
     float st_c[kMaxCand + 1];       // ResiSpec: Z * dscale * St/Sd.  Standard: C * St/Sd
     float st_a[kMaxCand + 1];       // ResiSpec: a
     float st_i[kMaxCand + 1];       // ResiSpec: 1/Z
+    float st_k1[kMaxCand + 1];      // ResiSpec: a/Z
+    float st_kc[kMaxCand + 1];      // ResiSpec: (1 - a) c/Z
     double st_zd[kMaxCand + 1], st_ad[kMaxCand + 1];
     double st_ds[kMaxCand + 1];     // draft scale (without replacement)
     double st_rx[kMaxCand + 1];     // R(x_i) of the tested candidate (normalised)

@@ -116,7 +116,9 @@ __device__ void zero_residual_row(const KParams& P, int64_t row) {
 // mass R (target units) and unnormalised draft mass Q:
 //   standard: A = max(R - C_i Q, 0)          (the collapsed recurrence, C_i = st_c[i])
 //   ResiSpec: A = min(c_i Q, R), B = R, both 0 at x_i   (c_i = Z_i dscale_i St/Sd),
-//             after the chain over the earlier steps 0..i-1.
+//             after the chain over the earlier steps 0..i-1.  A step of the chain,
+//             R <- (a (R - m) + m) / Z with m = min(c Q, R), equals
+//             min(a/Z R + (1 - a) c/Z Q, R/Z) because 0 <= a <= 1: four operations.
 template <int MODE>
 __device__ __forceinline__ void chain_terms(float R, float Q, int j, const Smem& sm, int i,
                                             float& A, float& Bv) {
@@ -126,8 +128,7 @@ __device__ __forceinline__ void chain_terms(float R, float Q, int j, const Smem&
         return;
     }
     for (int t = 0; t < i; ++t) {
-        const float m = fminf(sm.st_c[t] * Q, R);
-        R = fmaf(sm.st_a[t], R - m, m) * sm.st_i[t];
+        R = fminf(fmaf(sm.st_kc[t], Q, sm.st_k1[t] * R), sm.st_i[t] * R);
         if (j == sm.st_x[t]) R = 0.0f;
     }
     const bool x0 = j == sm.st_x[i];
@@ -778,14 +779,12 @@ __device__ __forceinline__ void verify_row(const KParams& P, Smem& sm, const int
                                 Q[u][e] = exp2_fast(expo(d[u][e], c2h, c2l, Kd));
                             }
                         for (int s2 = 0; s2 < ii; ++s2) {
-                            const float c = sm.st_c[s2], inv = sm.st_i[s2], a = sm.st_a[s2];
+                            const float kc = sm.st_kc[s2], k1 = sm.st_k1[s2], inv = sm.st_i[s2];
 #pragma unroll
                             for (int u = 0; u < UNR; ++u)
 #pragma unroll
-                                for (int e = 0; e < VEC; ++e) {
-                                    const float m = fminf(c * Q[u][e], R[u][e]);
-                                    R[u][e] = fmaf(a, R[u][e] - m, m) * inv;
-                                }
+                                for (int e = 0; e < VEC; ++e)
+                                    R[u][e] = fminf(fmaf(kc, Q[u][e], k1 * R[u][e]), inv * R[u][e]);
                             if (hit) {
                                 const int x = sm.st_x[s2];
 #pragma unroll
@@ -863,6 +862,8 @@ __device__ __forceinline__ void verify_row(const KParams& P, Smem& sm, const int
                     sm.st_ad[i] = a;
                     sm.st_a[i] = (float)a;
                     sm.st_i[i] = (float)(1.0 / z);
+                    sm.st_k1[i] = (float)(a / z);
+                    sm.st_kc[i] = (float)((1.0 - a) * sm.st_ds[i] * q2t);   // (1 - a) c / Z
                 }
             }
             if (lane == 0) {

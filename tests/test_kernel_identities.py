@@ -12,6 +12,8 @@ The kernel never materialises a residual row.  It evaluates:
   sum of max(p - C_i q, 0).  s_i is the draft scale of step i: 1 for i.i.d. candidates,
   and 1 / (1 - removed draft mass) without replacement.
 * min(c Q, R) as exp2(min(log2 R, log2 Q + log2 c)).
+* One step of that closed form as min(a/Z R + (1 - a) c/Z Q, R/Z), c Q = Z D, which
+  holds because 0 <= a <= 1 (the later rejection passes chain it).
 
 Each identity is compared with the oracle's own functions, which take the paper's
 steps one at a time.  These functions are pinned separately in test_oracle_pins.py.
@@ -104,3 +106,34 @@ def test_min_in_exponent_space(seed):
     lhs = np.minimum(c * np.exp2(aQ), np.exp2(aR))
     rhs = 2.0 ** f * np.exp2(np.minimum(aR - f, aQ + e))
     assert np.allclose(lhs, rhs, rtol=1e-13, atol=0)
+
+
+@pytest.mark.parametrize("seed", range(20))
+def test_getproxy_step_as_min_of_two_lines(seed):
+    """Several rejections in a row: the oracle's GetProxy steps against the kernel's
+    four-operation form of each step, min(k1 R + kc D, R / Z) with k1 = a / Z and
+    kc = (1 - a); also 0 <= a <= 1 at every step, which the form needs."""
+    rng = np.random.default_rng(3000 + seed)
+    V = int(rng.integers(4, 300))
+    R, D = _pair(rng, V)
+    chained = R.copy()
+    for step in range(int(rng.integers(2, 6))):
+        cand = np.flatnonzero((D > R) & (R > 0))
+        if cand.size == 0:
+            break
+        x0 = int(rng.choice(cand))
+        stepped, st = O.residual_update(R, O.get_proxy(R, D, x0)["K"])
+        assert st == O.OK
+        Z = D[x0] - R[x0]
+        m = np.minimum(Z * D, R)
+        m[x0] = 0.0
+        M = m.sum()
+        SR = 1.0 - R[x0]
+        a = (Z - M) / (SR - M) if SR - M > 0 else 0.0
+        assert -1e-15 <= a <= 1.0 + 1e-15
+        chained = np.minimum((a / Z) * chained + (1.0 - a) * D, chained / Z)
+        chained[x0] = 0.0
+        eps = np.finfo(np.float64).eps
+        tol = 1e-12 + 64 * eps * (np.abs(stepped) + stepped.sum()) / Z
+        assert (np.abs(chained - stepped) <= tol * 10 ** step).all()
+        R = stepped
