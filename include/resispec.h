@@ -168,11 +168,11 @@ rs_status resispec_verify_tree_path(const void* target_logits, const void* draft
  * formed group whose workgroups do not meet within 20 ms at a barrier reports
  * RS_SEQ_GROUP_TIMEOUT.
  *   group_size      : 0 = automatic (as many members as the device holds at once, up to
- *                     16 and to one per 16 slots of a row; 1 when that is under 2 or
+ *                     16 and to one per 8 slots of a row; 1 when that is under 2 or
  *                     workspace is NULL), 1 = one workgroup per sequence,
  *                     2..16 = that many (RS_ERR_UNSUPPORTED if B * group_size workgroups
- *                     cannot be resident at once, if the batch takes the 512-thread
- *                     schedule (B >= 2 per CU), or if a row has fewer slots than members)
+ *                     cannot be resident at once or if a row has fewer slots than
+ *                     members)
  *   workspace       : device buffer of at least resispec_path_workspace_bytes(B) bytes,
  *                     16-byte aligned, caller-owned; its counters are zeroed by the call
  *                     itself (on `stream`) before the verification kernel; NULL allowed

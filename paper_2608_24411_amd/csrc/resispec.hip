@@ -1316,6 +1316,25 @@ namespace {
 constexpr int kWalkBlock = 256;
 
 // compute units of the current device (queried once per device)
+// Workgroups of kPathBlock threads of kernel K that one CU holds at once, per device
+// (cached: the answer depends only on the kernel's resources); 0 if the query fails.
+template <auto K>
+int resident_per_cu() {
+    static std::atomic<int> cache[64];
+    int dev = 0;
+    if (hipGetDevice(&dev) != hipSuccess || dev < 0 || dev >= 64) dev = -1;
+    if (dev >= 0) {
+        const int n = cache[dev].load(std::memory_order_relaxed);
+        if (n > 0) return n;
+    }
+    int per_cu = 0;
+    if (hipOccupancyMaxActiveBlocksPerMultiprocessor(&per_cu, reinterpret_cast<const void*>(K), kPathBlock, 0) !=
+        hipSuccess)
+        per_cu = 0;
+    if (dev >= 0 && per_cu > 0) cache[dev].store(per_cu, std::memory_order_relaxed);
+    return per_cu;
+}
+
 int cu_count() {
     static std::atomic<int> cache[64];
     int dev = 0;
@@ -1371,11 +1390,7 @@ template <typename In, int VEC, int UNR, int MODE>
 int32_t resolve_group(const KParams& P, const PathOut* path) {
     if (path->group == 1 || (path->group == 0 && !path->ws)) return 1;
     if (!path->ws) return -1;
-    int per_cu = 0;
-    if (hipOccupancyMaxActiveBlocksPerMultiprocessor(
-            &per_cu, reinterpret_cast<const void*>(rs_path_kernel<In, VEC, UNR, MODE>), kPathBlock, 0) != hipSuccess)
-        per_cu = 0;
-    const int64_t cap = (int64_t)per_cu * cu_count();
+    const int64_t cap = (int64_t)resident_per_cu<rs_path_kernel<In, VEC, UNR, MODE>>() * cu_count();
     int64_t smax = (int64_t)kMaxGroup;
     if (cap / P.B < smax) smax = cap / P.B;
     if (path->group == 0) {
@@ -1402,7 +1417,8 @@ hipError_t launch_path_kernel(KParams P, PathOut* path, hipStream_t s) {
                            GroupArgs{1, nullptr, kGroupWaitTicks, kFormWaitTicks});
         return hipGetLastError();
     }
-    // a row group per sequence: counters zeroed, then every workgroup resident at once
+    // a row group per sequence: counters zeroed, then the members (which form their
+    // groups themselves)
     hipLaunchKernelGGL(rs_group_reset, dim3((unsigned)((P.B + 255) / 256)), dim3(256), 0, s, path->ws, P.B);
     const hipError_t e = hipGetLastError();
     if (e != hipSuccess) return e;
@@ -1433,12 +1449,7 @@ hipError_t launch_rowgroups(KParams P, int64_t nrows, RowGroupLaunch* rg, hipStr
     set_slots<VEC, UNR>(P);
     int32_t S = 1;
     if (rg->group >= 2 || (rg->group == 0 && rg->ws)) {
-        int per_cu = 0;
-        if (hipOccupancyMaxActiveBlocksPerMultiprocessor(
-                &per_cu, reinterpret_cast<const void*>(rs_rowgroup_kernel<In, VEC, UNR, MODE>), kPathBlock, 0) !=
-            hipSuccess)
-            per_cu = 0;
-        const int64_t cap = (int64_t)per_cu * cu_count();
+        const int64_t cap = (int64_t)resident_per_cu<rs_rowgroup_kernel<In, VEC, UNR, MODE>>() * cu_count();
         int64_t smax = (int64_t)kMaxGroup;
         if (cap / nrows < smax) smax = cap / nrows;
         if (rg->group == 0) {
