@@ -195,6 +195,12 @@ constexpr int64_t kGroupXbuf = 256;
 constexpr int64_t kGroupXmax = kGroupXbuf + 2 * 2 * kMaxSlots * (int64_t)sizeof(double);
 constexpr int32_t kMaxGroup = 16;
 constexpr int32_t kAutoRowGroup = 4;   // automatic members per row, all-nodes schedule
+// XCDs of the device, and when groups are placed on one XCD each: groups of at most 8
+// members, at least two groups per XCD (measured: a group that ends up alone on its XCD,
+// of 7 or of 15, is slower confined to that XCD's share of the chip)
+constexpr int64_t kXcds = 8;
+constexpr int32_t kXcdMaxMembers = 8;
+constexpr int64_t kXcdMinGroups = 2 * kXcds;
 static_assert(kGroupXmax + 2 * kMaxGroup * (int64_t)sizeof(float) <= kGroupStride, "group workspace layout");
 
 // Barrier of a row group with a time limit (20 ms of the 100 MHz wall clock unless a
@@ -1123,7 +1129,29 @@ struct GroupArgs {
     char* ws;
     uint64_t wait;       // barrier time limit (ticks)
     uint64_t form_wait;  // formation time limit (ticks)
+    int32_t groups;      // groups with work (sequences or rows)
+    int32_t xcd;         // 1: the XCD layout below
 };
+
+// Which group and member a workgroup is.  The dispatcher deals the workgroups of a launch
+// round-robin over the 8 XCDs (workgroup i runs on XCD i % 8), and each XCD has its own
+// L2.  In the XCD layout the S members of group g all run on XCD g % 8, so the traffic
+// of their barriers and exchanges stays within one L2: workgroup i = 8 k + x is member
+// k % S of group x + 8 (k / S).  The grid then holds a multiple of 8 groups, and the
+// workgroups of groups past the last return at once.  Without it, workgroup i is member
+// i % S of group i / S.  Returns false for a padding workgroup.
+__device__ __forceinline__ bool group_of(const GroupArgs& ga, int32_t& g, int32_t& w) {
+    const uint32_t i = blockIdx.x, S = (uint32_t)ga.S;
+    if (ga.xcd) {
+        const uint32_t k = i >> 3;
+        g = (int32_t)((i & 7u) + 8u * (k / S));
+        w = (int32_t)(k % S);
+    } else {
+        g = (int32_t)(i / S);
+        w = (int32_t)(i % S);
+    }
+    return g < ga.groups;
+}
 
 // Path-only schedule: a sequence's workgroup (or row group) walks its own tree from the
 // root and verifies only the nodes it reaches (each node's outcome depends on that
@@ -1142,8 +1170,8 @@ rs_path_kernel(const KParams P, int32_t max_depth, int32_t* __restrict__ out_tok
     __shared__ Smem sm;
     const int tid = threadIdx.x;
     const int32_t S = ga.S;
-    const int32_t b = (int32_t)(blockIdx.x / (uint32_t)S);
-    const int32_t member = (int32_t)blockIdx.x - b * S;
+    int32_t b, member;
+    if (!group_of(ga, b, member)) return;
     RowGroup grp{S, member, nullptr, nullptr, nullptr, 0u, ga.wait};
     bool lead = member == 0;
     if (S > 1) {
@@ -1231,8 +1259,8 @@ __global__ void __launch_bounds__(kPathBlock) __attribute__((amdgpu_waves_per_eu
 rs_rowgroup_kernel(const KParams P, const GroupArgs ga) {
     __shared__ Smem sm;
     const int32_t S = ga.S;
-    const int32_t g = (int32_t)(blockIdx.x / (uint32_t)S);
-    const int32_t member = (int32_t)blockIdx.x - g * S;
+    int32_t g, member;
+    if (!group_of(ga, g, member)) return;
     int64_t row;
     int32_t b, n;
     if (P.flat) {
@@ -1414,7 +1442,7 @@ hipError_t launch_path_kernel(KParams P, PathOut* path, hipStream_t s) {
     if (S == 1) {
         hipLaunchKernelGGL((rs_path_kernel<In, VEC, UNR, MODE>), dim3((unsigned)P.B), dim3(kPathBlock), 0, s,
                            P, path->max_depth, path->out_tokens, path->out_len, path->out_status,
-                           GroupArgs{1, nullptr, kGroupWaitTicks, kFormWaitTicks});
+                           GroupArgs{1, nullptr, kGroupWaitTicks, kFormWaitTicks, P.B, 0});
         return hipGetLastError();
     }
     // a row group per sequence: counters zeroed, then the members (which form their
@@ -1427,10 +1455,12 @@ hipError_t launch_path_kernel(KParams P, PathOut* path, hipStream_t s) {
     int32_t* ot = path->out_tokens;
     int32_t* ol = path->out_len;
     int32_t* os = path->out_status;
+    const bool xcd = S <= kXcdMaxMembers && P.B >= kXcdMinGroups;
     const GroupArgs ga{S, path->ws, g_group_wait.load(std::memory_order_relaxed),
-                       g_form_wait.load(std::memory_order_relaxed)};
-    hipLaunchKernelGGL((rs_path_kernel<In, VEC, UNR, MODE>), dim3((unsigned)((int64_t)P.B * S)), dim3(kPathBlock),
-                       0, s, kp, md, ot, ol, os, ga);
+                       g_form_wait.load(std::memory_order_relaxed), P.B, xcd ? 1 : 0};
+    const int64_t groups = xcd ? ((int64_t)P.B + kXcds - 1) / kXcds * kXcds : (int64_t)P.B;
+    hipLaunchKernelGGL((rs_path_kernel<In, VEC, UNR, MODE>), dim3((unsigned)(groups * S)), dim3(kPathBlock), 0, s,
+                       kp, md, ot, ol, os, ga);
     return hipGetLastError();
 }
 
@@ -1481,9 +1511,11 @@ hipError_t launch_rowgroups(KParams P, int64_t nrows, RowGroupLaunch* rg, hipStr
     const hipError_t e = hipGetLastError();
     if (e != hipSuccess) return e;
     KParams kp = P;
+    const bool xcd = S <= kXcdMaxMembers && nrows >= kXcdMinGroups;
     const GroupArgs ga{S, rg->ws, g_group_wait.load(std::memory_order_relaxed),
-                       g_form_wait.load(std::memory_order_relaxed)};
-    hipLaunchKernelGGL((rs_rowgroup_kernel<In, VEC, UNR, MODE>), dim3((unsigned)(nrows * S)), dim3(kPathBlock), 0,
+                       g_form_wait.load(std::memory_order_relaxed), (int32_t)nrows, xcd ? 1 : 0};
+    const int64_t groups = xcd ? (nrows + kXcds - 1) / kXcds * kXcds : nrows;
+    hipLaunchKernelGGL((rs_rowgroup_kernel<In, VEC, UNR, MODE>), dim3((unsigned)(groups * S)), dim3(kPathBlock), 0,
                        s, kp, ga);
     return hipGetLastError();
 }

@@ -40,7 +40,9 @@ def same(a, b):
 
 CASES = [(1, dict(B=8)), (2, dict(B=4)), (3, dict(B=3)), (4, dict(B=8)),
          (1, dict(B=4, V=32003)), (2, dict(B=2, V=100003, dtype="f32")),
-         (3, dict(B=2, V=65537, dtype="bf16")), (4, dict(B=3, V=4099))]
+         (3, dict(B=2, V=65537, dtype="bf16")), (4, dict(B=3, V=4099)),
+         # 21 sequences: groups placed one XCD each, the grid padded to 24 groups
+         (4, dict(B=21, V=20000))]
 
 
 @pytest.mark.parametrize("cfg,over", CASES, ids=[f"cfg{c}-{o}" for c, o in CASES])
