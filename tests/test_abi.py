@@ -232,3 +232,21 @@ def test_build_rejects_register_spills():
         "x.hip:12:1: remark:     VGPRs Spill: 0 [-Rpass-analysis=kernel-resource-usage]",
     ])
     assert build._spills(report) == [("k_bad", 50, 204), ("k_stack", 0, 16)]
+
+
+def test_plain_c_caller(tmp_path):
+    """The header is plain C: a C99 program built with gcc -Werror -pedantic against it and
+    linked to the library calls its host-side functions and argument checks."""
+    import shutil
+    import subprocess
+    from paper_2608_24411_amd import native
+    gcc = shutil.which("gcc")
+    if gcc is None:
+        pytest.skip("gcc not found")
+    libdir = os.path.dirname(native.LIB_PATH)
+    exe = str(tmp_path / "c_consumer")
+    subprocess.run([gcc, "-std=c99", "-Wall", "-Wextra", "-Werror", "-pedantic", "-I", HEADER_DIR,
+                    os.path.join(ROOT, "tests", "c_consumer.c"), "-o", exe, "-L", libdir,
+                    "-lresispec", "-Wl,-rpath," + libdir], check=True)
+    r = subprocess.run([exe], capture_output=True, text=True, timeout=60)
+    assert r.returncode == 0 and r.stdout.strip() == "ok", r.stdout + r.stderr
