@@ -123,6 +123,26 @@ def test_tree_parity_reduced(gpu_lib, cfg, over, mode):
     assert torch.equal(plain["accepted_len"], gpu["accepted_len"])
 
 
+@pytest.mark.parametrize("T", [0.2, 0.5, 1.5, 3.0])
+@pytest.mark.parametrize("mode", MODES)
+def test_tree_parity_temperatures(gpu_lib, T, mode):
+    """Temperatures away from the recipes' own (0.7-1.0): at T = 0.2 the exponents of a
+    Zipf row span hundreds of binades and most elements underflow against the row's
+    reference; at T = 3 the rows are nearly flat.  Ragged vocabularies, both dtypes,
+    walk and node outcomes against the oracle."""
+    for cfg, over in ((2, dict(B=2, V=40003)), (4, dict(B=3, V=30000, dtype="f32"))):
+        _log("tree parity at T", T, cfg, over, mode)
+        w = synth.make_workload(cfg, device="cuda", T=T, **over)
+        h = host_tree(w)
+        gpu = gpu_tree(gpu_lib, w, mode, debug=True)
+        n_cmp, _ = compare_walk(gpu, oracle_walk(h, w, mode))
+        assert n_cmp >= w["B"] - 1
+        B, N = h["parent"].shape
+        n_cmp, n_flag, _ = compare_nodes(gpu, h, w, mode)
+        _log("  nodes compared", n_cmp, "flagged", n_flag)
+        assert n_cmp >= 0.8 * B * N
+
+
 @pytest.mark.parametrize("cfg,nsample", [(1, 64), (2, 6), (3, 4), (4, 4)])
 def test_tree_parity_full_size_sampled(gpu_lib, cfg, nsample):
     """Full configurations in the launch shape the benchmark times; the oracle checks a
