@@ -107,7 +107,9 @@ rs_status resispec_verify(const void* target_logits, const void* draft_logits,
                           int32_t* out_accepted_len, int32_t* out_status, void* stream);
 
 /*
- * Tree verify over B sequences of N nodes each (node 0 = root).
+ * Tree verify over B sequences of N nodes each (node 0 = root): Algorithm 1 at every node
+ * (accept test Eq. 2; residual update Eq. 1/2 or GetProxy by prm->mode), then the walk
+ * down the accepted children of the tree-structured verification (§Preliminary).
  *   target_logits, draft_logits : [B][N][V]; row n is the target / draft distribution
  *                                 over the tokens that follow node n (the distribution
  *                                 node n's children were drawn from).  Draft rows of
@@ -157,16 +159,16 @@ rs_status resispec_verify_tree_path(const void* target_logits, const void* draft
                                     int32_t* out_accepted_len, int32_t* out_status, void* stream);
 
 /*
- * The path-only schedule with row groups, for batches too small to fill the device with
- * one workgroup per sequence (same results as resispec_verify_tree_path and
- * resispec_verify_tree, bit for bit).  Each sequence gets `group_size` 512-thread
- * workgroups that verify every row of its walk together: each sweeps its share of the
- * row's slots in every pass, and after a pass they exchange their slots' totals through
- * `workspace` and meet at a barrier (a counter in global memory).  The group forms only
- * when all its workgroups have started within 20 us of the first; otherwise the first to
- * give up waiting does the sequence alone (same results).  Every wait is bounded: a
- * formed group whose workgroups do not meet within 20 ms at a barrier reports
- * RS_SEQ_GROUP_TIMEOUT.
+ * The path-only schedule (§Preliminary walk, Algorithm 1 at each node it reaches) with row
+ * groups, for batches too small to fill the device with one workgroup per sequence (same
+ * results as resispec_verify_tree_path and resispec_verify_tree, bit for bit). Each
+ * sequence gets `group_size` 512-thread workgroups that verify every row of its walk
+ * together: each sweeps its share of the row's slots in every pass, and after a pass they
+ * exchange their slots' totals through `workspace` and meet at a barrier (a counter in
+ * global memory).  The group forms only when all its workgroups have started within 20 us
+ * of the first; otherwise the first to give up waiting does the sequence alone (same
+ * results).  Every wait is bounded: a formed group whose workgroups do not meet within 20
+ * ms at a barrier reports RS_SEQ_GROUP_TIMEOUT.
  *   group_size      : 0 = automatic (as many members as the device holds at once, up to
  *                     16 and to one per 8 slots of a row; 1 when that is under 2 or
  *                     workspace is NULL), 1 = one workgroup per sequence,
@@ -189,12 +191,12 @@ rs_status resispec_verify_tree_path_group(const void* target_logits, const void*
                                           size_t workspace_bytes, void* stream);
 
 /*
- * resispec_verify_tree with row groups, for batches of few rows (same results, bit for
- * bit): every node row gets `group_size` 512-thread workgroups that verify it together,
- * exchanging slot totals through the workspace at bounded barriers like the path
- * schedule's row groups (a group that does not form within 20 us is done by one of its
- * workgroups alone; RS_SEQ_GROUP_TIMEOUT after 20 ms at a barrier), then the walk runs
- * as in resispec_verify_tree.
+ * resispec_verify_tree (Algorithm 1 at every node, §Preliminary walk) with row groups, for
+ * batches of few rows (same results, bit for bit): every node row gets `group_size`
+ * 512-thread workgroups that verify it together, exchanging slot totals through the
+ * workspace at bounded barriers like the path schedule's row groups (a group that does not
+ * form within 20 us is done by one of its workgroups alone; RS_SEQ_GROUP_TIMEOUT after 20
+ * ms at a barrier), then the walk runs as in resispec_verify_tree.
  *   group_size : 0 = automatic (at most one workgroup per CU for B * N rows, up to 4
  *                members per row, one per 8 slots of a row and one per 64 KiB of a row's
  *                logits; 1 = the ordinary one-workgroup row kernel when that is under 2),
@@ -269,7 +271,7 @@ rs_status resispec_draft_candidates(const void* draft_logits, const int32_t* par
 
 /*
  * The two stages of resispec_verify_tree, for callers that schedule them separately
- * (same kernels, same results):
+ * (same kernels, same results): Algorithm 1 at every node, then the walk of §Preliminary.
  *   resispec_verify_nodes: every node's own outcome (accepted child or drawn token) into
  *     `workspace`, from the same inputs as resispec_verify_tree;
  *   resispec_walk: the walk from each root over the outcomes in `workspace` (written by
