@@ -154,3 +154,18 @@ def test_graph_draft_then_verify(gpu_lib):
         _log("draft then verify, replay", i, static["accepted_len"].tolist())
         assert torch.equal(tok, ref_tok)
         _same(static, ref)
+
+
+def test_binding_stream_is_torch_current_stream(gpu_lib):
+    """The binding launches on torch's current stream: the default one, a side stream in a
+    stream context, and the capture stream (covered by the graph tests above)."""
+    from paper_2608_24411_amd import native
+
+    def handle(stream):
+        return native._stream(stream).value or 0   # a NULL handle reads as None
+    assert handle(None) == torch.cuda.current_stream().cuda_stream
+    side = torch.cuda.Stream()
+    with torch.cuda.stream(side):
+        assert handle(None) == side.cuda_stream
+        assert handle(None) == torch.cuda.current_stream().cuda_stream
+    assert handle(side) == side.cuda_stream
