@@ -235,6 +235,8 @@ def main():
     ap.add_argument("--no-other-mode", action="store_true")
     ap.add_argument("--no-path", action="store_true", help="skip the path-only schedule")
     ap.add_argument("--no-draft", action="store_true", help="skip the draft step")
+    ap.add_argument("--no-single", action="store_true",
+                    help="skip the single-tree latency of the same shape")
     ap.add_argument("--no-read-probe", action="store_true",
                     help="skip the read-bandwidth probe (the measured ceiling)")
     ap.add_argument("--study", action="store_true",
@@ -390,6 +392,43 @@ def main():
         draft = {"kernel_ms": dms, "rows_per_s": B * N / (dms * 1e-3),
                  "alg_bytes_per_launch": d_bytes, "achieved_gbps": d_bytes / (dms * 1e-3) / 1e9}
 
+    # one tree of the same shape (the latency case of serving one sequence): the all-nodes
+    # schedule with row groups at the size the library picks; device time per call with
+    # 100 calls queued back to back, median of 5 such runs
+    single = None
+    if not args.no_single:
+        w1 = synth.make_workload(args.config, device="cuda", B=1)
+        a1 = (w1["target"], w1["draft"], w1["node_token"], w1["parent"], w1["u_accept"],
+              w1["u_resample"])
+        kw1 = dict(temperature=w1["temperature"], max_depth=w1["max_depth"], mode=args.mode,
+                   without_replacement=w1["without_replacement"], bonus=w1["bonus"])
+        ws1 = torch.empty(max(1, native.resispec_tree_group_workspace_bytes(1, N)),
+                          dtype=torch.uint8, device="cuda")
+        o1 = (torch.empty((1, w1["max_depth"] + 1), dtype=torch.int32, device="cuda"),
+              torch.empty(1, dtype=torch.int32, device="cuda"),
+              torch.empty(1, dtype=torch.int32, device="cuda"))
+        g1 = native.resispec_tree_group_size(1, N, V, dtype="bf16" if esz == 2 else "f32",
+                                             mode=args.mode)
+
+        def sstep():
+            native.resispec_verify_tree_group(*a1, group_size=0, workspace=ws1, out_tokens=o1[0],
+                                              out_accepted_len=o1[1], out_status=o1[2], **kw1)
+        for _ in range(20):
+            sstep()
+        torch.cuda.synchronize()
+        per_call = []
+        for _ in range(5):
+            e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+            e0.record()
+            for _ in range(100):
+                sstep()
+            e1.record()
+            torch.cuda.synchronize()
+            per_call.append(e0.elapsed_time(e1) * 1e3 / 100)
+        assert int(o1[2].cpu()[0]) == 0, "device status not OK"
+        single = {"B": 1, "schedule": "all-nodes with row groups", "group_size": g1,
+                  "us_per_call": float(np.median(per_call)), "calls_queued": 100}
+
     probe = None if args.no_read_probe else read_ceiling(torch)
 
     r = results[args.mode]
@@ -427,6 +466,7 @@ def main():
         "modes": results,
         "path_schedule": path,
         "draft_step": draft,
+        "single_tree": single,
     }
     if not args.no_cpu_baseline:
         out["cpu_baseline"] = cpu_baseline(w, args.cpu_seconds, args.mode)
