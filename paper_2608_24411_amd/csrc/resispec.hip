@@ -22,8 +22,9 @@
 //            i.e. norm(max(R - K, 0)) for the proxy K = R - r, K(x0) = D(x0).  So the
 //            residual is never materialised: every pass re-derives R_j from the two
 //            logits of token j through the chain of per-rejection scalars.  After the
-//            first rejection min(c Q, R) = exp2(min(log2 R, log2 Q + log2 c)) takes a
-//            single exponential per element;
+//            first rejection pass min(c Q, R) = exp2(min(log2 R, log2 Q + log2 c))
+//            takes a single exponential per element, and each later step of the chain
+//            is min(a/Z R + (1 - a) c/Z Q, R/Z);
 //   draw     when every candidate is rejected (or the node is a leaf: bonus draw from
 //            p), the token is the smallest j whose running sum of the final residual in
 //            vocabulary order exceeds u * total.  The last pass records partial sums
@@ -41,8 +42,9 @@
 // constants).
 //
 // A second kernel walks each tree from the root along accepted children; a third
-// (the path-only schedule) verifies only the nodes each walk reaches.  The draft step
-// that precedes verification is in draft.hip; shared helpers are in common.h.
+// (the path-only schedule) verifies only the nodes each walk reaches, and a fourth
+// verifies each row of a small batch with several workgroups (row groups).  The draft
+// step that precedes verification is in draft.hip; shared helpers are in common.h.
 
 #include <atomic>
 
@@ -172,8 +174,8 @@ __device__ double scalar_residual(const Smem& sm, int i, double p, double q, int
 // Verification of one node row by the whole workgroup: node n of sequence b (row
 // b * N + n; flat rows: b = row, n = 0).  emit(child, token, status) is called by
 // thread 0 once, with the node's outcome.
-// Workgroups that verify one row together (the path schedule with few sequences, one
-// workgroup per CU): member w of S sweeps slots [w * nslots / S, (w + 1) * nslots / S)
+// Workgroups that verify one row together (row groups of the path schedule or of the
+// all-nodes schedule, one workgroup per CU): member w of S sweeps slots [w * nslots / S, (w + 1) * nslots / S)
 // in every pass; after a pass the members publish their slots' totals in global memory
 // and meet at a barrier, then all continue from the same totals in the same order, so
 // each decision is taken identically by every member.  S = 1: one workgroup per row.
@@ -1121,9 +1123,10 @@ __global__ void __launch_bounds__(kBlock) __attribute__((amdgpu_waves_per_eu(4))
     }, solo);
 }
 
-// Row groups of the path schedule: S members per sequence (workgroups b * S .. b * S +
-// S - 1) and the workspace that holds each sequence's group state (kGroupStride bytes
-// per sequence).  S = 1 needs no workspace.
+// Row groups: S members per sequence (path schedule) or per row (all-nodes schedule),
+// the workspace that holds each group's state (kGroupStride bytes per group), and the
+// time limits; group_of below says which workgroup is which member.  S = 1 needs no
+// workspace.
 struct GroupArgs {
     int32_t S;
     char* ws;
@@ -1157,7 +1160,8 @@ __device__ __forceinline__ bool group_of(const GroupArgs& ga, int32_t& g, int32_
 // root and verifies only the nodes it reaches (each node's outcome depends on that
 // node's rows and uniforms alone, so the result equals the all-nodes schedule followed
 // by the walk, bit for bit: rows are cut into the same chunks and slots, and summed in
-// the same order).  Member 0 of a group writes the outputs.  The walk keeps its state
+// the same order).  Member 0 of a group (or the member that claimed the sequence)
+// writes the outputs.  The walk keeps its state
 // live across every row, so these workgroups take up to 256 registers per lane (two
 // waves per SIMD, one workgroup per CU) and nothing is spilled.
 constexpr int kPathBlock = 512;
@@ -1251,9 +1255,10 @@ __global__ void rs_group_reset(char* __restrict__ ws, int32_t count) {
 }
 
 // All-nodes schedule with row groups, for batches of few rows: S workgroups per node row
-// (workgroups g * S .. g * S + S - 1 verify row g of the node-major order, with the
-// row group of g at ws + g * kGroupStride).  The same chunks, slots and summation order
-// as the row kernel, so the outcomes are identical; member 0 writes them.
+// (group g of group_of verifies row g of the node-major order, with its state at
+// ws + g * kGroupStride).  The same chunks, slots and summation order as the row kernel,
+// so the outcomes are identical; member 0 (or the member that claimed the row) writes
+// them.
 template <typename In, int VEC, int UNR, int MODE>
 __global__ void __launch_bounds__(kPathBlock) __attribute__((amdgpu_waves_per_eu(2)))
 rs_rowgroup_kernel(const KParams P, const GroupArgs ga) {
