@@ -62,6 +62,9 @@ def _load():
     lib.or_invcdf.argtypes = [P, i64, ctypes.c_double, P, P]
     lib.or_verify_node.argtypes = [P, P, i64, P, P, i32, f32, i32, i32,
                                    ctypes.POINTER(NodeResult), P]
+    lib.or_check_node_outcome.argtypes = [P, P, i64, P, P, i32, f32, i32, i32, i32, i32, P]
+    lib.or_check_tree_nodes.argtypes = [P, P, i32, P, P, P, P, i32, i32, i64, f32,
+                                        i32, i32, i32, P, i64, P, P, P, P]
     lib.or_verify_node_batch.argtypes = [P, P, i64, P, P, P, i32, i64, i32, i32, P, P]
     lib.or_enumerate.argtypes = [P, P, i32, i32, i32, i32, P]
     lib.or_verify_tree_walk.argtypes = [P, P, i32, P, P, P, P, i32, i32, i64, i32, f32,
@@ -76,10 +79,12 @@ def _load():
     lib.or_node_uniforms.argtypes = [u64, u64, i32, i32, P, P, P]
     lib.or_node_uniforms.restype = None
     lib.or_sample_candidates.argtypes = [P, i32, i64, f32, i32, i32, P, P, P]
+    lib.or_check_candidates.argtypes = [P, i32, i64, f32, i32, i32, P, P, P]
     lib.or_draft_tree.argtypes = [P, i32, P, i32, i32, i64, f32, i32, u64, u64, P, P, P, P, P]
     for name in ("or_softmax", "or_get_proxy", "or_residual_update", "or_draft_remove",
                  "or_invcdf", "or_verify_node", "or_verify_node_batch", "or_enumerate",
                  "or_verify_tree_walk", "or_verify_tree_nodes", "or_sample_candidates",
+                 "or_check_node_outcome", "or_check_tree_nodes", "or_check_candidates",
                  "or_draft_tree"):
         getattr(lib, name).restype = i32
     _lib = lib
@@ -165,6 +170,25 @@ def verify_node(p, q, cand, ua, ur, mode="resispec", without_replacement=False,
     if want_residual:
         out["final_R"] = fr
     return out
+
+
+def check_node_outcome(p, q, cand, ua, ur, claim_index, claim_token, mode="resispec",
+                       without_replacement=False):
+    """Whether a claimed outcome of one node is admissible with decisions inside the flag
+    window free to go either way: 1 (agrees outside the window), 2 (only through a
+    windowed decision), 0 (not admissible)."""
+    p = _f64(p)
+    V = p.shape[0]
+    cand = np.ascontiguousarray(cand, dtype=np.int32)
+    ua = np.ascontiguousarray(ua, dtype=np.float32)
+    q = _f64(q) if q is not None else np.zeros(V)
+    verdict = ctypes.c_int32(-1)
+    st = _load().or_check_node_outcome(_ptr(p), _ptr(q), V, _ptr(cand), _ptr(ua), cand.shape[0],
+                                       float(ur), _MODES[mode], int(bool(without_replacement)),
+                                       int(claim_index), int(claim_token), ctypes.byref(verdict))
+    if st != OK:
+        raise ValueError("or_check_node_outcome failed (%d)" % st)
+    return verdict.value
 
 
 def verify_node_batch(p, q, cand, ua, ur, mode="resispec", without_replacement=False):
@@ -253,6 +277,31 @@ def verify_tree_nodes(target, draft, node_token, parent, u_accept, u_resample, r
     return out
 
 
+def check_tree_nodes(target, draft, node_token, parent, u_accept, u_resample, rows, claim_child,
+                     claim_token, claim_status, *, temperature, mode="resispec",
+                     without_replacement=False, bonus=True):
+    """Verdicts (1, 2 or 0 as in check_node_outcome) of claimed (child, token, status)
+    outcomes of the given rows."""
+    t, d, dt, tok, par, ua, ur = _tree_inputs(target, draft, node_token, parent, u_accept,
+                                              u_resample)
+    B, N, V = t.shape
+    rows = np.ascontiguousarray(rows, dtype=np.int64)
+    cc = np.ascontiguousarray(claim_child, dtype=np.int32)
+    ct = np.ascontiguousarray(claim_token, dtype=np.int32)
+    cs = np.ascontiguousarray(claim_status, dtype=np.int32)
+    if not (rows.shape == cc.shape == ct.shape == cs.shape):
+        raise ValueError("rows and claims must have one entry each")
+    verdict = np.empty(rows.shape[0], dtype=np.int32)
+    st = _load().or_check_tree_nodes(_ptr(t), _ptr(d), dt, _ptr(tok), _ptr(par), _ptr(ua),
+                                     _ptr(ur), B, N, V, float(temperature), _MODES[mode],
+                                     int(bool(without_replacement)), int(bool(bonus)),
+                                     _ptr(rows), rows.shape[0], _ptr(cc), _ptr(ct), _ptr(cs),
+                                     _ptr(verdict))
+    if st != OK:
+        raise ValueError("or_check_tree_nodes failed (%d)" % st)
+    return verdict
+
+
 # ------------------------------------------------------------------ draft step ----
 
 def philox4x32_10(counter, key):
@@ -284,6 +333,21 @@ def sample_candidates(draft_row, k, uc, *, temperature, without_replacement=Fals
     st = _load().or_sample_candidates(_ptr(a), dt, a.shape[-1], float(temperature), int(k),
                                       int(bool(without_replacement)), _ptr(uc), _ptr(tok), _ptr(mg))
     return tok, mg, st
+
+
+def check_candidates(draft_row, claimed, uc, *, temperature, without_replacement=False):
+    """Verdict (1 exact, 2 admissible through a windowed draw, 0 not admissible) of
+    claimed candidate draws from one draft row with uniforms uc."""
+    a, dt = _logits(draft_row)
+    claimed = np.ascontiguousarray(claimed, dtype=np.int32)
+    uc = np.ascontiguousarray(uc, dtype=np.float32)
+    verdict = ctypes.c_int32(-1)
+    st = _load().or_check_candidates(_ptr(a), dt, a.shape[-1], float(temperature),
+                                     claimed.shape[0], int(bool(without_replacement)), _ptr(uc),
+                                     _ptr(claimed), ctypes.byref(verdict))
+    if st != OK:
+        raise ValueError("or_check_candidates failed (%d)" % st)
+    return verdict.value
 
 
 def draft_tree(draft, parent, *, temperature, without_replacement=False, seed=0, offset=0):

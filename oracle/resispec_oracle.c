@@ -9,8 +9,9 @@
  *   - softmax with temperature: Preliminary (target/draft distributions), and the
  *     decoding configuration of the Reproducibility appendix (temperature, nucleus 1.0);
  *   - standard residual, Eq. (1), and the multi-candidate recurrence, Eq. (2);
- *   - Algorithm 1 (ResiSpec Sampling and Verification) with its GetProxy function,
- *     read together with the Step 1-3 description that follows it;
+ *   - Algorithm 1 (ResiSpec Sampling and Verification), with the proxy it subtracts
+ *     built from Definition 1 (proxy mechanism), its probability and local-alignment
+ *     constraints and Proposition 1 (global mass identity);
  *   - tree walk: Preliminary, "Multi-candidate Tree-structured Verification".
  */
 #include "resispec_oracle.h"
@@ -57,56 +58,54 @@ int32_t or_softmax(const void* logits, int32_t dtype, int64_t V, float temperatu
     return OR_OK;
 }
 
-/* Algorithm 1, function GetProxy(p, q, x0), applied to the current residual R
- * (in the role of p) and the current draft D (in the role of q):
- *   budget      Z = D(x0) - R(x0)
- *   projection  r_j = min(Z * D_j, R_j) for j != x0, r_x0 = 0
- *   deficit     Delta = Z - sum_j r_j
- *   redistribution: Delta is spread over the remaining capacity R_j - r_j of the
- *               tokens j != x0, in proportion to that capacity (one-shot fill,
- *               x0 keeps r_x0 = 0 as the projection step fixed it)
- *   proxy       K = R - r + s, then K(x0) = D(x0); the slack s is what the last
- *               assignment adds, so it is non-zero only at x0 where r is zero
- *               (disjoint supports, Definition 1). */
+/* The proxy of Definition 1 for the residual R (in the place of the target) and the
+ * draft D once the candidate x0 has been rejected (Algorithm 1 calls it with the
+ * current pair; reading A-4).  Definition 1 writes the proxy as k = R - r + s:
+ *
+ *  - s, the slack, is fixed by the local-alignment constraint k(x0) = D(x0).  No mass
+ *    can be reserved at x0 (R is exhausted there, r(x0) = 0), so s(x0) = D(x0) - R(x0);
+ *    the algorithm's budget Z is exactly this gap, and by Proposition 1 (sum s = Z) the
+ *    slack has no mass anywhere else.
+ *  - r, the reserved mass, is the residual the proxy leaves behind (R' = r / Z).  Its
+ *    ideal shape is the draft scaled to the budget, Z * D, which the target cannot
+ *    always hold: r <= R caps it, and the mass the cap removes is given back to the
+ *    tokens that still have headroom R_j - min(Z D_j, R_j), in proportion to that
+ *    headroom (reading A-2; x0 has neither a share of the shape nor headroom), so that
+ *    r sums to Z.
+ *
+ * The four sums the construction rests on are returned in info: Z, the capped shape's
+ * mass M, the missing mass Z - M and the total headroom C. */
 int32_t or_get_proxy(const double* R, const double* D, int64_t V, int64_t x0,
                      double* r, double* s, double* K, or_proxy_info* info) {
     if (!R || !D || !r || !s || !K || V <= 0 || x0 < 0 || x0 >= V) return OR_BAD_ARG;
     const double Z = D[x0] - R[x0];
     if (!(Z > 0.0)) return OR_BAD_ARG;
 
-    /* Step 1: budgeting and initial projection. */
-    for (int64_t j = 0; j < V; ++j) {
-        if (j == x0) { r[j] = 0.0; continue; }
-        const double want = Z * D[j];
-        r[j] = (want < R[j]) ? want : R[j];
-    }
+    /* the capped shape (kept in r for now) and its mass */
     double M = 0.0;
-    for (int64_t j = 0; j < V; ++j) M += r[j];
-    const double delta = Z - M;
-
-    /* Step 2: capacity-aware redistribution of the deficit. */
-    double C = 0.0;
     for (int64_t j = 0; j < V; ++j) {
-        const double cap = (j == x0) ? 0.0 : (R[j] - r[j]);
-        C += cap;
+        r[j] = (j == x0) ? 0.0 : fmin(Z * D[j], R[j]);
+        M += r[j];
     }
-    if (C > 0.0) {
-        for (int64_t j = 0; j < V; ++j) {
-            if (j == x0) continue;
-            const double cap = R[j] - r[j];
-            r[j] += delta * cap / C;
-        }
-    }
+    /* headroom left under the cap, and the share of it the missing mass fills */
+    double C = 0.0;
+    for (int64_t j = 0; j < V; ++j) C += (j == x0) ? 0.0 : R[j] - r[j];
+    const double missing = Z - M;
+    const double fill = (C > 0.0) ? missing / C : 0.0;
+    for (int64_t j = 0; j < V; ++j)
+        if (j != x0) r[j] += fill * (R[j] - r[j]);
 
-    /* Step 3: proxy formulation with the local alignment at x0. */
-    for (int64_t j = 0; j < V; ++j) K[j] = R[j] - r[j];
-    K[x0] = D[x0];
-    for (int64_t j = 0; j < V; ++j) s[j] = K[j] - (R[j] - r[j]);
+    /* the proxy: away from x0 there is no slack and K = R - r; at x0 the alignment
+     * constraint fixes K(x0) = D(x0), which is R(x0) - r(x0) plus the slack Z */
+    for (int64_t j = 0; j < V; ++j) {
+        s[j] = (j == x0) ? Z : 0.0;
+        K[j] = (j == x0) ? D[x0] : R[j] - r[j];
+    }
 
     if (info) {
         info->Z = Z;
         info->M = M;
-        info->delta = delta;
+        info->delta = missing;
         info->C = C;
     }
     return OR_OK;
@@ -184,7 +183,59 @@ static void result_init(or_node_result* res) {
     res->sample_margin = 1e300;
 }
 
-/* Algorithm 1 (mode RESISPEC) / Eq. (2) (mode SPECINFER) for one node. */
+/* Scratch rows of one node's verification. */
+typedef struct {
+    double *R, *D, *Rn, *r, *s, *K;
+} node_rows;
+
+static int node_rows_alloc(node_rows* w, int64_t V) {
+    const size_t bytes = (size_t)V * sizeof(double);
+    w->R = (double*)malloc(bytes);
+    w->D = (double*)malloc(bytes);
+    w->Rn = (double*)malloc(bytes);
+    w->r = (double*)malloc(bytes);
+    w->s = (double*)malloc(bytes);
+    w->K = (double*)malloc(bytes);
+    return w->R && w->D && w->Rn && w->r && w->s && w->K;
+}
+
+static void node_rows_free(node_rows* w) {
+    free(w->R); free(w->D); free(w->Rn); free(w->r); free(w->s); free(w->K);
+}
+
+/* The state after candidate x is rejected.  The residual loses what was subtracted for
+ * the test, norm(max(R - K, 0)): K is the draft itself in the standard recurrence
+ * (Eq. 2) and the proxy of Definition 1 in ResiSpec (Algorithm 1).  Without
+ * replacement x also leaves the draft (reading A-6). */
+static int32_t reject_candidate(node_rows* w, int64_t V, int32_t x, int32_t mode, int32_t worep) {
+    const double* K = w->D;
+    if (mode == OR_MODE_RESISPEC) {
+        const int32_t st = or_get_proxy(w->R, w->D, V, x, w->r, w->s, w->K, NULL);
+        if (st != OR_OK) return st;
+        K = w->K;
+    }
+    const int32_t st = or_residual_update(w->R, K, V, w->Rn);
+    if (st != OR_OK) return st;
+    double* t = w->R;
+    w->R = w->Rn;
+    w->Rn = t;
+    if (worep) (void)or_draft_remove(w->D, V, x);
+    return OR_OK;
+}
+
+/* The checks every tested candidate passes before its ratio is formed. */
+static int32_t candidate_fault(const node_rows* w, int64_t V, int32_t x, double u) {
+    if (x < 0 || (int64_t)x >= V) return OR_BAD_TOKEN;
+    if (!(u >= 0.0 && u < 1.0)) return OR_BAD_UNIFORM;
+    if (!(w->D[x] > 0.0)) return OR_ZERO_DRAFT;
+    return OR_OK;
+}
+
+/* One node (mode RESISPEC: Algorithm 1; mode SPECINFER: Eq. 2).  Candidate i is
+ * accepted when its uniform falls strictly below R(x_i) / D(x_i) for the residual and
+ * draft left by the candidates before it; the first accepted candidate ends the node.
+ * When none is accepted (or there is none), the node's token is the inverse-CDF draw
+ * from the last residual. */
 int32_t or_verify_node(const double* p, const double* q, int64_t V,
                        const int32_t* cand, const float* ua, int32_t b, float ur,
                        int32_t mode, int32_t without_replacement,
@@ -195,74 +246,124 @@ int32_t or_verify_node(const double* p, const double* q, int64_t V,
     result_init(res);
     if (final_R) memset(final_R, 0, (size_t)V * sizeof(double));
 
-    const size_t bytes = (size_t)V * sizeof(double);
-    double* R  = (double*)malloc(bytes);
-    double* D  = (double*)malloc(bytes);
-    double* Rn = (double*)malloc(bytes);
-    double* r  = (double*)malloc(bytes);
-    double* s  = (double*)malloc(bytes);
-    double* K  = (double*)malloc(bytes);
-    if (!R || !D || !Rn || !r || !s || !K) {
-        free(R); free(D); free(Rn); free(r); free(s); free(K);
+    node_rows w;
+    if (!node_rows_alloc(&w, V)) {
+        node_rows_free(&w);
         return OR_BAD_ARG;
     }
-    memcpy(R, p, bytes);                 /* residual R <- P */
-    if (b > 0) memcpy(D, q, bytes);      /* draft D <- Q */
+    const size_t bytes = (size_t)V * sizeof(double);
+    memcpy(w.R, p, bytes);
+    if (b > 0) memcpy(w.D, q, bytes);
 
     int32_t st = OR_OK;
-    for (int32_t i = 0; i < b; ++i) {
+    int32_t accepted = -1;
+    for (int32_t i = 0; i < b && accepted < 0 && st == OR_OK; ++i) {
         const int32_t x = cand[i];
-        if (x < 0 || (int64_t)x >= V) { st = OR_BAD_TOKEN; goto done; }
         const double u = (double)ua[i];
-        if (!(u >= 0.0 && u < 1.0)) { st = OR_BAD_UNIFORM; goto done; }
-        if (!(D[x] > 0.0)) { st = OR_ZERO_DRAFT; goto done; }
-
-        const double ratio = R[x] / D[x];
+        st = candidate_fault(&w, V, x, u);
+        if (st != OR_OK) break;
+        const double ratio = w.R[x] / w.D[x];
         const double margin = fabs(u - ratio);
         if (margin < res->min_accept_margin) res->min_accept_margin = margin;
         if (margin < OR_FLAG_WINDOW) res->flagged = 1;
         res->n_tests += 1;
-
-        if (u < ratio) {                   /* accept x_i */
-            res->kind = OR_KIND_ACCEPT;
-            res->accepted_index = i;
-            res->token = x;
-            goto done;
-        }
-        if (mode == OR_MODE_SPECINFER) {   /* Eq. (2): K is the draft itself */
-            st = or_residual_update(R, D, V, Rn);
-        } else {                           /* Algorithm 1: K = GetProxy(R, D, x_i) */
-            or_proxy_info info;
-            st = or_get_proxy(R, D, V, x, r, s, K, &info);
-            if (st == OR_OK) st = or_residual_update(R, K, V, Rn);
-        }
-        if (st != OR_OK) goto done;
-        { double* t = R; R = Rn; Rn = t; }
-        if (without_replacement) (void)or_draft_remove(D, V, x);
+        if (u < ratio) accepted = i;
+        else st = reject_candidate(&w, V, x, mode, without_replacement);
     }
 
-    /* All candidates rejected (or none): draw from the current residual. */
-    {
-        const double u = (double)ur;
+    if (st == OR_OK && accepted >= 0) {
+        res->kind = OR_KIND_ACCEPT;
+        res->accepted_index = accepted;
+        res->token = cand[accepted];
+    } else if (st == OR_OK) {
         int32_t tok = -1;
         double margin = 0.0;
-        st = or_invcdf(R, V, u, &tok, &margin);
-        if (st != OR_OK) goto done;
-        res->kind = (b > 0) ? OR_KIND_RESAMPLE : OR_KIND_BONUS;
-        res->token = tok;
-        res->sample_margin = margin;
-        if (margin < OR_FLAG_WINDOW) res->flagged = 1;
-        if (final_R) memcpy(final_R, R, bytes);
+        st = or_invcdf(w.R, V, (double)ur, &tok, &margin);
+        if (st == OR_OK) {
+            res->kind = (b > 0) ? OR_KIND_RESAMPLE : OR_KIND_BONUS;
+            res->token = tok;
+            res->sample_margin = margin;
+            if (margin < OR_FLAG_WINDOW) res->flagged = 1;
+            if (final_R) memcpy(final_R, w.R, bytes);
+        }
     }
-
-done:
     res->status = st;
     if (st != OR_OK) {
         res->kind = OR_KIND_FAULT;
         res->accepted_index = -1;
         res->token = -1;
     }
-    free(R); free(D); free(Rn); free(r); free(s); free(K);
+    node_rows_free(&w);
+    return OR_OK;
+}
+
+/* Whether a claimed outcome of one node is admissible: every decision the claim implies
+ * must be the oracle's own, except that a decision inside the flag window may go either
+ * way.  The claim fixes the path through the node: candidates before claim_index are
+ * rejected and claim_index is accepted, or (claim_index < 0) every candidate is
+ * rejected and claim_token is drawn.  An accept test is within the window when
+ * |u - ratio| < OR_FLAG_WINDOW; a draw may return any token j with R_j > 0 whose
+ * interval [C_{j-1}, C_j) of the cumulative residual comes within
+ * OR_FLAG_WINDOW * sum(R) of u * sum(R).  *verdict: 1 if every decision agrees outside
+ * the window, 2 if the claim is admissible only through decisions inside it, 0 if it is
+ * not admissible (a fault on the claimed path included). */
+int32_t or_check_node_outcome(const double* p, const double* q, int64_t V,
+                              const int32_t* cand, const float* ua, int32_t b, float ur,
+                              int32_t mode, int32_t without_replacement,
+                              int32_t claim_index, int32_t claim_token, int32_t* verdict) {
+    if (!p || !verdict || V <= 0 || b < 0 || claim_index >= b) return OR_BAD_ARG;
+    if (b > 0 && (!q || !cand || !ua)) return OR_BAD_ARG;
+    if (mode != OR_MODE_RESISPEC && mode != OR_MODE_SPECINFER) return OR_BAD_ARG;
+    *verdict = 0;
+    node_rows w;
+    if (!node_rows_alloc(&w, V)) {
+        node_rows_free(&w);
+        return OR_BAD_ARG;
+    }
+    const size_t bytes = (size_t)V * sizeof(double);
+    memcpy(w.R, p, bytes);
+    if (b > 0) memcpy(w.D, q, bytes);
+
+    int windowed = 0, ok = 1;
+    const int32_t tested = (claim_index >= 0) ? claim_index + 1 : b;
+    for (int32_t i = 0; i < tested && ok; ++i) {
+        const int32_t x = cand[i];
+        const double u = (double)ua[i];
+        if (candidate_fault(&w, V, x, u) != OR_OK) { ok = 0; break; }
+        const double ratio = w.R[x] / w.D[x];
+        const int accept_claimed = (i == claim_index);
+        const int accept_oracle = u < ratio;
+        if (accept_claimed != accept_oracle) {
+            if (fabs(u - ratio) < OR_FLAG_WINDOW) windowed = 1;
+            else ok = 0;
+        }
+        if (ok && !accept_claimed && reject_candidate(&w, V, x, mode, without_replacement) != OR_OK)
+            ok = 0;
+    }
+    if (ok && claim_index >= 0) {
+        ok = (cand[claim_index] == claim_token);
+    } else if (ok) {
+        const double u = (double)ur;
+        double total = 0.0;
+        for (int64_t j = 0; j < V; ++j) total += w.R[j];
+        if (!(u >= 0.0 && u < 1.0) || !(total > 0.0) || claim_token < 0 || (int64_t)claim_token >= V) {
+            ok = 0;
+        } else {
+            int32_t tok = -1;
+            double margin = 0.0;
+            (void)or_invcdf(w.R, V, u, &tok, &margin);
+            if (tok != claim_token) {
+                double before = 0.0;
+                for (int64_t j = 0; j < claim_token; ++j) before += w.R[j];
+                const double after = before + w.R[claim_token];
+                const double t = u * total, win = OR_FLAG_WINDOW * total;
+                if (before <= t + win && after > t - win) windowed = 1;
+                else ok = 0;
+            }
+        }
+    }
+    *verdict = ok ? (windowed ? 2 : 1) : 0;
+    node_rows_free(&w);
     return OR_OK;
 }
 
@@ -495,6 +596,67 @@ int32_t or_verify_tree_nodes(const void* target, const void* draft, int32_t dtyp
     return rc;
 }
 
+/* Claimed outcomes of selected nodes (rows[i] = b * N + n), checked one by one with
+ * or_check_node_outcome.  A claim is (child, token, status) as the node outcome arrays
+ * of a verification hold them.  A claimed fault is admissible only when the oracle's
+ * own evaluation of the node ends in the same fault; a claimed child must be a child of
+ * the node (its position among the children in ascending index is the claimed
+ * candidate).  out_verdict[i]: 1, 2 or 0 as for one node. */
+int32_t or_check_tree_nodes(const void* target, const void* draft, int32_t dtype,
+                            const int32_t* node_token, const int32_t* parent,
+                            const float* u_accept, const float* u_resample,
+                            int32_t B, int32_t N, int64_t V, float temperature,
+                            int32_t mode, int32_t without_replacement, int32_t bonus,
+                            const int64_t* rows, int64_t n_rows, const int32_t* claim_child,
+                            const int32_t* claim_token, const int32_t* claim_status,
+                            int32_t* out_verdict) {
+    if (!target || !draft || !node_token || !parent || !u_accept || !u_resample || !rows) return OR_BAD_ARG;
+    if (!claim_child || !claim_token || !claim_status || !out_verdict) return OR_BAD_ARG;
+    if (B < 0 || N <= 0 || V <= 0 || n_rows < 0) return OR_BAD_ARG;
+    double* p = (double*)malloc((size_t)V * sizeof(double));
+    double* q = (double*)malloc((size_t)V * sizeof(double));
+    int32_t* kids = (int32_t*)malloc((size_t)N * sizeof(int32_t));
+    int32_t* cand = (int32_t*)malloc((size_t)N * sizeof(int32_t));
+    float* ua = (float*)malloc((size_t)N * sizeof(float));
+    if (!p || !q || !kids || !cand || !ua) {
+        free(p); free(q); free(kids); free(cand); free(ua);
+        return OR_BAD_ARG;
+    }
+    int32_t rc = OR_OK;
+    for (int64_t i = 0; i < n_rows; ++i) {
+        const int64_t row = rows[i];
+        if (row < 0 || row >= (int64_t)B * N) { rc = OR_BAD_ARG; break; }
+        const int32_t b = (int32_t)(row / N), n = (int32_t)(row % N);
+        or_node_result res;
+        int32_t child = -1;
+        rc = eval_node(target, draft, dtype, node_token, parent, u_accept, u_resample, b, N, V,
+                       temperature, mode, without_replacement, bonus, n, kids, p, q, cand, ua,
+                       &res, &child, NULL);
+        if (rc != OR_OK) break;
+        int32_t verdict = 0;
+        if (claim_status[i] != OR_OK || res.status != OR_OK) {
+            /* faults are not decisions: the claim must name the oracle's own fault */
+            verdict = (claim_status[i] == res.status && claim_child[i] == -1 && claim_token[i] == -1) ? 1 : 0;
+        } else if (res.kind == OR_KIND_NONE) {
+            verdict = (claim_child[i] == -1 && claim_token[i] == -1) ? 1 : 0;
+        } else {
+            const int32_t nk = children_of(parent + (int64_t)b * N, N, n, kids);
+            int32_t idx = -1, known = (claim_child[i] == -1);
+            for (int32_t c = 0; c < nk; ++c)
+                if (kids[c] == claim_child[i]) { idx = c; known = 1; }
+            if (known) {
+                rc = or_check_node_outcome(p, nk > 0 ? q : NULL, V, cand, ua, nk,
+                                           u_resample[row], mode, without_replacement, idx,
+                                           claim_token[i], &verdict);
+                if (rc != OR_OK) break;
+            }
+        }
+        out_verdict[i] = verdict;
+    }
+    free(p); free(q); free(kids); free(cand); free(ua);
+    return rc;
+}
+
 /* ------------------------------------------------------------------------------------
  * The draft step: Philox4x32-10 uniforms and candidate draws.
  * ---------------------------------------------------------------------------------- */
@@ -559,6 +721,43 @@ int32_t or_sample_candidates(const void* draft, int32_t dtype, int64_t V, float 
     }
     free(D);
     return st;
+}
+
+/* Whether claimed draws of k candidates from D = softmax(draft / T) are admissible: draw
+ * i, from the draft left by the claimed draws before it (without replacement), must be
+ * the inverse-CDF draw of uc[i], or a token whose interval [C_{j-1}, C_j) comes within
+ * OR_FLAG_WINDOW * sum(D) of uc[i] * sum(D).  *verdict: 1 every draw exact, 2 admissible
+ * only through a windowed draw, 0 not admissible. */
+int32_t or_check_candidates(const void* draft, int32_t dtype, int64_t V, float temperature,
+                            int32_t k, int32_t without_replacement, const float* uc,
+                            const int32_t* claimed, int32_t* verdict) {
+    if (!draft || !verdict || V <= 0 || k < 0 || (k > 0 && (!uc || !claimed))) return OR_BAD_ARG;
+    *verdict = 0;
+    double* D = (double*)malloc((size_t)V * sizeof(double));
+    if (!D) return OR_BAD_ARG;
+    int ok = (or_softmax(draft, dtype, V, temperature, D) == OR_OK);
+    int windowed = 0;
+    for (int32_t i = 0; i < k && ok; ++i) {
+        const int32_t c = claimed[i];
+        int32_t tok = -1;
+        double margin = 0.0;
+        if (c < 0 || (int64_t)c >= V || or_invcdf(D, V, (double)uc[i], &tok, &margin) != OR_OK) {
+            ok = 0;
+            break;
+        }
+        if (tok != c) {
+            double total = 0.0, before = 0.0;
+            for (int64_t j = 0; j < V; ++j) total += D[j];
+            for (int64_t j = 0; j < c; ++j) before += D[j];
+            const double t = (double)uc[i] * total, win = OR_FLAG_WINDOW * total;
+            if (before <= t + win && before + D[c] > t - win) windowed = 1;
+            else ok = 0;
+        }
+        if (ok && without_replacement && i + 1 < k && or_draft_remove(D, V, c) != OR_OK) ok = 0;
+    }
+    *verdict = ok ? (windowed ? 2 : 1) : 0;
+    free(D);
+    return OR_OK;
 }
 
 int32_t or_draft_tree(const void* draft, int32_t dtype, const int32_t* parent, int32_t B,

@@ -74,8 +74,9 @@ typedef struct {
 /* softmax((l - max l) / T) in fp64.  Returns OR_OK, OR_UNDERFLOW (all -inf) or OR_BAD_ARG. */
 int32_t or_softmax(const void* logits, int32_t dtype, int64_t V, float temperature, double* out);
 
-/* GetProxy(R, D, x0) of Algorithm 1, literally: writes r (reserved mass), s (slack),
- * K (proxy).  Requires D[x0] > R[x0].  Returns OR_OK or OR_BAD_ARG. */
+/* The proxy K = R - r + s of Definition 1 after the rejection of x0 (Algorithm 1's
+ * GetProxy, applied to the current residual R and draft D): writes r (reserved mass),
+ * s (slack) and K.  Requires D[x0] > R[x0].  Returns OR_OK or OR_BAD_ARG. */
 int32_t or_get_proxy(const double* R, const double* D, int64_t V, int64_t x0,
                      double* r, double* s, double* K, or_proxy_info* info);
 
@@ -97,6 +98,16 @@ int32_t or_verify_node(const double* p, const double* q, int64_t V,
                        const int32_t* cand, const float* ua, int32_t b, float ur,
                        int32_t mode, int32_t without_replacement,
                        or_node_result* res, double* final_R);
+
+/* Whether a claimed outcome of one node (claim_index >= 0: that candidate accepted and
+ * claim_token its id; claim_index < 0: every candidate rejected and claim_token drawn)
+ * is admissible when decisions inside the flag window may go either way.
+ * *verdict: 1 every decision agrees outside the window, 2 admissible only through
+ * decisions inside it, 0 not admissible. */
+int32_t or_check_node_outcome(const double* p, const double* q, int64_t V,
+                              const int32_t* cand, const float* ua, int32_t b, float ur,
+                              int32_t mode, int32_t without_replacement,
+                              int32_t claim_index, int32_t claim_token, int32_t* verdict);
 
 /* Same node, many independent trials (statistics tests): cand[n][b], ua[n][b], ur[n]. */
 int32_t or_verify_node_batch(const double* p, const double* q, int64_t V,
@@ -138,6 +149,18 @@ int32_t or_verify_tree_nodes(const void* target, const void* draft, int32_t dtyp
                              int32_t* out_flagged, double* out_margin /* n_rows or NULL */,
                              double* out_final_R /* n_rows*V or NULL */);
 
+/* Claimed (child, token, status) outcomes of selected nodes checked against the
+ * oracle with or_check_node_outcome; out_verdict[n_rows] as there.  A claimed fault
+ * must be the oracle's own fault of that node. */
+int32_t or_check_tree_nodes(const void* target, const void* draft, int32_t dtype,
+                            const int32_t* node_token, const int32_t* parent,
+                            const float* u_accept, const float* u_resample,
+                            int32_t B, int32_t N, int64_t V, float temperature,
+                            int32_t mode, int32_t without_replacement, int32_t bonus,
+                            const int64_t* rows, int64_t n_rows, const int32_t* claim_child,
+                            const int32_t* claim_token, const int32_t* claim_status,
+                            int32_t* out_verdict);
+
 /* ---- the draft step: uniforms and candidate draws (run before verification) ---- */
 
 /* Philox4x32-10 (Salmon, Moraes, Dror and Shaw, "Parallel random numbers: as easy as
@@ -162,6 +185,15 @@ void or_node_uniforms(uint64_t seed, uint64_t offset, int32_t b, int32_t n, floa
 int32_t or_sample_candidates(const void* draft, int32_t dtype, int64_t V, float temperature,
                              int32_t k, int32_t without_replacement, const float* uc,
                              int32_t* tokens, double* margins);
+
+/* Whether claimed draws claimed[k] of k candidates are admissible draws of
+ * or_sample_candidates with uniforms uc[k]: each draw (from the draft left by the
+ * claimed draws before it, without replacement) exact, or within the flag window of its
+ * inverse-CDF boundary.  *verdict: 1 all exact, 2 admissible through a windowed draw,
+ * 0 not admissible. */
+int32_t or_check_candidates(const void* draft, int32_t dtype, int64_t V, float temperature,
+                            int32_t k, int32_t without_replacement, const float* uc,
+                            const int32_t* claimed, int32_t* verdict);
 
 /* The draft step of a tree batch: for every node with children, its children's
  * tokens drawn from its draft row (children in ascending node index), and every

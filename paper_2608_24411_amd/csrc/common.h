@@ -16,21 +16,13 @@
 namespace {
 
 
-#ifndef RS_BLOCK
-#define RS_BLOCK 512
-#endif
-constexpr int kBlock = RS_BLOCK;          // threads per row workgroup (all-nodes schedule)
+constexpr int kBlock = 512;              // threads per row workgroup (all-nodes schedule)
 constexpr int kMaxWaves = 16;            // waves per workgroup at most
 constexpr int kMaxCand = RS_MAX_CANDIDATES;
-#ifndef RS_MAX_SLOTS
-#define RS_MAX_SLOTS 128
-#endif
-#ifndef RS_UNR16
-#define RS_UNR16 2
-#endif
-#ifndef RS_UNR32
-#define RS_UNR32 2
-#endif
+// 128-bit loads per lane and row in one chunk: bf16 rows (8 elements a load), fp32 rows
+// (4 elements a load)
+constexpr int kUnr16 = 2;
+constexpr int kUnr32 = 2;
 // Load policy.  Data whose last full use is the current pass is read with nontemporal
 // loads (about 12% more streaming bandwidth on gfx950): pass 1 of rows without
 // children and every rejection pass.  Pass 1 of a row with children uses ordinary loads,
@@ -39,7 +31,7 @@ constexpr int kMaxCand = RS_MAX_CANDIDATES;
 constexpr bool kNtPass1 = false;
 constexpr bool kNtRej = true;
 constexpr bool kNtLeaf = true;
-constexpr int kMaxSlots = RS_MAX_SLOTS;   // per-row slots (runs of chunks) with partial sums
+constexpr int kMaxSlots = 128;           // per-row slots (runs of chunks) with partial sums
 // A row's exponent reference is fixed before pass 1; sums outside [2^-kLow, inf) send the
 // row through an exact-maximum pass and a second pass 1.
 constexpr double kLowSum = 1.0 / 1048576.0;

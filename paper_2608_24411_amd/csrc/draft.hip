@@ -460,9 +460,9 @@ rs_status resispec_draft_candidates(const void* draft_logits, const int32_t* par
     const hipStream_t s = (hipStream_t)stream;
     hipError_t e;
     if (prm->logits_dtype == RS_BF16)
-        e = vec ? launch_draft_t<uint16_t, 8, RS_UNR16>(P, s) : launch_draft_t<uint16_t, 1, 4>(P, s);
+        e = vec ? launch_draft_t<uint16_t, 8, kUnr16>(P, s) : launch_draft_t<uint16_t, 1, 4>(P, s);
     else
-        e = vec ? launch_draft_t<float, 4, RS_UNR32>(P, s) : launch_draft_t<float, 1, 4>(P, s);
+        e = vec ? launch_draft_t<float, 4, kUnr32>(P, s) : launch_draft_t<float, 1, 4>(P, s);
     return e == hipSuccess ? RS_OK : RS_ERR_HIP;
 }
 

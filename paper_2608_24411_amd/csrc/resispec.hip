@@ -81,18 +81,6 @@ struct KParams {
     int32_t nslots;      // slots per row
 };
 
-#ifdef RS_TIMING
-// Phase timestamps (s_memrealtime, 100 MHz) per row, for profiling builds only.
-__device__ long long* g_timing = nullptr;
-#define RS_STAMP(row, k)                                                               \
-    do {                                                                               \
-        if (threadIdx.x == 0 && g_timing) g_timing[(row) * 16 + (k)] = wall_clock64(); \
-    } while (0)
-#else
-#define RS_STAMP(row, k) \
-    do {                 \
-    } while (0)
-#endif
 
 __device__ __forceinline__ void write_outcome(const KParams& P, int64_t row, int32_t child,
                                               int32_t tok, int32_t status) {
@@ -336,7 +324,6 @@ __device__ __forceinline__ void verify_row(const KParams& P, Smem& sm, const int
     const In* __restrict__ tg = reinterpret_cast<const In*>(P.tgt) + row * V;
     const In* __restrict__ dg = reinterpret_cast<const In*>(P.dft) + row * V;
 
-    RS_STAMP(row, 0);
     using W = Vec<In, VEC>;
     // This wave's first target chunk is requested before anything else, so its latency
     // overlaps the row description below (the first slot of wave w is slot s0 + w).
@@ -478,7 +465,6 @@ __device__ __forceinline__ void verify_row(const KParams& P, Smem& sm, const int
         hld = widen(dg[hx]);
     }
 
-    RS_STAMP(row, 1);
     const bool internal = nc > 0;
     const float c2h = P.c2h, c2l = P.c2l;
 
@@ -543,10 +529,6 @@ __device__ __forceinline__ void verify_row(const KParams& P, Smem& sm, const int
                 flush);
         }
         if (attempt == 0) {
-            RS_STAMP(row, 2);
-#ifdef RS_TIMING
-            if (lane == 0 && wid < 8 && g_timing) g_timing[row * 16 + 8 + wid] = wall_clock64();   // per-wave end (waves 0-7)
-#endif
         }
         __syncthreads();
         if (!pass_totals<BLK, SPLIT>(sm, grp, nslots, s0, nl, internal, true)) {
@@ -652,7 +634,6 @@ __device__ __forceinline__ void verify_row(const KParams& P, Smem& sm, const int
     __syncthreads();
 
     const bool worep = P.worep != 0;
-    RS_STAMP(row, 3);
 
     // ---- sequential accept / reject
     int i = 0;
@@ -887,10 +868,6 @@ __device__ __forceinline__ void verify_row(const KParams& P, Smem& sm, const int
         if (sm.decision == -2) break;
     }
 
-    RS_STAMP(row, 4);
-#ifdef RS_TIMING
-    if (threadIdx.x == 0 && g_timing) g_timing[row * 16 + 7] = i;   // rejection passes
-#endif
     if (sm.decision == -2) {
         if (tid == 0) emit(-1, -1, sm.status);
         zero_residual_row(P, row);
@@ -1076,14 +1053,12 @@ __device__ __forceinline__ void verify_row(const KParams& P, Smem& sm, const int
         }
     }
     __syncthreads();
-    RS_STAMP(row, 5);
     const int32_t tok = sm.token;
     if (tid == 0) {
         if (sm.status != RS_SEQ_OK) emit(-1, -1, sm.status);
         else if (tok < 0) emit(-1, -1, RS_SEQ_UNDERFLOW);
         else emit(-1, tok, RS_SEQ_OK);
     }
-    RS_STAMP(row, 6);
 
     // debug: the normalised distribution of the draw
     if (P.residual_out) {
@@ -1529,9 +1504,9 @@ template <int MODE>
 hipError_t launch_rowgroups_m(const KParams& P, int dtype, bool vec, int64_t nrows, RowGroupLaunch* rg,
                               hipStream_t s) {
     if (dtype == RS_BF16)
-        return vec ? launch_rowgroups<uint16_t, 8, RS_UNR16, MODE>(P, nrows, rg, s)
+        return vec ? launch_rowgroups<uint16_t, 8, kUnr16, MODE>(P, nrows, rg, s)
                    : launch_rowgroups<uint16_t, 1, 4, MODE>(P, nrows, rg, s);
-    return vec ? launch_rowgroups<float, 4, RS_UNR32, MODE>(P, nrows, rg, s)
+    return vec ? launch_rowgroups<float, 4, kUnr32, MODE>(P, nrows, rg, s)
                : launch_rowgroups<float, 1, 4, MODE>(P, nrows, rg, s);
 }
 
@@ -1540,16 +1515,16 @@ hipError_t launch_rows_m(const KParams& P, int dtype, bool vec, int64_t nrows, P
                          hipStream_t s) {
     if (path) {
         if (dtype == RS_BF16)
-            return vec ? launch_path_kernel<uint16_t, 8, RS_UNR16, MODE>(P, path, s)
+            return vec ? launch_path_kernel<uint16_t, 8, kUnr16, MODE>(P, path, s)
                        : launch_path_kernel<uint16_t, 1, 4, MODE>(P, path, s);
-        return vec ? launch_path_kernel<float, 4, RS_UNR32, MODE>(P, path, s)
+        return vec ? launch_path_kernel<float, 4, kUnr32, MODE>(P, path, s)
                    : launch_path_kernel<float, 1, 4, MODE>(P, path, s);
     }
     if (dtype == RS_BF16) {
-        return vec ? launch_row_kernel<uint16_t, 8, RS_UNR16, MODE>(P, nrows, s)
+        return vec ? launch_row_kernel<uint16_t, 8, kUnr16, MODE>(P, nrows, s)
                    : launch_row_kernel<uint16_t, 1, 4, MODE>(P, nrows, s);
     }
-    return vec ? launch_row_kernel<float, 4, RS_UNR32, MODE>(P, nrows, s)
+    return vec ? launch_row_kernel<float, 4, kUnr32, MODE>(P, nrows, s)
                : launch_row_kernel<float, 1, 4, MODE>(P, nrows, s);
 }
 hipError_t launch_rows(const KParams& P, const rs_params* prm, bool vec, int64_t nrows, hipStream_t s,
@@ -1650,11 +1625,6 @@ rs_status check_tree_args(const void* target_logits, const void* draft_logits,
 
 extern "C" {
 
-#ifdef RS_TIMING
-int32_t resispec_debug_set_timing(void* dev_ptr) {
-    return hipMemcpyToSymbol(HIP_SYMBOL(g_timing), &dev_ptr, sizeof(dev_ptr)) == hipSuccess ? 0 : 1;
-}
-#endif
 
 int32_t resispec_abi_version(void) { return RESISPEC_ABI_VERSION; }
 

@@ -21,6 +21,33 @@ def _log(*a):
 
 # ------------------------------------------------------------------ flat ----
 
+def _flat_check(w, tok, length, st, mode):
+    """Every flat row against the oracle: exact outside the flag window, admissible inside
+    it.  Returns (exact, flagged)."""
+    t, d = synth.to_host(w["target"]), synth.to_host(w["draft"])
+    cand, ua, ur = (synth.to_host(w[k]) for k in ("cand_ids", "u_accept", "u_resample"))
+    tok, length, st = tok.cpu().numpy(), length.cpu().numpy(), st.cpu().numpy()
+    n_flag = 0
+    for b in range(w["B"]):
+        p = O.softmax(t[b], w["temperature"])
+        q = O.softmax(d[b], w["temperature"])
+        r = O.verify_node(p, q, cand[b], ua[b], ur[b], mode)
+        same = (st[b] == STATUS_MAP[r["status"]] and tok[b] == (r["token"] if r["status"] == O.OK else -1)
+                and length[b] == (1 if r["kind"] == O.KIND_ACCEPT else (0 if r["status"] == O.OK else -1)))
+        if not r["flagged"]:
+            assert same, (b, tok[b], length[b], st[b], r)
+            continue
+        n_flag += 1
+        if same:
+            continue
+        # the accepted candidate is the first one carrying the returned token (a rejected
+        # token has no residual mass left, so a later copy of it is rejected too)
+        assert st[b] == 0, (b, st[b], r)
+        idx = int(np.flatnonzero(cand[b] == tok[b])[0]) if length[b] == 1 else -1
+        assert O.check_node_outcome(p, q, cand[b], ua[b], ur[b], idx, int(tok[b]), mode) != 0, (b, r)
+    return w["B"] - n_flag, n_flag
+
+
 @pytest.mark.parametrize("mode", MODES)
 def test_flat_config0_full(gpu_lib, mode):
     """8 rows, V = 32000 fp32, k = 4 i.i.d. candidates: every row against the oracle."""
@@ -29,20 +56,8 @@ def test_flat_config0_full(gpu_lib, mode):
                                               w["u_accept"], w["u_resample"],
                                               temperature=w["temperature"], mode=mode)
     torch.cuda.synchronize()
-    t, d = synth.to_host(w["target"]), synth.to_host(w["draft"])
-    cand, ua, ur = (synth.to_host(w[k]) for k in ("cand_ids", "u_accept", "u_resample"))
-    n_flag = 0
-    for b in range(w["B"]):
-        p = O.softmax(t[b], w["temperature"])
-        q = O.softmax(d[b], w["temperature"])
-        r = O.verify_node(p, q, cand[b], ua[b], ur[b], mode)
-        if r["flagged"]:
-            n_flag += 1
-            continue
-        assert st[b].item() == 0
-        assert tok[b].item() == r["token"], (b, tok[b].item(), r)
-        assert length[b].item() == (1 if r["kind"] == O.KIND_ACCEPT else 0)
-    assert n_flag <= 1
+    n_exact, n_flag = _flat_check(w, tok, length, st, mode)
+    _log("flat config 0", mode, "exact", n_exact, "flagged", n_flag)
 
 
 @pytest.mark.parametrize("V,dtype", [(32003, "f32"), (50001, "bf16"), (7, "f32"), (1, "bf16")])
@@ -54,15 +69,7 @@ def test_flat_ragged_vocab(gpu_lib, V, dtype):
                                                   w["u_accept"], w["u_resample"],
                                                   temperature=w["temperature"], mode=mode)
         torch.cuda.synchronize()
-        t, d = synth.to_host(w["target"]), synth.to_host(w["draft"])
-        cand, ua, ur = (synth.to_host(w[k]) for k in ("cand_ids", "u_accept", "u_resample"))
-        for b in range(w["B"]):
-            r = O.verify_node(O.softmax(t[b], w["temperature"]), O.softmax(d[b], w["temperature"]),
-                              cand[b], ua[b], ur[b], mode)
-            if r["flagged"]:
-                continue
-            assert st[b].item() == STATUS_MAP[r["status"]]
-            assert tok[b].item() == r["token"], (V, dtype, mode, b)
+        _flat_check(w, tok, length, st, mode)
 
 
 def test_flat_k0_draws_from_target(gpu_lib):
@@ -74,11 +81,16 @@ def test_flat_k0_draws_from_target(gpu_lib):
     torch.cuda.synchronize()
     t = synth.to_host(w["target"])
     ur = synth.to_host(w["u_resample"])
+    empty = np.empty(0, np.int32)
     for b in range(8):
-        ref, margin, _ = O.invcdf(O.softmax(t[b], 1.0), float(ur[b]))
-        if margin < 1e-6:
-            continue
-        assert tok[b].item() == ref and length[b].item() == 0 and st[b].item() == 0
+        p = O.softmax(t[b], 1.0)
+        ref, margin, _ = O.invcdf(p, float(ur[b]))
+        assert length[b].item() == 0 and st[b].item() == 0
+        if margin >= 1e-6:
+            assert tok[b].item() == ref
+        else:
+            assert O.check_node_outcome(p, None, empty, np.empty(0, np.float32), float(ur[b]), -1,
+                                        tok[b].item()) != 0
 
 
 # ------------------------------------------------------------------ trees ---
@@ -105,18 +117,18 @@ def test_tree_parity_reduced(gpu_lib, cfg, over, mode):
     h = host_tree(w)
     gpu = gpu_tree(gpu_lib, w, mode, debug=True, want_residual=True)
     orc = oracle_walk(h, w, mode)
-    n_cmp, n_flag = compare_walk(gpu, orc)
-    assert n_cmp >= w["B"] - 1
+    compare_walk(gpu, orc, h, w, mode)
+    _log("  walks", compare_walk.last)
     B, N = h["parent"].shape
     # residual parity on every node that drew a token (up to 40 rows)
     nt = gpu["node_token"].cpu().numpy().reshape(-1)
     nc = gpu["node_child"].cpu().numpy().reshape(-1)
     drew = np.flatnonzero((nc < 0) & (nt >= 0))[:40]
-    n_cmp, n_flag, _ = compare_nodes(gpu, h, w, mode, residual_rows=drew)
-    _log("  nodes compared", n_cmp, "flagged", n_flag, compare_nodes.last)
-    # flagged decisions are excluded, not hidden: most of them are draws that land on a
-    # token whose own mass is below the window (V = 128k Zipf tails)
-    assert n_cmp >= 0.8 * B * N
+    n_exact, n_flag, _ = compare_nodes(gpu, h, w, mode, residual_rows=drew)
+    _log("  nodes", compare_nodes.last)
+    # flagged decisions are checked for admissibility above; most of them are draws that
+    # land on a token whose own mass is below the window (V = 128k Zipf tails)
+    assert n_flag <= 0.15 * B * N
     # the plain entry point returns the same walk as the debug one
     plain = gpu_tree(gpu_lib, w, mode)
     assert torch.equal(plain["tokens"], gpu["tokens"])
@@ -135,44 +147,72 @@ def test_tree_parity_temperatures(gpu_lib, T, mode):
         w = synth.make_workload(cfg, device="cuda", T=T, **over)
         h = host_tree(w)
         gpu = gpu_tree(gpu_lib, w, mode, debug=True)
-        n_cmp, _ = compare_walk(gpu, oracle_walk(h, w, mode))
-        assert n_cmp >= w["B"] - 1
+        compare_walk(gpu, oracle_walk(h, w, mode), h, w, mode)
         B, N = h["parent"].shape
-        n_cmp, n_flag, _ = compare_nodes(gpu, h, w, mode)
-        _log("  nodes compared", n_cmp, "flagged", n_flag)
-        assert n_cmp >= 0.8 * B * N
+        n_exact, n_flag, _ = compare_nodes(gpu, h, w, mode)
+        _log("  nodes", compare_nodes.last)
+        assert n_flag <= 0.15 * B * N
 
 
-@pytest.mark.parametrize("cfg,nsample", [(1, 64), (2, 6), (3, 4), (4, 4)])
-def test_tree_parity_full_size_sampled(gpu_lib, cfg, nsample):
-    """Full configurations in the launch shape the benchmark times; the oracle checks a
-    seeded sample of sequences (all of them for the 32000-vocabulary chain)."""
-    _log("full-size parity", cfg)
-    w = synth.make_workload(cfg, device="cuda")
-    rng = np.random.default_rng(100 + cfg)
-    seqs = np.sort(rng.choice(w["B"], size=min(nsample, w["B"]), replace=False))
-    h = host_tree(w, seqs)
-    for mode in MODES:
-        gpu = gpu_tree(gpu_lib, w, mode, debug=True)
-        orc = oracle_walk(h, w, mode)
-        compare_walk(gpu, orc, seqs)
-        compare_nodes(gpu, h, w, mode, seqs=seqs)
-        plain = gpu_tree(gpu_lib, w, mode)
-        assert torch.equal(plain["tokens"], gpu["tokens"])
-        # property at any size: accepted tokens are the tokens of a root path
-        toks = plain["tokens"].cpu().numpy()
-        lens = plain["accepted_len"].cpu().numpy()
-        par = w["parent"].cpu().numpy()
-        ntok = w["node_token"].cpu().numpy()
-        assert (plain["status"].cpu().numpy() == 0).all()
-        for b in range(0, w["B"], max(1, w["B"] // 64)):
-            n = 0
-            for i in range(lens[b]):
-                kids = np.flatnonzero(par[b] == n)
-                match = [c for c in kids if ntok[b, c] == toks[b, i]]
-                assert match, (b, i)
-                n = match[0]
-            assert toks[b, lens[b]] >= 0 and (toks[b, lens[b] + 1:] == -1).all()
+_FULL = {}
+
+
+@pytest.fixture(scope="module", autouse=True)
+def _release_full_workloads():
+    yield
+    _FULL.clear()
+    torch.cuda.empty_cache()
+
+
+def _full_workload(cfg):
+    """One full-size workload per configuration, with its host copy (the 1024 x 26
+    serving batch is 8.1 GB per logits tensor on both sides)."""
+    if cfg not in _FULL:
+        _FULL.clear()
+        torch.cuda.empty_cache()
+        w = synth.make_workload(cfg, device="cuda")
+        _FULL[cfg] = (w, host_tree(w))
+    return _FULL[cfg]
+
+
+@pytest.mark.parametrize("mode", MODES)
+@pytest.mark.parametrize("cfg", [1, 2, 3, 4])
+def test_tree_parity_full_size_walk(gpu_lib, cfg, mode):
+    """Full configurations in the launch shape the benchmark times: the walk of every
+    sequence against the oracle's sequential walk (exact outside the window, admissible
+    inside it), for the all-nodes step and for the path-only schedule."""
+    _log("full-size walk parity", cfg, mode)
+    w, h = _full_workload(cfg)
+    plain = gpu_tree(gpu_lib, w, mode)
+    orc = oracle_walk(h, w, mode)
+    compare_walk(plain, orc, h, w, mode)
+    _log("  all-nodes step", compare_walk.last)
+    assert compare_walk.last["compared"] == w["B"]
+    assert (plain["status"].cpu().numpy() == 0).all()
+    pt, pl, ps = gpu_lib.resispec_verify_tree_path(
+        w["target"], w["draft"], w["node_token"], w["parent"], w["u_accept"], w["u_resample"],
+        temperature=w["temperature"], max_depth=w["max_depth"], mode=mode,
+        without_replacement=w["without_replacement"])
+    torch.cuda.synchronize()
+    assert torch.equal(pt, plain["tokens"]) and torch.equal(pl, plain["accepted_len"])
+    assert torch.equal(ps, plain["status"])
+
+
+@pytest.mark.parametrize("mode", MODES)
+@pytest.mark.parametrize("cfg", [2, 3, 4])
+def test_tree_parity_full_size_nodes(gpu_lib, cfg, mode):
+    """Full configurations: every node row's own outcome (the all-nodes step verifies all
+    of them) against the oracle's evaluation of that node."""
+    _log("full-size node parity", cfg, mode)
+    w, h = _full_workload(cfg)
+    gpu = gpu_tree(gpu_lib, w, mode, debug=True)
+    compare_nodes(gpu, h, w, mode)
+    _log("  nodes", compare_nodes.last)
+    B, N = h["parent"].shape
+    assert compare_nodes.last["compared"] == B * N
+    assert compare_nodes.last["flagged"] <= 0.15 * B * N
+    plain = gpu_tree(gpu_lib, w, mode)
+    assert torch.equal(plain["tokens"], gpu["tokens"])
 
 
 def test_tree_edges(gpu_lib):
@@ -188,12 +228,12 @@ def test_tree_edges(gpu_lib):
         for bonus in (True, False):
             gpu = gpu_tree(gpu_lib, w, mode, debug=True, bonus=bonus)
             orc = oracle_walk(h, w, mode, bonus=bonus)
-            compare_walk(gpu, orc)
+            compare_walk(gpu, orc, h, w, mode, bonus=bonus)
             compare_nodes(gpu, h, w, mode, bonus=bonus)
         st = gpu_tree(gpu_lib, w, mode)["status"].cpu().numpy()
         assert st[4] == 4
         short = gpu_tree(gpu_lib, w, mode, max_depth=1)
-        compare_walk(short, oracle_walk(h, w, mode, max_depth=1))
+        compare_walk(short, oracle_walk(h, w, mode, max_depth=1), h, w, mode)
     # root only
     w1 = synth.make_workload(1, device="cuda", B=5, V=777)
     for k in ("target", "draft", "node_token", "parent", "u_accept", "u_resample"):
@@ -201,7 +241,7 @@ def test_tree_edges(gpu_lib):
     w1["max_depth"] = 0
     h1 = host_tree(w1)
     gpu = gpu_tree(gpu_lib, w1, "resispec", debug=True)
-    compare_walk(gpu, oracle_walk(h1, w1, "resispec"))
+    compare_walk(gpu, oracle_walk(h1, w1, "resispec"), h1, w1, "resispec")
     assert (gpu["accepted_len"].cpu() == 0).all()
     # empty batch
     e = {k: (v[:0] if isinstance(v, torch.Tensor) else v) for k, v in w.items()}
@@ -232,7 +272,7 @@ def test_masked_logits(gpu_lib, cfg, over):
     h = host_tree(w)
     for mode in MODES:
         gpu = gpu_tree(gpu_lib, w, mode, debug=True)
-        compare_walk(gpu, oracle_walk(h, w, mode))
+        compare_walk(gpu, oracle_walk(h, w, mode), h, w, mode)
         compare_nodes(gpu, h, w, mode)
         assert (gpu["status"].cpu().numpy() == 0).all()
 
@@ -248,14 +288,14 @@ def test_reference_fallback(gpu_lib):
     h = host_tree(w)
     for mode in MODES:
         gpu = gpu_tree(gpu_lib, w, mode, debug=True)
-        compare_walk(gpu, oracle_walk(h, w, mode))
+        compare_walk(gpu, oracle_walk(h, w, mode), h, w, mode)
         compare_nodes(gpu, h, w, mode)
     ws = dict(w)
     ws["draft"] = (w["draft"].float() - 60.0).to(w["draft"].dtype)
     hs = host_tree(ws)
     for mode in MODES:
         a = gpu_tree(gpu_lib, ws, mode, debug=True)
-        compare_walk(a, oracle_walk(hs, ws, mode))
+        compare_walk(a, oracle_walk(hs, ws, mode), hs, ws, mode)
         compare_nodes(a, hs, ws, mode)
 
 
@@ -279,7 +319,8 @@ def test_max_children(gpu_lib):
             if expect_status:
                 assert (gpu["status"].cpu().numpy() == expect_status).all()
             else:
-                compare_walk(gpu, oracle_walk(host_tree(w), w, mode))
+                h = host_tree(w)
+                compare_walk(gpu, oracle_walk(h, w, mode), h, w, mode)
 
 
 @pytest.mark.parametrize("worep", [False, True])
@@ -318,11 +359,11 @@ def test_long_rejection_chains(gpu_lib, worep, V, dtype):
     for mode in MODES:
         _log("long chains", V, dtype, "worep", worep, mode)
         gpu = gpu_tree(gpu_lib, w, mode, debug=True, want_residual=True)
-        compare_walk(gpu, oracle_walk(h, w, mode))
+        compare_walk(gpu, oracle_walk(h, w, mode), h, w, mode)
         drew = [r for r in range(B * N) if gpu["node_child"].reshape(-1)[r].item() < 0]
-        n_cmp, n_flag, orc = compare_nodes(gpu, h, w, mode, residual_rows=drew)
-        _log("  nodes compared", n_cmp, "flagged", n_flag, compare_nodes.last)
-        assert n_cmp >= 0.8 * B * N
+        n_exact, n_flag, orc = compare_nodes(gpu, h, w, mode, residual_rows=drew)
+        _log("  nodes", compare_nodes.last)
+        assert n_flag <= 0.15 * B * N
         # the chains are long: internal nodes reject candidates before they accept (the
         # proxy-shaped residual accepts within two or three), and with the standard
         # residual most of them reject every candidate and draw
@@ -373,7 +414,7 @@ def test_max_vocab(gpu_lib):
     h = host_tree(w)
     for mode in MODES:
         gpu = gpu_tree(gpu_lib, w, mode, debug=True)
-        compare_walk(gpu, oracle_walk(h, w, mode))
+        compare_walk(gpu, oracle_walk(h, w, mode), h, w, mode)
         compare_nodes(gpu, h, w, mode)
         t2, l2, s2 = gpu_lib.resispec_verify_tree_path(
             t, d, tok, par, ua, ur, temperature=1.0, max_depth=2, mode=mode)

@@ -52,7 +52,8 @@ def test_path_equals_all_nodes_and_oracle(gpu_lib, cfg, over, mode):
     w = synth.make_workload(cfg, device="cuda", **over)
     p = path_tree(gpu_lib, w, mode)
     same(p, gpu_tree(gpu_lib, w, mode))
-    compare_walk(p, oracle_walk(host_tree(w), w, mode))
+    h = host_tree(w)
+    compare_walk(p, oracle_walk(h, w, mode), h, w, mode)
 
 
 @pytest.mark.parametrize("cfg", [2, 4])
@@ -78,7 +79,7 @@ def test_path_edges(gpu_lib):
         for bonus in (True, False):
             p = path_tree(gpu_lib, w, mode, bonus=bonus)
             same(p, gpu_tree(gpu_lib, w, mode, bonus=bonus))
-            compare_walk(p, oracle_walk(h, w, mode, bonus=bonus))
+            compare_walk(p, oracle_walk(h, w, mode, bonus=bonus), h, w, mode, bonus=bonus)
         short = path_tree(gpu_lib, w, mode, max_depth=1)
         same(short, gpu_tree(gpu_lib, w, mode, max_depth=1))
         assert p["status"].cpu().numpy()[4] == 4
@@ -134,7 +135,8 @@ def test_path_groups_equal_path(gpu_lib, cfg, over, mode):
     for g in (2, 3, 5, 0):
         _log("path group", cfg, over, mode, g)
         same(group_tree(gpu_lib, w, mode, g), ref)
-    compare_walk(ref, oracle_walk(host_tree(w), w, mode))
+    h = host_tree(w)
+    compare_walk(ref, oracle_walk(h, w, mode), h, w, mode)
 
 
 def test_path_groups_full_size(gpu_lib):

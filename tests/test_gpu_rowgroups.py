@@ -55,7 +55,8 @@ def test_row_groups_equal_all_nodes(gpu_lib, cfg, over, mode):
             continue
         _log("row groups", cfg, over, mode, g)
         same(group_tree(gpu_lib, w, mode, g), ref)
-    compare_walk(ref, oracle_walk(host_tree(w), w, mode))
+    h = host_tree(w)
+    compare_walk(ref, oracle_walk(h, w, mode), h, w, mode)
 
 
 def test_row_groups_fallback_and_faults(gpu_lib):

@@ -133,3 +133,57 @@ def test_draft_tree_consistency():
     bad = parent.copy()
     bad[1, 3] = 5
     assert O.draft_tree(draft, bad, temperature=1.0)["status"] == O.BAD_TREE
+
+
+def test_check_candidates_pins():
+    """The admissibility check of claimed draws.  Logits ln(1), ln(2), ln(3), ln(4) at
+    T = 1 give D = (1, 2, 3, 4) / 10, whose cumulative sums are .1, .3, .6, 1."""
+    row = np.log(np.array([1.0, 2.0, 3.0, 4.0], np.float32)).astype(np.float32)
+    D = _softmax(row, 1.0)
+    assert np.allclose(D, [0.1, 0.2, 0.3, 0.4], atol=1e-7)
+    chk = lambda claimed, uc, worep=False: O.check_candidates(
+        row, np.array(claimed, np.int32), np.array(uc, np.float32), temperature=1.0,
+        without_replacement=worep)
+    assert chk([1], [0.2]) == 1           # .2 lies in [.1, .3)
+    assert chk([2], [0.2]) == 0
+    assert chk([3, 3], [0.9, 0.65]) == 1  # i.i.d.: the same token twice
+    # without replacement the second draw is from (1, 2, 3) / 6: .65 * 6 = 3.9 -> token 2
+    assert chk([3, 2], [0.9, 0.65], worep=True) == 1
+    assert chk([3, 3], [0.9, 0.65], worep=True) == 0
+    # a uniform on a boundary (float32 of .3 is within 1e-8 of it): either side
+    u = float(np.float32(0.3))
+    assert {chk([1], [u]), chk([2], [u])} == {1, 2}
+    assert chk([0], [u]) == 0
+    # the claim is followed, not the oracle's own draw: after a windowed first draw the
+    # second is judged against the draft without the claimed token
+    first = 2 if chk([2], [u]) == 2 else 1
+    other = 3 - first
+    rest = np.array([0.1, 0.2, 0.3, 0.4])
+    rest[first] = 0.0
+    rest /= rest.sum()
+    v = chk([first, other], [u, float(np.float32(rest[:other].sum() + rest[other] / 2))], worep=True)
+    assert v == 2
+
+
+def test_check_candidates_random_rows():
+    """The oracle's own draws are always exact; changing one unflagged draw makes the
+    claim inadmissible."""
+    rng = np.random.default_rng(21)
+    changed = 0
+    for _ in range(300):
+        V, k = int(rng.integers(2, 30)), int(rng.integers(1, 5))
+        worep = bool(rng.integers(0, 2)) and k <= V
+        row = rng.normal(size=V).astype(np.float32)
+        uc = rng.random(k).astype(np.float32)
+        tok, mg, st = O.sample_candidates(row, k, uc, temperature=1.0, without_replacement=worep)
+        if st != O.OK:
+            continue
+        assert O.check_candidates(row, tok, uc, temperature=1.0, without_replacement=worep) == 1
+        i = int(rng.integers(0, k))
+        if mg[i] < 1e-6 or (i > 0 and (mg[:i] < 1e-6).any()):
+            continue
+        bad = tok.copy()
+        bad[i] = (tok[i] + 1) % V
+        assert O.check_candidates(row, bad, uc, temperature=1.0, without_replacement=worep) == 0
+        changed += 1
+    assert changed > 100
