@@ -50,34 +50,103 @@ def measured_traffic(workload, mode):
     return rec.get("hbm_bytes_per_launch")
 
 
-def cpu_baseline(w, seconds, mode):
-    """The fp64 oracle (all-nodes evaluation, single thread) on a bounded sample of the
-    same workload: whole sequences until about `seconds` of CPU time."""
+def _cpu_model():
+    try:
+        with open("/proc/cpuinfo") as f:
+            for line in f:
+                if line.startswith("model name"):
+                    return line.split(":", 1)[1].strip()
+    except OSError:
+        pass
+    import platform
+    return platform.processor() or "unknown"
+
+
+def cpu_baseline(w, seconds, mode, gpu_nodes=None):
+    """The fp64 oracle on the host, on the same workload, three ways:
+      - all-nodes: every node row evaluated on its own (what the row kernel computes),
+        over the host's cores (threads over chunks of rows; the oracle is re-entrant and
+        ctypes releases the interpreter lock around it); this is `value`;
+      - walk: each sequence walked from its root (only the nodes the walk reaches), over
+        the same threads (one sequence per task);
+      - single thread: all-nodes on whole sequences until about `seconds` of CPU time.
+    With `gpu_nodes` (the node outcomes of the last timed GPU step) the all-nodes results
+    are also the parity check of that step: bit-exact outside the 1e-6 flag window, and
+    every flagged node either identical or admissible (the oracle's outcome check).
+    Returns (record, parity)."""
     import numpy as np
+    from concurrent.futures import ThreadPoolExecutor
     import oracle as O
     from paper_2608_24411_amd import synth
     B, N = w["B"], w["N"]
-    rows_done, t_used, seqs = 0, 0.0, 0
+    h = dict(target=synth.to_host(w["target"]), draft=synth.to_host(w["draft"]),
+             node_token=synth.to_host(w["node_token"]), parent=synth.to_host(w["parent"]),
+             u_accept=synth.to_host(w["u_accept"]), u_resample=synth.to_host(w["u_resample"]))
+    args = (h["target"], h["draft"], h["node_token"], h["parent"], h["u_accept"], h["u_resample"])
+    kw = dict(temperature=w["temperature"], mode=mode, without_replacement=w["without_replacement"],
+              bonus=w["bonus"])
+    nproc = os.cpu_count() or 1
+    avail = len(os.sched_getaffinity(0))
+    # the CPU share of one GPU on the benchmark machines is 16 cores
+    threads = max(1, min(16, avail))
+
+    rows = np.arange(B * N)
+    chunks = [c for c in np.array_split(rows, 8 * threads) if c.size]
+    t0 = time.perf_counter()
+    with ThreadPoolExecutor(threads) as ex:
+        parts = list(ex.map(lambda c: O.verify_tree_nodes(*args, c, **kw), chunks))
+    t_nodes = time.perf_counter() - t0
+    orc = {k: np.concatenate([p[k] for p in parts]) for k in parts[0]}
+
+    def walk(b):
+        sl = tuple(a[b:b + 1] for a in args)
+        return O.verify_tree_walk(*sl, max_depth=w["max_depth"], **kw)
+    t0 = time.perf_counter()
+    with ThreadPoolExecutor(threads) as ex:
+        walks = list(ex.map(walk, range(B)))
+    t_walk = time.perf_counter() - t0
+    walk_rows = int(sum(int(r["accepted_len"][0]) + 1 for r in walks))
+
+    # single thread on whole sequences, bounded by CPU time
+    single_rows, t_single, seqs = 0, 0.0, 0
     for b in range(B):
-        sel = [b]
-        h = dict(target=synth.to_host(w["target"][sel]), draft=synth.to_host(w["draft"][sel]),
-                 node_token=synth.to_host(w["node_token"][sel]),
-                 parent=synth.to_host(w["parent"][sel]),
-                 u_accept=synth.to_host(w["u_accept"][sel]),
-                 u_resample=synth.to_host(w["u_resample"][sel]))
-        t0 = time.process_time()
-        O.verify_tree_nodes(h["target"], h["draft"], h["node_token"], h["parent"], h["u_accept"],
-                            h["u_resample"], np.arange(N), temperature=w["temperature"],
-                            mode=mode, without_replacement=w["without_replacement"],
-                            bonus=w["bonus"])
-        t_used += time.process_time() - t0
-        rows_done += N
+        c0 = time.process_time()
+        O.verify_tree_nodes(*args, np.arange(b * N, (b + 1) * N), **kw)
+        t_single += time.process_time() - c0
+        single_rows += N
         seqs += 1
-        if t_used >= seconds:
+        if t_single >= seconds:
             break
-    return {"value": rows_done / t_used, "unit": "rows/s", "cores": 1, "kind": "oracle",
-            "sample": "%d of %d sequences (%d node rows) of %s, every node evaluated, fp64, "
-                      "one thread, %.1f s CPU" % (seqs, B, rows_done, w["cfg"]["name"], t_used)}
+
+    rec = {"value": B * N / t_nodes, "unit": "rows/s", "cores": threads, "kind": "oracle",
+           "sample": "all %d node rows of %s (%d sequences), every node evaluated, fp64, %d host "
+                     "threads over chunks of rows (%.2f s wall)" % (B * N, w["cfg"]["name"], B,
+                                                                   threads, t_nodes),
+           "nproc": nproc, "cores_available": avail, "cpu_model": _cpu_model(),
+           "all_nodes_rows_per_s": B * N / t_nodes,
+           "walk_rows_per_s": walk_rows / t_walk, "walk_sequences_per_s": B / t_walk,
+           "walk_rows": walk_rows,
+           "single_thread_rows_per_s": single_rows / t_single,
+           "single_thread_sample": "%d of %d sequences (%d rows), all-nodes, %.1f s CPU" % (
+               seqs, B, single_rows, t_single)}
+
+    parity = None
+    if gpu_nodes is not None:
+        gc, gk, gs = (np.asarray(a).reshape(-1) for a in gpu_nodes)
+        fl = orc["flagged"].astype(bool)
+        exp_status = orc["status"]   # the oracle's codes 0-6 are the library's
+        diff = (gc != orc["child"]) | (gk != orc["token"]) | (gs != exp_status)
+        redo = np.flatnonzero(fl & diff)
+        verdict = (O.check_tree_nodes(*args, redo, gc[redo], gk[redo], gs[redo], **kw)
+                   if redo.size else np.empty(0, np.int32))
+        parity = {"compared": int(B * N), "exact": int((~fl).sum()),
+                  "mismatches": int((~fl & diff).sum()),
+                  "flagged": int(fl.sum()), "flagged_identical": int((fl & ~diff).sum()),
+                  "flagged_valid": int((verdict != 0).sum()),
+                  "flagged_invalid": int((verdict == 0).sum()),
+                  "mismatches_margin_ge_1e-7": int((fl & diff & (orc["margin"] >= 1e-7)).sum()),
+                  "reference": "fp64 oracle, all-nodes evaluation of the timed step's inputs"}
+    return rec, parity
 
 
 def read_ceiling(torch, chunk=1 << 19, nbytes=4 << 30, reps=5):
@@ -148,6 +217,118 @@ def time_mode(native, torch, w, mode, steps, warmup, settle, ws, out_tok, out_le
     wall = time.perf_counter() - t0
     kern_ms = [e0.elapsed_time(e1) for e0, e1 in ev]
     return wall, kern_ms
+
+
+def _event_ms(torch, fn, steps, warmup, flush=None):
+    """Device time of fn() in ms per call: HIP events on the current stream (the stream
+    the binding launches on) around every call.  flush(), when given, runs before each
+    call outside the events."""
+    for _ in range(warmup):
+        if flush:
+            flush()
+        fn()
+    ev = [(torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True))
+          for _ in range(steps)]
+    torch.cuda.synchronize()
+    for e0, e1 in ev:
+        if flush:
+            flush()
+        e0.record()
+        fn()
+        e1.record()
+    torch.cuda.synchronize()
+    return [e0.elapsed_time(e1) for e0, e1 in ev]
+
+
+def configs_record(native, torch, np, synth, steps, warmup, mode, headline):
+    """The row kernel on every workload of the benchmark recipes (the headline workload's
+    figures are copied from its timed run): algorithmic bytes per launch, mean launch
+    time from HIP events, GB/s and the fraction of 8 TB/s.  The flat 8-row workload is
+    launch-bound and reported in microseconds per call; the 64 x 21 chain workload
+    (213 MB, inside the last-level cache) is timed warm and cold (a 512 MiB buffer
+    written before every cold call)."""
+    out = {}
+    for cfg in (0, 1, 2, 3, 4):
+        name = synth.CONFIGS[cfg]["name"]
+        if cfg == 2:
+            out[name] = headline
+            continue
+        w = synth.make_workload(cfg, device="cuda")
+        esz = 2 if w["target"].dtype == torch.bfloat16 else 4
+        if cfg == 0:
+            B, V = w["B"], w["V"]
+            alg = 2 * B * V * esz + 24 * B   # both rows of every position; ids, uniforms, outputs
+
+            def call():
+                native.resispec_verify(w["target"], w["draft"], w["cand_ids"], w["u_accept"],
+                                       w["u_resample"], temperature=w["temperature"], mode=mode)
+            for _ in range(20):
+                call()
+            torch.cuda.synchronize()
+            queued = []
+            for _ in range(5):
+                e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+                e0.record()
+                for _ in range(100):
+                    call()
+                e1.record()
+                torch.cuda.synchronize()
+                queued.append(e0.elapsed_time(e1) * 1e3 / 100)
+            lone = []
+            for _ in range(20):
+                torch.cuda.synchronize()
+                t0 = time.perf_counter()
+                call()
+                torch.cuda.synchronize()
+                lone.append((time.perf_counter() - t0) * 1e6)
+            out[name] = {"B": B, "V": V, "k": w["k"], "us_per_call": float(np.median(queued)),
+                         "us_per_call_note": "device time per call with 100 calls queued, median of 5",
+                         "lone_call_us": float(np.median(lone)),
+                         "lone_call_note": "host wall time of one call and its synchronisation, median of 20",
+                         "alg_bytes_per_call": alg,
+                         "achieved_gbps": alg / (float(np.median(queued)) * 1e-6) / 1e9}
+            del w
+            continue
+        B, N, V = w["B"], w["N"], w["V"]
+        logit_bytes, rows_t, rows_d = synth.algorithmic_bytes(w["parent"].cpu().numpy(), V, esz)
+        alg = logit_bytes + 28 * B * N
+        ws = torch.empty(native.resispec_workspace_bytes(B, N), dtype=torch.uint8, device="cuda")
+        args = (w["target"], w["draft"], w["node_token"], w["parent"], w["u_accept"], w["u_resample"])
+        kw = dict(temperature=w["temperature"], mode=mode,
+                  without_replacement=w["without_replacement"], bonus=w["bonus"])
+
+        def nodes():
+            native.resispec_verify_nodes(*args, ws, **kw)
+        t_end = time.perf_counter() + 0.3
+        while time.perf_counter() < t_end:
+            nodes()
+            torch.cuda.synchronize()
+        ms = _event_ms(torch, nodes, steps, warmup)
+        kms = float(np.mean(ms))
+        rec = {"B": B, "N": N, "V": V, "logits": "bf16" if esz == 2 else "f32",
+               "rows_target": rows_t, "rows_draft": rows_d, "alg_bytes_per_launch": alg,
+               "row_kernel_ms": kms, "row_kernel_ms_min": float(np.min(ms)),
+               "rows_per_s": B * N / (kms * 1e-3),
+               "achieved_gbps": alg / (kms * 1e-3) / 1e9,
+               "frac": alg / (kms * 1e-3) / 1e9 / HBM_PEAK_GBPS}
+        if cfg == 1:
+            flush_buf = torch.empty(512 << 20, dtype=torch.uint8, device="cuda")
+            fill = [0]
+
+            def flush():
+                fill[0] = (fill[0] + 1) & 0xff
+                flush_buf.fill_(fill[0])
+            cold = _event_ms(torch, nodes, steps, 2, flush=flush)
+            cms = float(np.mean(cold))
+            rec["warm"] = {"row_kernel_ms": kms, "achieved_gbps": rec["achieved_gbps"]}
+            rec["cold"] = {"row_kernel_ms": cms, "achieved_gbps": alg / (cms * 1e-3) / 1e9,
+                           "frac": alg / (cms * 1e-3) / 1e9 / HBM_PEAK_GBPS,
+                           "flush": "512 MiB written before every call, outside the events"}
+            del flush_buf
+        out[name] = rec
+        del w, ws, args
+        torch.cuda.empty_cache()
+    return out
 
 
 def run_study(native, torch, np, synth):
@@ -239,6 +420,8 @@ def main():
                     help="skip the single-tree latency of the same shape")
     ap.add_argument("--no-read-probe", action="store_true",
                     help="skip the read-bandwidth probe (the measured ceiling)")
+    ap.add_argument("--no-configs", action="store_true",
+                    help="skip the row kernel on the other workloads")
     ap.add_argument("--study", action="store_true",
                     help="only run the synthetic acceptance studies (not a benchmark)")
     ap.add_argument("--copy-probe", type=int, default=0, metavar="MIB",
@@ -284,6 +467,7 @@ def main():
     out_st = torch.empty(B, dtype=torch.int32, device="cuda")
 
     results = {}
+    gpu_nodes = None
     modes = [args.mode] + ([] if args.no_other_mode else
                            [m for m in ("resispec", "specinfer") if m != args.mode])
     for mode in modes:
@@ -291,6 +475,9 @@ def main():
                                   args.settle_ms * 1e-3, ws, out_tok, out_len, out_st)
         lens = out_len.cpu().numpy()
         assert (out_st.cpu().numpy() == 0).all(), "device status not OK"
+        if mode == args.mode:
+            # the node outcomes the last timed step left in its workspace (parity below)
+            gpu_nodes = tuple(t.cpu().numpy() for t in native.resispec_node_outcomes(ws, B, N))
         kms = float(np.mean(kern_ms))
         results[mode] = {
             "ms_per_step": 1e3 * wall / args.steps,
@@ -468,9 +655,24 @@ def main():
         "draft_step": draft,
         "single_tree": single,
     }
+    if not args.no_configs:
+        headline = {"B": B, "N": N, "V": V, "logits": "bf16" if esz == 2 else "f32",
+                    "rows_target": rows_t, "rows_draft": rows_d, "alg_bytes_per_launch": alg_bytes,
+                    "row_kernel_ms": r["row_kernel_ms"], "row_kernel_ms_min": r["row_kernel_ms_min"],
+                    "rows_per_s": B * N / (r["row_kernel_ms"] * 1e-3),
+                    "achieved_gbps": achieved, "frac": achieved / HBM_PEAK_GBPS,
+                    "step_ms": r["ms_per_step"], "note": "the headline run"}
+        out["configs"] = configs_record(native, torch, np, synth, args.steps, args.warmup,
+                                        args.mode, headline)
+    parity = None
     if not args.no_cpu_baseline:
-        out["cpu_baseline"] = cpu_baseline(w, args.cpu_seconds, args.mode)
+        out["cpu_baseline"], parity = cpu_baseline(w, args.cpu_seconds, args.mode, gpu_nodes)
+        out["parity"] = parity
     print(json.dumps(out), flush=True)
+    if parity and (parity["mismatches"] or parity["flagged_invalid"]
+                   or parity["mismatches_margin_ge_1e-7"]):
+        print("parity failure: %s" % json.dumps(parity), file=sys.stderr)
+        sys.exit(1)
 
 
 if __name__ == "__main__":

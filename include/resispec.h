@@ -288,6 +288,20 @@ rs_status resispec_walk(const int32_t* node_token, int32_t B, int32_t N, int32_t
                         const void* workspace, size_t workspace_bytes, int32_t* out_tokens,
                         int32_t* out_accepted_len, int32_t* out_status, void* stream);
 
+/*
+ * Every node's own outcome as resispec_verify_nodes left it in `workspace` (the same
+ * B and N, earlier on the same stream), copied into caller arrays (device-to-device,
+ * stream-ordered, asynchronous): the outcome of Algorithm 1 at each node, as the debug
+ * entry below reports it.
+ *   node_child, node_token_out, node_status : [B][N] int32 device out, as in
+ *                 resispec_verify_tree_debug
+ * RS_ERR_INVALID_ARG for B < 0, N <= 0 or NULL outputs (B > 0); RS_ERR_WORKSPACE for a
+ * missing or short workspace.
+ */
+rs_status resispec_node_outcomes(const void* workspace, size_t workspace_bytes, int32_t B,
+                                 int32_t N, int32_t* node_child, int32_t* node_token_out,
+                                 int32_t* node_status, void* stream);
+
 /* Workspace bytes resispec_verify_tree needs for B sequences of N nodes. */
 size_t resispec_workspace_bytes(int32_t B, int32_t N);
 

@@ -245,6 +245,11 @@ struct Smem {
     int32_t sx0;                    // slot holding x_0
     double slotP[kMaxSlots];        // pass-1 slot totals of the target row
     uint32_t hit_slots[kMaxSlots / 32];  // slots that hold a rejected token
+    // slots that hold a candidate (without replacement: pass 1 sums the draft row without
+    // the candidates, whose masses are added in fp64, so the draft mass left after any
+    // removals is a sum of what remains rather than a difference)
+    uint32_t cand_slots[kMaxSlots / 32];
+    double Sd_nc;                   // draft mass outside the candidates (without replacement)
     // per-lane partials of every slot of the running pass ([lane][slot], padded so a
     // wave's 64 stores hit 64 distinct banks), reduced after the pass in a fixed order
     float partA[64][kMaxSlots + 1];

@@ -61,7 +61,6 @@ struct DraftSmem {
     int32_t cand_tok[kMaxCand];
     int32_t cand_node[kMaxCand];
     float cand_u[kMaxCand];
-    double cand_p[kMaxCand];
     float wmax[2][kMaxWaves];
     double slotA[kMaxSlots];
     float partA[64][kMaxSlots + 1];
@@ -161,7 +160,6 @@ __global__ void __launch_bounds__(kBlock) __attribute__((amdgpu_waves_per_eu(4))
         for (int w = 0; w < kWaves; ++w) m0 = fmaxf(m0, sm.wmax[0][w]);
         K = kref(m0, c2h);
     }
-    double total = 0.0;
     for (int attempt = 0;; ++attempt) {
         float fa = 0.0f;
         wave_sweep<In, VEC, UNR, false, 1, true>(dg, dg, V, G, nslots, 0, false, pre, pre, &sm.next_slot,
@@ -191,10 +189,7 @@ __global__ void __launch_bounds__(kBlock) __attribute__((amdgpu_waves_per_eu(4))
             }
         }
         __syncthreads();
-        if (sm.decision != -3) {
-            total = sm.total;
-            break;
-        }
+        if (sm.decision != -3) break;
         if (attempt == 1) {
             // no usable distribution: the children keep token -1
             if (tid < nc) P.node_token[sb + sm.cand_node[tid]] = -1;
@@ -227,39 +222,26 @@ __global__ void __launch_bounds__(kBlock) __attribute__((amdgpu_waves_per_eu(4))
     const bool worep = P.worep != 0;
     if (worep && wid != 0) return;
     const int R = G * VEC * UNR;          // elements of a slot per lane
-    double removed = 0.0;                 // mass drawn so far (without replacement)
+    // slot totals in vocabulary order, lane l holding slots 4l .. 4l+3.  Without
+    // replacement a draw replaces its slot's total by the fp64 sum of the slot's elements
+    // that remain (computed in the draw below), so the mass left is always a sum of
+    // what remains, never the total less the removed mass.
+    double Ts[4];
+#pragma unroll
+    for (int q = 0; q < 4; ++q) {
+        const int s2 = 4 * lane + q;
+        Ts[q] = s2 < nslots ? sm.slotA[s2] : 0.0;
+    }
     for (int i = worep ? 0 : wid; i < nc; i += worep ? 1 : kWaves) {
-        const double thr = (double)sm.cand_u[i] * (total - removed);
-        // removed tokens of each slot (lane j holds removed token j, j < i)
+        // removed tokens (lane j holds removed token j, j < i)
         const int32_t rtok = (worep && lane < i) ? sm.cand_tok[lane] : -1;
         const int rslot = rtok >= 0 ? (rtok / CHUNK) / G : -1;
-        const double rval = rtok >= 0 ? sm.cand_p[lane] : 0.0;
-        double Ts[4];
         double own = 0.0;
 #pragma unroll
-        for (int q = 0; q < 4; ++q) {
-            const int s2 = 4 * lane + q;
-            double T = 0.0;
-            if (s2 < nslots) T = sm.slotA[s2];
-            Ts[q] = T;
-        }
-        // subtract removed masses slot by slot (at most i tokens, broadcast one by one)
-        if (worep) {
-            for (int j = 0; j < i; ++j) {
-                const int sj = __builtin_amdgcn_readlane(rslot, j);
-                const double vj = readlane_d(rval, j);
-#pragma unroll
-                for (int q = 0; q < 4; ++q)
-                    if (4 * lane + q == sj) Ts[q] -= vj;
-            }
-        }
-#pragma unroll
-        for (int q = 0; q < 4; ++q) {
-            Ts[q] = Ts[q] > 0.0 ? Ts[q] : 0.0;
-            own += Ts[q];
-        }
+        for (int q = 0; q < 4; ++q) own += Ts[q];
         const double incl = wave_incl_scan(own, lane);
         const double excl = incl - own;
+        const double thr = (double)sm.cand_u[i] * readlane_d(incl, 63);
         uint64_t hit = __ballot(own > 0.0 && incl > thr);
         int L = hit ? (__ffsll((unsigned long long)hit) - 1) : -1;
         if (L < 0) {
@@ -396,18 +378,26 @@ __global__ void __launch_bounds__(kBlock) __attribute__((amdgpu_waves_per_eu(4))
                 tok = __builtin_amdgcn_readlane(tok, L2);
                 tval = (double)readlane_f(tv, L2);
             }
+            if (worep && tok >= 0) {
+                // the slot's remaining mass: its elements summed in fp64 without the
+                // removed tokens and without this draw (own2 is exact up to fp64 rounding
+                // of fp32 values, so taking the drawn value out cancels nothing)
+                const bool mine = tok >= t0 && tok < t0 + R;
+                const double rest = wave_sum(own2 - (mine ? tval : 0.0));
+#pragma unroll
+                for (int q = 0; q < 4; ++q)
+                    if (4 * lane + q == ks) Ts[q] = rest > 0.0 ? rest : 0.0;
+            }
         }
         if (lane == 0) {
             P.node_token[sb + sm.cand_node[i]] = tok;
             sm.cand_tok[i] = tok;
-            sm.cand_p[i] = tval;
         }
         if (tok < 0 && worep) {
             // nothing left to draw from: the remaining children keep token -1
             for (int i2 = i + 1 + lane; i2 < nc; i2 += 64) P.node_token[sb + sm.cand_node[i2]] = -1;
             break;
         }
-        if (worep) removed += tval;
         __builtin_amdgcn_wave_barrier();
     }
 }

@@ -339,7 +339,10 @@ __device__ __forceinline__ void verify_row(const KParams& P, Smem& sm, const int
         sm.next_slot = kWaves;
         sm.ur = P.flat ? P.ur_flat[row] : P.ur[row];
     }
-    for (int w = tid; w < kMaxSlots / 32; w += kBlock) sm.hit_slots[w] = 0u;
+    for (int w = tid; w < kMaxSlots / 32; w += kBlock) {
+        sm.hit_slots[w] = 0u;
+        sm.cand_slots[w] = 0u;
+    }
     // The maximum over the first chunks of the first slots (chunk w * G for wave w) fixes
     // the row's exponent reference, the same in every schedule and in every member of a
     // row group: each wave requested its chunk above, except in members whose slots start
@@ -433,6 +436,10 @@ __device__ __forceinline__ void verify_row(const KParams& P, Smem& sm, const int
                         const bool ok = x >= 0 && x < V;
                         sm.cand_lt[idx] = ok ? widen(tg[x]) : 0.0f;
                         sm.cand_ld[idx] = ok ? widen(dg[x]) : 0.0f;
+                        if (ok && P.worep) {
+                            const int cs = (x / CHUNK) / G;
+                            atomicOr(&sm.cand_slots[cs >> 5], 1u << (cs & 31));
+                        }
                     }
                 }
                 count += __popcll(mask);
@@ -498,6 +505,22 @@ __device__ __forceinline__ void verify_row(const KParams& P, Smem& sm, const int
         sm.cand_ld[hrank] = hld;
         sm.cand_p[hrank] = pe;
         sm.cand_q[hrank] = qe;
+        if (hx >= 0 && hx < V && P.worep) {
+            const int cs = (hx / CHUNK) / G;
+            atomicOr(&sm.cand_slots[cs >> 5], 1u << (cs & 31));
+        }
+    }
+    // Without replacement pass 1 leaves the candidates out of the draft sum (their masses
+    // are added in fp64 after it), so every wave needs the candidate list and its slots.
+    const bool mask_cands = internal && P.worep;
+    static_assert(kMaxSlots == 128, "four words of candidate slots");
+    uint32_t cm0 = 0u, cm1 = 0u, cm2 = 0u, cm3 = 0u;
+    if (mask_cands) {
+        __syncthreads();
+        cm0 = __builtin_amdgcn_readfirstlane(sm.cand_slots[0]);
+        cm1 = __builtin_amdgcn_readfirstlane(sm.cand_slots[1]);
+        cm2 = __builtin_amdgcn_readfirstlane(sm.cand_slots[2]);
+        cm3 = __builtin_amdgcn_readfirstlane(sm.cand_slots[3]);
     }
     for (int attempt = 0;; ++attempt) {
         float fa = 0.0f, fc = 0.0f;   // this slot's lane partials
@@ -508,7 +531,25 @@ __device__ __forceinline__ void verify_row(const KParams& P, Smem& sm, const int
         };
         if (internal) {
             wave_sweep<In, VEC, UNR, true, 1, kNtPass1>(tg, dg, V, G, nl, s0, false, pre, pre, &sm.next_slot,
-                [&](const float (&t)[UNR][VEC], const float (&d)[UNR][VEC], int, int) {
+                [&](const float (&t)[UNR][VEC], const float (&d)[UNR][VEC], int idx0, int slot) {
+                    const int sw = slot >> 5;
+                    const uint32_t cw = sw == 0 ? cm0 : (sw == 1 ? cm1 : (sw == 2 ? cm2 : cm3));
+                    if ((cw >> (slot & 31)) & 1u) {
+                        // a slot holding a candidate (without replacement): its draft
+                        // elements are summed without the candidates
+#pragma unroll
+                        for (int u = 0; u < UNR; ++u)
+#pragma unroll
+                            for (int e = 0; e < VEC; ++e) {
+                                fa += exp2_fast(expo(t[u][e], c2h, c2l, Kt));
+                                float q = exp2_fast(expo(d[u][e], c2h, c2l, Kd));
+                                const int j = idx0 + u * 64 * VEC + e;
+                                for (int c = 0; c < nc; ++c)
+                                    if (j == sm.cand_tok[c]) q = 0.0f;
+                                fc += q;
+                            }
+                        return;
+                    }
 #pragma unroll
                     for (int u = 0; u < UNR; ++u)
 #pragma unroll
@@ -528,8 +569,6 @@ __device__ __forceinline__ void verify_row(const KParams& P, Smem& sm, const int
                 },
                 flush);
         }
-        if (attempt == 0) {
-        }
         __syncthreads();
         if (!pass_totals<BLK, SPLIT>(sm, grp, nslots, s0, nl, internal, true)) {
             if (tid == 0) emit(-1, -1, RS_SEQ_GROUP_TIMEOUT);
@@ -544,11 +583,34 @@ __device__ __forceinline__ void verify_row(const KParams& P, Smem& sm, const int
             }
             const double s0 = wave_sum(a0);
             const double s1 = wave_sum(a1);
-            const bool ok = s0 >= kLowSum && s0 < INFINITY && (!internal || (s1 >= kLowSum && s1 < INFINITY));
+            // Without replacement: the candidates' draft masses (each token once, fp64)
+            // complete the draft sum, and the draft left after the first i rejections
+            // weighs s1 plus the masses of the candidates from i on (a suffix sum, no
+            // cancellation); its scale against the whole draft is st_ds[i].
+            double wc = 0.0;
+            if (mask_cands && lane < nc) {
+                const int32_t x = sm.cand_tok[lane];
+                bool first = x >= 0 && x < V;
+                for (int c = 0; c < lane; ++c) first = first && sm.cand_tok[c] != x;
+                if (first) wc = exp2((double)sm.cand_ld[lane] * c2d + (double)Kd);
+            }
+            const double sd = mask_cands ? s1 + wave_sum(wc) : s1;
+            const bool ok = s0 >= kLowSum && s0 < INFINITY && (!internal || (sd >= kLowSum && sd < INFINITY));
+            if (mask_cands) {
+                double suf = 0.0;
+                for (int c = nc - 1; c >= 0; --c) {
+                    suf += readlane_d(wc, c);
+                    const double rem = s1 + suf;
+                    if (lane == 0) sm.st_ds[c] = c == 0 ? 1.0 : (rem > 0.0 ? sd / rem : 0.0);
+                }
+                if (lane == 0) sm.st_ds[nc] = s1 > 0.0 ? sd / s1 : 0.0;
+            } else if (lane == 0) {
+                for (int c = 0; c <= nc; ++c) sm.st_ds[c] = 1.0;
+            }
             if (lane == 0) {
                 sm.St = s0;
-                sm.Sd = s1;
-                sm.st_ds[0] = 1.0;
+                sm.Sd = sd;
+                sm.Sd_nc = s1;
                 sm.decision = ok ? -1 : -3;   // -3: sum again with exact maxima
                 sm.next_slot = kWaves;
             }
@@ -853,14 +915,6 @@ __device__ __forceinline__ void verify_row(const KParams& P, Smem& sm, const int
                     sm.st_i[i] = (float)(1.0 / z);
                     sm.st_k1[i] = (float)(a / z);
                     sm.st_kc[i] = (float)((1.0 - a) * sm.st_ds[i] * q2t);   // (1 - a) c / Z
-                }
-            }
-            if (lane == 0) {
-                if (worep) {
-                    const double rest = 1.0 - sm.cand_q[i] * sm.st_ds[i];
-                    sm.st_ds[i + 1] = rest > 0.0 ? sm.st_ds[i] / rest : 0.0;
-                } else {
-                    sm.st_ds[i + 1] = 1.0;
                 }
             }
         }
@@ -1859,6 +1913,25 @@ rs_status resispec_walk(const int32_t* node_token, int32_t B, int32_t N, int32_t
     return launch_walk(ws_array(ws, rows, 0), ws_array(ws, rows, 1), ws_array(ws, rows, 2),
                        node_token, B, N, max_depth, out_tokens, out_accepted_len, out_status,
                        (hipStream_t)stream) == hipSuccess ? RS_OK : RS_ERR_HIP;
+}
+
+rs_status resispec_node_outcomes(const void* workspace, size_t workspace_bytes, int32_t B,
+                                 int32_t N, int32_t* node_child, int32_t* node_token_out,
+                                 int32_t* node_status, void* stream) {
+    if (B < 0 || N <= 0) return RS_ERR_INVALID_ARG;
+    if ((int64_t)B * N > 0x7fffffffLL) return RS_ERR_UNSUPPORTED;
+    if (B == 0) return RS_OK;
+    if (!node_child || !node_token_out || !node_status) return RS_ERR_INVALID_ARG;
+    if (!workspace || workspace_bytes < resispec_workspace_bytes(B, N) || !aligned16(workspace))
+        return RS_ERR_WORKSPACE;
+    const int64_t rows = (int64_t)B * N;
+    void* ws = const_cast<void*>(workspace);
+    int32_t* dst[3] = {node_child, node_token_out, node_status};
+    for (int k = 0; k < 3; ++k)
+        if (hipMemcpyAsync(dst[k], ws_array(ws, rows, k), (size_t)rows * sizeof(int32_t),
+                           hipMemcpyDeviceToDevice, (hipStream_t)stream) != hipSuccess)
+            return RS_ERR_HIP;
+    return RS_OK;
 }
 
 rs_status resispec_verify_tree_debug(const void* target_logits, const void* draft_logits,

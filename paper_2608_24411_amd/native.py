@@ -27,7 +27,7 @@ EXPORTS = ("resispec_verify", "resispec_verify_tree", "resispec_verify_tree_path
            "resispec_verify_tree_group", "resispec_tree_group_workspace_bytes",
            "resispec_tree_group_size",
            "resispec_draft_candidates",
-           "resispec_verify_nodes", "resispec_walk",
+           "resispec_verify_nodes", "resispec_walk", "resispec_node_outcomes",
            "resispec_workspace_bytes", "resispec_validate_tree_host",
            "resispec_verify_tree_debug", "resispec_status_string", "resispec_abi_version")
 
@@ -83,6 +83,8 @@ def _load():
     lib.resispec_verify_nodes.restype = i32
     lib.resispec_walk.argtypes = [P, i32, i32, i32, P, sz, P, P, P, P]
     lib.resispec_walk.restype = i32
+    lib.resispec_node_outcomes.argtypes = [P, sz, i32, i32, P, P, P, P]
+    lib.resispec_node_outcomes.restype = i32
     lib.resispec_workspace_bytes.argtypes = [i32, i32]
     lib.resispec_workspace_bytes.restype = sz
     lib.resispec_validate_tree_host.argtypes = [P, P, i32, i32, i32, ctypes.POINTER(i64)]
@@ -476,6 +478,18 @@ def resispec_walk(node_token, workspace, out_tokens, out_accepted_len, out_statu
         _dev(out_status, torch.int32, "out_status") if out_status is not None else None,
         _stream(stream))
     _check(st)
+
+
+def resispec_node_outcomes(workspace, B: int, N: int, *, stream=None):
+    """Every node's outcome left in `workspace` by resispec_verify_nodes: (node_child,
+    node_token, node_status), [B, N] int32 each."""
+    import torch
+    dev = workspace.device
+    out = [torch.empty((B, N), dtype=torch.int32, device=dev) for _ in range(3)]
+    st = lib.resispec_node_outcomes(_dev(workspace, torch.uint8, "workspace"), workspace.numel(),
+                                    int(B), int(N), *[o.data_ptr() for o in out], _stream(stream))
+    _check(st)
+    return tuple(out)
 
 
 def resispec_verify_tree_debug(target_logits, draft_logits, node_token, parent, u_accept,
