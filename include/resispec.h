@@ -141,6 +141,28 @@ rs_status resispec_verify_tree(const void* target_logits, const void* draft_logi
                                void* workspace, size_t workspace_bytes, void* stream);
 
 /*
+ * resispec_verify_tree without a caller workspace, for callers that cannot allocate
+ * device memory (code under HIP graph capture, tight serving loops, harnesses that
+ * forbid hipMalloc).  Same arguments, kernels and results as resispec_verify_tree; the
+ * per-node outcomes go to a static device array of the library (one per GPU, held until
+ * the process ends) sized for RS_NOALLOC_MAX_ROWS node rows (768 KiB).  The call
+ * allocates nothing and nothing needs clearing: every call writes all B * N outcomes
+ * before its walk reads them.  All calls on one GPU share that array, so calls that
+ * overlap on one GPU (on different streams, or from different threads) race; calls
+ * ordered on one stream do not.
+ * RS_ERR_UNSUPPORTED when B * N > RS_NOALLOC_MAX_ROWS; RS_ERR_HIP if the array's device
+ * address cannot be found; otherwise the errors of resispec_verify_tree.
+ */
+#define RS_NOALLOC_MAX_ROWS 65536
+rs_status resispec_verify_tree_noalloc(const void* target_logits, const void* draft_logits,
+                                       const int32_t* node_token, const int32_t* parent,
+                                       const float* u_accept, const float* u_resample,
+                                       int32_t B, int32_t N, int32_t V, int32_t max_depth,
+                                       const rs_params* prm, int32_t* out_tokens,
+                                       int32_t* out_accepted_len, int32_t* out_status,
+                                       void* stream);
+
+/*
  * Path-only schedule of resispec_verify_tree (same arguments without the workspace, same
  * results): one workgroup per sequence walks its tree from the root and verifies only
  * the nodes the walk reaches, one after another (Preliminary, tree-structured

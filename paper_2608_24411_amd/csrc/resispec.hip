@@ -47,6 +47,7 @@
 // step that precedes verification is in draft.hip; shared helpers are in common.h.
 
 #include <atomic>
+#include <mutex>
 
 #include "common.h"
 
@@ -1677,8 +1678,36 @@ rs_status check_tree_args(const void* target_logits, const void* draft_logits,
 
 }  // namespace
 
-extern "C" {
+// Scratch of the entry point that allocates nothing (resispec_verify_tree_noalloc): the
+// per-node outcome arrays of RS_NOALLOC_MAX_ROWS node rows, laid out as the caller
+// workspace of resispec_verify_tree.  Every GPU the library runs on holds one copy until
+// the process ends; its device address is looked up once per device (in host code the
+// array's name is not a device address).
+constexpr int64_t kNoAllocRows = RS_NOALLOC_MAX_ROWS;
+constexpr size_t kNoAllocBytes = 3 * (((size_t)kNoAllocRows * sizeof(int32_t) + 255) & ~(size_t)255);
+__device__ __align__(256) char scratch[kNoAllocBytes];
 
+namespace {
+
+std::mutex g_scratch_mu;
+void* g_scratch_ptr[64];   // per device, null until looked up
+
+// The current device's address of `scratch` (null if the lookup fails).
+void* scratch_ptr() {
+    int dev = 0;
+    if (hipGetDevice(&dev) != hipSuccess || dev < 0 || dev >= 64) return nullptr;
+    std::lock_guard<std::mutex> lock(g_scratch_mu);
+    if (!g_scratch_ptr[dev]) {
+        void* p = nullptr;
+        if (hipGetSymbolAddress(&p, HIP_SYMBOL(scratch)) != hipSuccess) return nullptr;
+        g_scratch_ptr[dev] = p;
+    }
+    return g_scratch_ptr[dev];
+}
+
+}  // namespace
+
+extern "C" {
 
 int32_t resispec_abi_version(void) { return RESISPEC_ABI_VERSION; }
 
@@ -1744,6 +1773,30 @@ rs_status resispec_verify_tree(const void* target_logits, const void* draft_logi
                      max_depth, prm, out_tokens, out_accepted_len, out_status,
                      ws_array(workspace, rows, 0), ws_array(workspace, rows, 1),
                      ws_array(workspace, rows, 2), nullptr, (hipStream_t)stream);
+}
+
+rs_status resispec_verify_tree_noalloc(const void* target_logits, const void* draft_logits,
+                                       const int32_t* node_token, const int32_t* parent,
+                                       const float* u_accept, const float* u_resample,
+                                       int32_t B, int32_t N, int32_t V, int32_t max_depth,
+                                       const rs_params* prm, int32_t* out_tokens,
+                                       int32_t* out_accepted_len, int32_t* out_status,
+                                       void* stream) {
+    const rs_status as = check_tree_args(target_logits, draft_logits, node_token, parent, u_accept,
+                                         u_resample, B, N, V, max_depth, prm, out_tokens,
+                                         out_accepted_len);
+    if (as != RS_OK || B == 0) return as;
+    const int64_t rows = (int64_t)B * N;
+    if (rows > kNoAllocRows) return RS_ERR_UNSUPPORTED;
+    void* ws = scratch_ptr();
+    if (!ws) return RS_ERR_HIP;
+    // the node arrays of `rows` rows fit the scratch laid out for kNoAllocRows rows; the
+    // row kernel writes every row's outcome before the walk reads it, so nothing needs
+    // clearing between calls
+    return tree_impl(target_logits, draft_logits, node_token, parent, u_accept, u_resample, B, N, V,
+                     max_depth, prm, out_tokens, out_accepted_len, out_status,
+                     ws_array(ws, rows, 0), ws_array(ws, rows, 1), ws_array(ws, rows, 2), nullptr,
+                     (hipStream_t)stream);
 }
 
 size_t resispec_tree_group_workspace_bytes(int32_t B, int32_t N) {

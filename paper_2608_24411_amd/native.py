@@ -21,7 +21,8 @@ RS_MAX_CANDIDATES = 64
 MODES = {"resispec": RS_MODE_RESISPEC, "specinfer": RS_MODE_SPECINFER}
 
 # Every symbol include/resispec.h declares.
-EXPORTS = ("resispec_verify", "resispec_verify_tree", "resispec_verify_tree_path",
+EXPORTS = ("resispec_verify", "resispec_verify_tree", "resispec_verify_tree_noalloc",
+           "resispec_verify_tree_path",
            "resispec_verify_tree_path_group", "resispec_path_workspace_bytes",
            "resispec_path_group_size", "resispec_debug_set_group_waits",
            "resispec_verify_tree_group", "resispec_tree_group_workspace_bytes",
@@ -54,6 +55,9 @@ def _load():
     lib.resispec_verify_tree.argtypes = [P, P, P, P, P, P, i32, i32, i32, i32, prm, P, P, P,
                                          P, sz, P]
     lib.resispec_verify_tree.restype = i32
+    lib.resispec_verify_tree_noalloc.argtypes = [P, P, P, P, P, P, i32, i32, i32, i32, prm, P, P,
+                                                 P, P]
+    lib.resispec_verify_tree_noalloc.restype = i32
     lib.resispec_verify_tree_path.argtypes = [P, P, P, P, P, P, i32, i32, i32, i32, prm, P, P, P,
                                               P]
     lib.resispec_verify_tree_path.restype = i32
@@ -261,6 +265,38 @@ def resispec_verify_tree(target_logits, draft_logits, node_token, parent, u_acce
         _dev(out_accepted_len, torch.int32, "out_accepted_len"),
         _dev(out_status, torch.int32, "out_status"),
         _dev(workspace, torch.uint8, "workspace"), workspace.numel(), _stream(stream))
+    _check(st)
+    return out_tokens, out_accepted_len, out_status
+
+
+RS_NOALLOC_MAX_ROWS = 65536
+
+
+def resispec_verify_tree_noalloc(target_logits, draft_logits, node_token, parent, u_accept,
+                                 u_resample, *, temperature, max_depth, mode="resispec",
+                                 without_replacement=False, bonus=True, out_tokens, out_accepted_len,
+                                 out_status=None, stream=None):
+    """resispec_verify_tree with the library's static per-GPU scratch instead of a
+    workspace (B * N <= RS_NOALLOC_MAX_ROWS); the caller passes the outputs.  Calls that
+    overlap on one GPU race."""
+    import torch
+    B, N, V = _tree_common(target_logits, draft_logits, node_token, parent, u_accept, u_resample,
+                           max_depth)
+    _shape(out_tokens, (B, max_depth + 1), "out_tokens")
+    _shape(out_accepted_len, (B,), "out_accepted_len")
+    if out_status is not None:
+        _shape(out_status, (B,), "out_status")
+    prm = _params(target_logits, temperature, mode, without_replacement, bonus)
+    st = lib.resispec_verify_tree_noalloc(
+        _dev(target_logits, target_logits.dtype, "target_logits"),
+        _dev(draft_logits, target_logits.dtype, "draft_logits"),
+        _dev(node_token, torch.int32, "node_token"), _dev(parent, torch.int32, "parent"),
+        _dev(u_accept, torch.float32, "u_accept"), _dev(u_resample, torch.float32, "u_resample"),
+        B, N, V, int(max_depth), ctypes.byref(prm),
+        _dev(out_tokens, torch.int32, "out_tokens"),
+        _dev(out_accepted_len, torch.int32, "out_accepted_len"),
+        _dev(out_status, torch.int32, "out_status") if out_status is not None else None,
+        _stream(stream))
     _check(st)
     return out_tokens, out_accepted_len, out_status
 
