@@ -331,14 +331,34 @@ def configs_record(native, torch, np, synth, steps, warmup, mode, headline):
     return out
 
 
-def run_study(native, torch, np, synth):
+STUDY_BASE = dict(kind="tree", V=32000, T=1.0, dtype="f32", zipf=1.1, tgt_sigma=1.0, worep=False)
+
+
+def study_configs(B_root=512, B_tree=256):
+    """The workloads of the synthetic studies: a root with 8 i.i.d. candidates (the
+    paper's first figure), trees of similar size and different depth/width (its topology
+    ablation), and depth-3 trees of growing width (its efficiency score)."""
+    base = STUDY_BASE
+    root = dict(base, name="root8", B=B_root, draft=("add", 1.5), tree=("first_child_chain", (8,)))
+    shapes = {"d%db%d" % (d, bw): dict(base, name="d%db%d" % (d, bw), B=B_tree,
+                                       draft=("add_depth", 1.0, 0.25, 4),
+                                       tree=("first_child_chain", (bw,) * d))
+              for d, bw in ((7, 2), (5, 3), (4, 5), (3, 11))}
+    widths = {k: dict(base, name="d3b%d" % k, B=B_tree, draft=("add_depth", 1.0, 0.25, 4),
+                      tree=("first_child_chain", (k,) * 3)) for k in (1, 2, 3, 4, 6, 8)}
+    return root, shapes, widths
+
+
+def run_study(native, torch, np, synth, B_root=512, B_tree=256, n_root=16, n_tree=8, trace=None):
     """Synthetic analogues of the paper's studies on the device path (Zipf+noise rows,
     candidates and uniforms from the device draft step, many trials per workload by
     advancing the Philox offset): acceptance by candidate index at one node (the
     paper's first figure), mean accepted length over tree shapes of similar size (its
     topology ablation), and the marginal gain per extra candidate (its efficiency
-    score).  Not timed; prints one JSON line."""
-    base = dict(kind="tree", V=32000, T=1.0, dtype="f32", zipf=1.1, tgt_sigma=1.0, worep=False)
+    score).  Not timed; returns one JSON-able dict.  trace(kind, mode, w, out), when
+    given, sees every trial's inputs (w: the workload with the device's draws) and
+    outputs (the debug entry's node outcomes for the root study, the walk otherwise)."""
+    root_cfg, shapes, widths = study_configs(B_root, B_tree)
 
     def trials(cfg, n_off, fn):
         w = synth.make_workload(cfg, device="cuda")
@@ -353,15 +373,16 @@ def run_study(native, torch, np, synth):
 
     res = {}
     # 1. acceptance by candidate index: a root with 8 i.i.d. candidates
-    cfg = dict(base, name="root8", B=512, draft=("add", 1.5), tree=("first_child_chain", (8,)))
     for mode in ("resispec", "specinfer"):
         def one(w2):
             d = native.resispec_verify_tree_debug(
                 w2["target"], w2["draft"], w2["node_token"], w2["parent"], w2["u_accept"],
                 w2["u_resample"], temperature=1.0, max_depth=w2["max_depth"], mode=mode)
             torch.cuda.synchronize()
+            if trace:
+                trace("root8", mode, w2, d)
             return d["node_child"][:, 0].cpu().numpy()
-        _, outs = trials(cfg, 16, one)
+        _, outs = trials(root_cfg, n_root, one)
         c = np.concatenate(outs)
         hist = [float(np.mean(c == i + 1)) for i in range(8)]
         res.setdefault("accept_by_candidate_index", {})[mode] = {
@@ -377,6 +398,8 @@ def run_study(native, torch, np, synth):
                     w2["u_resample"], temperature=1.0, max_depth=w2["max_depth"], mode=mode)
                 torch.cuda.synchronize()
                 assert (s.cpu().numpy() == 0).all()
+                if trace:
+                    trace(cfg["name"], mode, w2, {"tokens": t, "accepted_len": l, "status": s})
                 return l.cpu().numpy()
             _, outs = trials(cfg, n_off, one)
             r[mode] = float(np.concatenate(outs).mean())
@@ -384,21 +407,20 @@ def run_study(native, torch, np, synth):
         return r
 
     # 2. tree shapes of similar size: depth d, b candidates per level under the first
-    for d, bw in ((7, 2), (5, 3), (4, 5), (3, 11)):
-        cfg = dict(base, name="d%db%d" % (d, bw), B=256,
-                   draft=("add_depth", 1.0, 0.25, 4), tree=("first_child_chain", (bw,) * d))
-        res.setdefault("mean_accepted_length_by_shape", {})["d%db%d" % (d, bw)] = eal(cfg, 8)
+    for name, cfg in shapes.items():
+        res.setdefault("mean_accepted_length_by_shape", {})[name] = eal(cfg, n_tree)
     # 3. marginal gain per extra candidate at depth 3
-    curve = {}
-    for k in (1, 2, 3, 4, 6, 8):
-        cfg = dict(base, name="d3b%d" % k, B=256, draft=("add_depth", 1.0, 0.25, 4),
-                   tree=("first_child_chain", (k,) * 3))
-        curve[k] = eal(cfg, 8)
+    curve = {k: eal(cfg, n_tree) for k, cfg in widths.items()}
     eta = {}
     for mode in ("resispec", "specinfer"):
         eta[mode] = {str(k): (curve[k][mode] - curve[1][mode]) / (k - 1) for k in curve if k > 1}
     res["mean_accepted_length_by_width_depth3"] = {str(k): v for k, v in curve.items()}
     res["eta_marginal_gain_per_extra_candidate"] = eta
+    res["setup"] = {"V": STUDY_BASE["V"], "logits": STUDY_BASE["dtype"], "T": STUDY_BASE["T"],
+                    "target": "Zipf(%.1f) + N(0, 1)" % STUDY_BASE["zipf"],
+                    "draft": "root8: target + N(0, 1.5^2); trees: target + N(0, (1 + 0.25 depth)^2)",
+                    "root_trials": B_root * n_root, "tree_trials_per_shape": B_tree * n_tree,
+                    "draws": "device draft step, Philox seed 2608, offsets 0..n-1"}
     return res
 
 
