@@ -19,7 +19,8 @@ import numpy as np
 from . import build as _build
 
 _HERE = os.path.dirname(os.path.abspath(__file__))
-_LIB_PATH = os.path.join(_HERE, "liboracle.so")
+# an instrumented build (the sanitizer run of the CPU tests) is picked with this variable
+_LIB_PATH = os.environ.get("RESISPEC_ORACLE_LIBRARY") or os.path.join(_HERE, "liboracle.so")
 
 OK, BAD_TOKEN, ZERO_DRAFT, UNDERFLOW, BAD_TREE, BAD_UNIFORM, DEPTH_EXCEEDED = range(7)
 MODE_RESISPEC, MODE_SPECINFER = 0, 1

@@ -41,10 +41,10 @@ def _spills(report):
     return bad
 
 
-def _compile(srcs, lib, verbose):
+def _compile(srcs, lib, verbose, extra=()):
     tmp = lib + ".tmp%d" % os.getpid()
-    cmd = ([HIPCC] + FLAGS + ["-Rpass-analysis=kernel-resource-usage", "-I",
-                              os.path.join(ROOT, "include"), "-o", tmp] + srcs)
+    cmd = ([HIPCC] + FLAGS + list(extra) + ["-Rpass-analysis=kernel-resource-usage", "-I",
+                                            os.path.join(ROOT, "include"), "-o", tmp] + srcs)
     if verbose:
         print(" ".join(cmd), flush=True)
     r = subprocess.run(cmd, capture_output=True, text=True)
@@ -66,11 +66,29 @@ def _compile(srcs, lib, verbose):
     os.replace(tmp, lib)
 
 
+# Host-side AddressSanitizer + UndefinedBehaviorSanitizer build of the same sources: the
+# argument checks, host validator and size queries run instrumented (every -fsanitize
+# flag is for the host pass only; the device code is built as usual).  Used by the
+# sanitizer run of the CPU tests, never by the GPU path.
+SAN_LIB = os.path.join(HERE, "libresispec_san.so")
+SAN_FLAGS = ["-Xarch_host", "-fsanitize=address", "-Xarch_host", "-fsanitize=undefined",
+             "-Xarch_host", "-fno-sanitize-recover=undefined", "-Xarch_host", "-fno-omit-frame-pointer",
+             "-Xarch_host", "-g"]
+
+
 def build(verbose: bool = False) -> str:
     _compile(SRCS, LIB, verbose)
     _compile(PROBE_SRCS, PROBE_LIB, verbose)
     return LIB
 
 
+def build_sanitized(verbose: bool = False) -> str:
+    _compile(SRCS, SAN_LIB, verbose, extra=SAN_FLAGS)
+    return SAN_LIB
+
+
 if __name__ == "__main__":
-    build(verbose="-v" in sys.argv)
+    if "--sanitize" in sys.argv:
+        build_sanitized(verbose="-v" in sys.argv)
+    else:
+        build(verbose="-v" in sys.argv)

@@ -9,7 +9,8 @@ import ctypes
 import os
 
 HERE = os.path.dirname(os.path.abspath(__file__))
-LIB_PATH = os.path.join(HERE, "libresispec.so")
+# an instrumented build (the sanitizer run of the CPU tests) is picked with this variable
+LIB_PATH = os.environ.get("RESISPEC_LIBRARY") or os.path.join(HERE, "libresispec.so")
 
 RS_OK, RS_ERR_INVALID_ARG, RS_ERR_WORKSPACE, RS_ERR_UNSUPPORTED, RS_ERR_HIP = range(5)
 (RS_SEQ_OK, RS_SEQ_BAD_TOKEN, RS_SEQ_ZERO_DRAFT, RS_SEQ_UNDERFLOW, RS_SEQ_BAD_TREE,
