@@ -197,12 +197,27 @@ __device__ __forceinline__ double wave_sum(double v) {
     return (readlane_d(v, 0) + readlane_d(v, 16)) + (readlane_d(v, 32) + readlane_d(v, 48));
 }
 
-__device__ __forceinline__ double wave_incl_scan(double v, int lane) {
-#pragma unroll
-    for (int o = 1; o < 64; o <<= 1) {
-        const double n = __shfl_up(v, o, 64);
-        if (lane >= o) v += n;
-    }
+// Inclusive prefix sum over the 64 lanes (fp64) with DPP moves: Hillis-Steele steps of
+// 1, 2, 4 and 8 lanes inside each row of 16 lanes, then the last lane of rows 0 and 2
+// added to rows 1 and 3 (row_bcast:15), then the last lane of row 1 added to rows 2 and 3
+// (row_bcast:31).  The additions come in a fixed order, so every call gives the same
+// bits.  Lanes with no source lane add zero.
+template <int CTRL, int ROWMASK>
+__device__ __forceinline__ double dpp_d_or_zero(double v) {
+    const int lo = __builtin_amdgcn_update_dpp(0, __double2loint(v), CTRL, ROWMASK, 0xF, true);
+    const int hi = __builtin_amdgcn_update_dpp(0, __double2hiint(v), CTRL, ROWMASK, 0xF, true);
+    return __hiloint2double(hi, lo);
+}
+constexpr int kDppRowShr1 = 0x111, kDppRowShr2 = 0x112, kDppRowShr4 = 0x114, kDppRowShr8 = 0x118;
+constexpr int kDppRowBcast15 = 0x142, kDppRowBcast31 = 0x143;
+
+__device__ __forceinline__ double wave_incl_scan(double v, int) {
+    v += dpp_d_or_zero<kDppRowShr1, 0xF>(v);
+    v += dpp_d_or_zero<kDppRowShr2, 0xF>(v);
+    v += dpp_d_or_zero<kDppRowShr4, 0xF>(v);
+    v += dpp_d_or_zero<kDppRowShr8, 0xF>(v);
+    v += dpp_d_or_zero<kDppRowBcast15, 0xA>(v);
+    v += dpp_d_or_zero<kDppRowBcast31, 0xC>(v);
     return v;
 }
 

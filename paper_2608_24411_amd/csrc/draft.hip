@@ -48,10 +48,11 @@ struct DParams {
     int32_t G, nslots;
 };
 
-// The draft kernel's shared state: one sum per slot, so 35 KB instead of the
-// verification kernels' 77 KB.  When a row's draws leave one wave running (draws without
-// replacement, or a single child), the other waves' registers and this small LDS let a
-// further row's workgroup start on the CU.
+// The draft kernel's shared state: one fp64 total per slot (the wave that sweeps a slot
+// sums its lanes' partials itself), so about 2 KB instead of the verification kernels'
+// 77 KB.  While a row's draws leave one wave running (draws without replacement, or a
+// single child), the other waves' registers and the small LDS let further rows'
+// workgroups start on the CU and stream.
 struct DraftSmem {
     int32_t decision;
     int32_t next_slot;
@@ -63,7 +64,6 @@ struct DraftSmem {
     float cand_u[kMaxCand];
     float wmax[2][kMaxWaves];
     double slotA[kMaxSlots];
-    float partA[64][kMaxSlots + 1];
 };
 
 template <typename In, int VEC, int UNR>
@@ -170,13 +170,12 @@ __global__ void __launch_bounds__(kBlock) __attribute__((amdgpu_waves_per_eu(4))
                     for (int e = 0; e < VEC; ++e) fa += exp2_fast(expo(t[u][e], c2h, c2l, K));
             },
             [&](int slot) {
-                sm.partA[lane][slot] = fa;
+                // the slot's total: its lanes' partials summed in a fixed order, so the
+                // total does not depend on which wave swept the slot
+                const double v = wave_sum((double)fa);
+                if (lane == 0) sm.slotA[slot] = v;
                 fa = 0.0f;
             });
-        __syncthreads();
-        slot_sums_stage1_one<kBlock>(sm.partA, 0, nslots);
-        __syncthreads();
-        if (tid < nslots) sm.slotA[tid] = slot_group_sum<kBlock>(sm.partA, tid);
         __syncthreads();
         if (wid == 0) {
             double a0 = 0.0;

@@ -514,14 +514,15 @@ __device__ __forceinline__ void verify_row(const KParams& P, Smem& sm, const int
     // Without replacement pass 1 leaves the candidates out of the draft sum (their masses
     // are added in fp64 after it), so every wave needs the candidate list and its slots.
     const bool mask_cands = internal && P.worep;
-    static_assert(kMaxSlots == 128, "four words of candidate slots");
+    static_assert(kMaxSlots % 32 == 0 && kMaxSlots <= 128, "at most four words of candidate slots");
+    constexpr int kSlotWords = kMaxSlots / 32;
     uint32_t cm0 = 0u, cm1 = 0u, cm2 = 0u, cm3 = 0u;
     if (mask_cands) {
         __syncthreads();
         cm0 = __builtin_amdgcn_readfirstlane(sm.cand_slots[0]);
-        cm1 = __builtin_amdgcn_readfirstlane(sm.cand_slots[1]);
-        cm2 = __builtin_amdgcn_readfirstlane(sm.cand_slots[2]);
-        cm3 = __builtin_amdgcn_readfirstlane(sm.cand_slots[3]);
+        if (kSlotWords > 1) cm1 = __builtin_amdgcn_readfirstlane(sm.cand_slots[kSlotWords > 1 ? 1 : 0]);
+        if (kSlotWords > 2) cm2 = __builtin_amdgcn_readfirstlane(sm.cand_slots[kSlotWords > 2 ? 2 : 0]);
+        if (kSlotWords > 3) cm3 = __builtin_amdgcn_readfirstlane(sm.cand_slots[kSlotWords > 3 ? 3 : 0]);
     }
     for (int attempt = 0;; ++attempt) {
         float fa = 0.0f, fc = 0.0f;   // this slot's lane partials

@@ -8,8 +8,8 @@ import torch
 
 import oracle as O
 from paper_2608_24411_amd import synth
-from parity_util import (STATUS_MAP, compare_nodes, compare_walk, gpu_tree, host_tree,
-                         oracle_walk)
+from parity_util import (STATUS_MAP, compare_node_outcomes, compare_nodes, compare_walk,
+                         gpu_tree, host_tree, oracle_nodes, oracle_walk)
 
 pytestmark = pytest.mark.gpu
 MODES = ("resispec", "specinfer")
@@ -420,3 +420,72 @@ def test_max_vocab(gpu_lib):
             t, d, tok, par, ua, ur, temperature=1.0, max_depth=2, mode=mode)
         torch.cuda.synchronize()
         assert torch.equal(t2, gpu["tokens"]) and torch.equal(l2, gpu["accepted_len"])
+
+
+@pytest.mark.parametrize("mode", MODES)
+def test_large_trees(gpu_lib, mode):
+    """Trees of more nodes than a workgroup has threads (700): the row is described
+    directly in shared memory and the candidates' logits gathered by one wave.  Sequence 0
+    has a root with 64 children (the limit) and a random tree below; sequence 1 the same
+    with 65 children under node 2 (that node reports RS_SEQ_TOO_MANY_CHILDREN, 7);
+    sequence 2 a parent that is not topological (every node and the walk report
+    RS_SEQ_BAD_TREE, 4).  All-nodes step and path schedule (one workgroup and row groups)
+    against the oracle and each other."""
+    B, N, V = 3, 700, 3000
+    rng = np.random.default_rng(700)
+    par = np.empty((B, N), np.int32)
+    for b in range(B):
+        par[b, 0] = -1
+        par[b, 1:65] = 0
+        for n in range(65, N):   # below the root's children, at most 64 children each
+            while True:
+                p = int(rng.integers(1, n))
+                if (par[b, :n] == p).sum() < 64:
+                    break
+            par[b, n] = p
+    # sequence 1: node 2 takes 65 children (moved from elsewhere, keeping the order)
+    kids2 = np.flatnonzero(par[1] == 2)
+    extra = [n for n in range(200, N) if par[1, n] != 2][:65 - kids2.size]
+    par[1, extra] = 2
+    assert (par[1] == 2).sum() == 65
+    par[2, 500] = 600
+    g = torch.Generator().manual_seed(5)
+    t = 1.5 * torch.randn((B, N, V), generator=g)
+    d = t + torch.randn((B, N, V), generator=g)
+    tok = torch.zeros((B, N), dtype=torch.int32)
+    for b in range(B):   # children drawn from the parent's draft row
+        q = torch.softmax(d[b], dim=-1)
+        for n in range(1, N):
+            tok[b, n] = int(torch.multinomial(q[par[b, n]], 1, generator=g))
+    w = dict(target=t.cuda(), draft=d.cuda(), node_token=tok.cuda(),
+             parent=torch.as_tensor(par).cuda(), u_accept=torch.rand((B, N), generator=g).cuda(),
+             u_resample=torch.rand((B, N), generator=g).cuda(), temperature=1.0,
+             without_replacement=False, max_depth=N)
+    h = host_tree(w)
+    gpu = gpu_tree(gpu_lib, w, mode, debug=True)
+    gc = gpu["node_child"].cpu().numpy().reshape(-1)
+    gk = gpu["node_token"].cpu().numpy().reshape(-1)
+    gs = gpu["node_status"].cpu().numpy().reshape(-1)
+    # the over-full node, then every other row against the oracle
+    r7 = 1 * N + 2
+    assert gs[r7] == 7 and gc[r7] == -1 and gk[r7] == -1
+    assert (gs[2 * N:3 * N] == 4).all()
+    rows = np.setdiff1d(np.arange(B * N), [r7])
+    orc = oracle_nodes(h, w, mode, rows=rows)
+    summary = compare_node_outcomes(gc[rows], gk[rows], gs[rows], orc, h, w, mode, rows=rows)
+    _log("large trees", mode, summary)
+    # walks: sequence 0 against the oracle; sequence 1 too unless it reaches node 2
+    orc_w = oracle_walk(h, w, mode)
+    st = gpu["status"].cpu().numpy()
+    assert st[2] == 4 and orc_w["status"][2] == O.BAD_TREE
+    excl = np.array([False, st[1] == 7, False])
+    compare_walk(gpu, orc_w, h, w, mode, exclude=excl)
+    # the path schedule returns the same, alone and with row groups
+    plain = gpu_tree(gpu_lib, w, mode)
+    for group in (1, 2, 4):
+        pt, pl, ps = gpu_lib.resispec_verify_tree_path_group(
+            w["target"], w["draft"], w["node_token"], w["parent"], w["u_accept"],
+            w["u_resample"], temperature=1.0, max_depth=N, mode=mode, group_size=group)
+        torch.cuda.synchronize()
+        assert torch.equal(pt, plain["tokens"]) and torch.equal(pl, plain["accepted_len"])
+        assert torch.equal(ps, plain["status"])
