@@ -562,7 +562,7 @@ __device__ __forceinline__ void verify_row(const KParams& P, Smem& sm, const int
                 },
                 flush);
         } else {
-            wave_sweep<In, VEC, UNR, false, 1, kNtLeaf>(tg, dg, V, G, nl, s0, false, pre, pre, &sm.next_slot,
+            wave_sweep<In, VEC, UNR, false, 1, kNtLeaf, true>(tg, dg, V, G, nl, s0, false, pre, pre, &sm.next_slot,
                 [&](const float (&t)[UNR][VEC], const float (&)[UNR][VEC], int, int) {
 #pragma unroll
                     for (int u = 0; u < UNR; ++u)
