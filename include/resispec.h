@@ -69,8 +69,8 @@ typedef enum {
     RS_SEQ_BAD_UNIFORM = 5,      /* a used uniform outside [0, 1) */
     RS_SEQ_DEPTH_EXCEEDED = 6,   /* accepted path longer than max_depth */
     RS_SEQ_TOO_MANY_CHILDREN = 7, /* a node with more than RS_MAX_CANDIDATES children */
-    RS_SEQ_GROUP_TIMEOUT = 8     /* path schedule with row groups: the workgroups of a
-                                    sequence did not meet at a barrier within 20 ms */
+    RS_SEQ_GROUP_TIMEOUT = 8     /* row groups: a workgroup did not receive the others'
+                                    slot totals of a pass within 20 ms */
 } rs_seq_status;
 
 typedef enum { RS_MODE_RESISPEC = 0, RS_MODE_SPECINFER = 1 } rs_mode;
@@ -186,11 +186,12 @@ rs_status resispec_verify_tree_path(const void* target_logits, const void* draft
  * results as resispec_verify_tree_path and resispec_verify_tree, bit for bit). Each
  * sequence gets `group_size` 512-thread workgroups that verify every row of its walk
  * together: each sweeps its share of the row's slots in every pass, and after a pass they
- * exchange their slots' totals through `workspace` and meet at a barrier (a counter in
- * global memory).  The group forms only when all its workgroups have started within 20 us
- * of the first; otherwise the first to give up waiting does the sequence alone (same
- * results).  Every wait is bounded: a formed group whose workgroups do not meet within 20
- * ms at a barrier reports RS_SEQ_GROUP_TIMEOUT.
+ * exchange their slots' totals through `workspace` (64-bit words tagged with the pass, so
+ * a reader waits for the words of the current pass and no fence is needed).  The group
+ * forms only when all its workgroups have started within 20 us of the first; otherwise
+ * the first to give up waiting does the sequence alone (same results).  Every wait is
+ * bounded: a workgroup that does not receive the others' totals within 20 ms reports
+ * RS_SEQ_GROUP_TIMEOUT.
  *   group_size      : 0 = automatic (as many members as the device holds at once, up to
  *                     16 and to one per 8 slots of a row; 1 when that is under 2 or
  *                     workspace is NULL), 1 = one workgroup per sequence,
@@ -198,8 +199,9 @@ rs_status resispec_verify_tree_path(const void* target_logits, const void* draft
  *                     cannot be resident at once or if a row has fewer slots than
  *                     members)
  *   workspace       : device buffer of at least resispec_path_workspace_bytes(B) bytes,
- *                     16-byte aligned, caller-owned; its counters are zeroed by the call
- *                     itself (on `stream`) before the verification kernel; NULL allowed
+ *                     16-byte aligned, caller-owned; its counters and exchange words are
+ *                     zeroed by the call itself (on `stream`) before the verification
+ *                     kernel; NULL allowed
  *                     when group_size is 0 or 1.  Calls that overlap on one workspace race.
  * Other arguments, outputs and statuses as resispec_verify_tree_path.
  */
@@ -216,9 +218,9 @@ rs_status resispec_verify_tree_path_group(const void* target_logits, const void*
  * resispec_verify_tree (Algorithm 1 at every node, §Preliminary walk) with row groups, for
  * batches of few rows (same results, bit for bit): every node row gets `group_size`
  * 512-thread workgroups that verify it together, exchanging slot totals through the
- * workspace at bounded barriers like the path schedule's row groups (a group that does not
+ * workspace with bounded waits like the path schedule's row groups (a group that does not
  * form within 20 us is done by one of its workgroups alone; RS_SEQ_GROUP_TIMEOUT after 20
- * ms at a barrier), then the walk runs as in resispec_verify_tree.
+ * ms without the others' totals), then the walk runs as in resispec_verify_tree.
  *   group_size : 0 = automatic (at most one workgroup per CU for B * N rows, up to 4
  *                members per row, one per 8 slots of a row and one per 64 KiB of a row's
  *                logits; 1 = the ordinary one-workgroup row kernel when that is under 2),
@@ -249,9 +251,10 @@ int32_t resispec_tree_group_size(int32_t B, int32_t N, int32_t V, const rs_param
 
 /* Testing hook: the time limits of row groups in later launches of this process, in
  * ticks of the device's 100 MHz wall clock; UINT64_MAX restores a default.
- *   barrier_ticks   : every barrier of a formed group (default 2,000,000 = 20 ms); a
- *                     small limit makes groups report RS_SEQ_GROUP_TIMEOUT instead of
- *                     waiting, which is how the tests exercise that path
+ *   barrier_ticks   : every wait of a formed group for its members' totals (default
+ *                     2,000,000 = 20 ms); a small limit makes groups report
+ *                     RS_SEQ_GROUP_TIMEOUT instead of waiting, which is how the tests
+ *                     exercise that path
  *   formation_ticks : the wait for a group's workgroups to start (default 2,000 = 20 us);
  *                     0 makes nearly every group fall back to one workgroup
  * Not for concurrent use with launches on other threads.  Always RS_OK. */

@@ -165,26 +165,34 @@ __device__ double scalar_residual(const Smem& sm, int i, double p, double q, int
 // thread 0 once, with the node's outcome.
 // Workgroups that verify one row together (row groups of the path schedule or of the
 // all-nodes schedule, one workgroup per CU): member w of S sweeps slots [w * nslots / S, (w + 1) * nslots / S)
-// in every pass; after a pass the members publish their slots' totals in global memory
-// and meet at a barrier, then all continue from the same totals in the same order, so
-// each decision is taken identically by every member.  S = 1: one workgroup per row.
+// in every pass; after a pass the members exchange their slots' totals through global
+// memory, then all continue from the same totals in the same order, so each decision is
+// taken identically by every member.  S = 1: one workgroup per row.
+//
+// The exchange needs no fence: every value travels in 64-bit atomic words that carry the
+// exchange's number (the same count in every member) in their upper half and 32 bits of
+// the value in the lower half, and a reader waits until each word it needs carries the
+// current number.  Per-location coherence of the atomics is all this relies on, and a
+// member writes exchange e + 2 into the buffer of exchange e only after reading every
+// member's exchange e + 1, which each wrote after reading exchange e: two buffers are
+// enough.
 struct RowGroup {
-    int32_t S, w;      // members, this member
-    uint32_t* ctr;     // arrivals at this sequence's barriers (zero before the launch)
-    double* xbuf;      // [2 (barrier parity)][2 (first sum, second sum)][kMaxSlots]
-    float* xmax;       // [S][2]: the members' maxima of the target and draft rows
-    uint32_t epoch;    // barriers passed so far (the same count in every member)
-    uint64_t wait;     // time limit of one barrier, in ticks of the 100 MHz wall clock
+    int32_t S, w;              // members, this member
+    unsigned long long* xw;    // [2 (parity)][2 (first, second sum)][kMaxSlots][2 (halves)]
+    unsigned long long* xm;    // [2 (parity)][kMaxGroup][2]: the members' maxima of both rows
+    uint32_t epoch;            // exchanges so far (the same count in every member)
+    uint64_t wait;             // time limit of one exchange, in ticks of the 100 MHz wall clock
 };
 
-// per-sequence (or per-row) workspace of a row group: barrier counter, formation
-// arrivals and state (each on its own 64-byte line), slot totals, maxima
-constexpr int64_t kGroupStride = 4608;
+// per-sequence (or per-row) workspace of a row group: formation arrivals and state (each
+// on its own 64-byte line), slot totals, maxima (tagged words, zero before the launch)
+constexpr int32_t kMaxGroup = 16;
 constexpr int64_t kGroupArrive = 64;
 constexpr int64_t kGroupState = 128;
-constexpr int64_t kGroupXbuf = 256;
-constexpr int64_t kGroupXmax = kGroupXbuf + 2 * 2 * kMaxSlots * (int64_t)sizeof(double);
-constexpr int32_t kMaxGroup = 16;
+constexpr int64_t kGroupXw = 256;
+constexpr int64_t kGroupXm = kGroupXw + 2 * 2 * kMaxSlots * 2 * (int64_t)sizeof(unsigned long long);
+constexpr int64_t kGroupWordsEnd = kGroupXm + 2 * kMaxGroup * 2 * (int64_t)sizeof(unsigned long long);
+constexpr int64_t kGroupStride = (kGroupWordsEnd + 255) / 256 * 256;
 constexpr int32_t kAutoRowGroup = 4;   // automatic members per row, all-nodes schedule
 // XCDs of the device, and when groups are placed on one XCD each: groups of at most 8
 // members, at least two groups per XCD (measured: a group that ends up alone on its XCD,
@@ -192,20 +200,52 @@ constexpr int32_t kAutoRowGroup = 4;   // automatic members per row, all-nodes s
 constexpr int64_t kXcds = 8;
 constexpr int32_t kXcdMaxMembers = 8;
 constexpr int64_t kXcdMinGroups = 2 * kXcds;
-static_assert(kGroupXmax + 2 * kMaxGroup * (int64_t)sizeof(float) <= kGroupStride, "group workspace layout");
 
-// Barrier of a row group with a time limit (20 ms of the 100 MHz wall clock unless a
-// test sets another): false if the other members did not arrive in time, so every
+// Time limit of one exchange (20 ms of the 100 MHz wall clock unless a test sets
+// another): a member whose partners have not published in time gives up, so every
 // workgroup ends whatever happens to the others (the row then reports
 // RS_SEQ_GROUP_TIMEOUT).
 constexpr uint64_t kGroupWaitTicks = 2000000ull;
+
+__device__ __forceinline__ void put_tagged(unsigned long long* w, uint32_t tag, uint32_t v) {
+    __hip_atomic_store(w, ((unsigned long long)tag << 32) | v, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+}
+
+// The value of word w once it carries `tag`; false if it does not within `limit` ticks
+// of t0.
+__device__ __forceinline__ bool get_tagged(const unsigned long long* w, uint32_t tag, uint32_t& v, uint64_t t0,
+                                           uint64_t limit) {
+    for (;;) {
+        const unsigned long long x = __hip_atomic_load(w, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+        if ((uint32_t)(x >> 32) == tag) {
+            v = (uint32_t)x;
+            return true;
+        }
+        if ((uint64_t)wall_clock64() - t0 > limit) return false;
+        __builtin_amdgcn_s_sleep(1);
+    }
+}
+
+__device__ __forceinline__ void put_tagged_d(unsigned long long* w, uint32_t tag, double v) {
+    const unsigned long long bits = (unsigned long long)__double_as_longlong(v);
+    put_tagged(w, tag, (uint32_t)bits);
+    put_tagged(w + 1, tag, (uint32_t)(bits >> 32));
+}
+
+__device__ __forceinline__ bool get_tagged_d(const unsigned long long* w, uint32_t tag, double& v, uint64_t t0,
+                                             uint64_t limit) {
+    uint32_t lo = 0, hi = 0;
+    const bool ok = get_tagged(w, tag, lo, t0, limit) && get_tagged(w + 1, tag, hi, t0, limit);
+    v = __longlong_as_double((long long)(((unsigned long long)hi << 32) | lo));
+    return ok;
+}
 
 // Group formation, before a group's first row.  Members are launched as ordinary
 // workgroups, so they need not all be resident at once: each counts its arrival, and
 // the last to arrive marks the group formed.  A member that sees no such mark within
 // the formation limit (20 us unless a test sets another) claims the group's work for
 // itself, and members that find it claimed leave.  The state moves once, from open to
-// formed or claimed: when formed, every member is running and reaches every barrier.
+// formed or claimed: when formed, every member is running and takes part in every exchange.
 // Returns 1 (formed: work as member w of S), 2 (claimed: do all of it alone) or 0
 // (leave).
 constexpr uint32_t kFormOpen = 0u, kFormed = 1u, kFormClaimed = 2u;
@@ -236,37 +276,14 @@ __device__ __forceinline__ int form_group(Smem& sm, const RowGroup& g, char* bas
     }
     __syncthreads();
     const int res = __builtin_amdgcn_readfirstlane(sm.group_ok);
-    __syncthreads();   // group_ok is reused by the barriers
+    __syncthreads();   // every thread has read group_ok
     return res;
-}
-
-__device__ __forceinline__ bool group_barrier(Smem& sm, RowGroup& g) {
-    __syncthreads();
-    ++g.epoch;
-    if (threadIdx.x == 0) {
-        __threadfence();   // this member's published totals before its arrival
-        atomicAdd(g.ctr, 1u);
-        const uint32_t target = g.epoch * (uint32_t)g.S;
-        const uint64_t t0 = (uint64_t)wall_clock64();
-        int ok = 1;
-        while (__hip_atomic_load(g.ctr, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT) < target) {
-            __builtin_amdgcn_s_sleep(2);
-            if ((uint64_t)wall_clock64() - t0 > g.wait) {
-                ok = 0;
-                break;
-            }
-        }
-        __threadfence();   // the other members' totals after their arrivals
-        sm.group_ok = ok;
-    }
-    __syncthreads();
-    return sm.group_ok != 0;
 }
 
 // Slot totals of the pass just swept (this workgroup's slots [s0, s0 + nl)): summed in
 // shared memory, then, in a row group, published and gathered, so that on return
 // slotA / slotB (and slotP if keepP) hold the totals of every slot of the row.
-// False if a group barrier timed out.
+// False if the exchange timed out.
 template <int BLK, bool SPLIT>
 __device__ __forceinline__ bool pass_totals(Smem& sm, RowGroup& grp, int nslots, int s0, int nl,
                                             bool wantB, bool keepP) {
@@ -283,24 +300,26 @@ __device__ __forceinline__ bool pass_totals(Smem& sm, RowGroup& grp, int nslots,
         __syncthreads();
         return true;
     }
-    // the buffer of the coming barrier (parity): no member still reads it, since that
-    // needs the barrier before it, which every member has passed
-    double* xa = grp.xbuf + (size_t)((grp.epoch + 1) & 1u) * 2 * kMaxSlots;
-    double* xb = xa + kMaxSlots;
+    const uint32_t tag = ++grp.epoch;
+    unsigned long long* xa = grp.xw + (size_t)(tag & 1u) * (2 * kMaxSlots * 2);
+    unsigned long long* xb = xa + kMaxSlots * 2;
     if (tid < nl) {
         const int s = s0 + tid;
-        xa[s] = slot_group_sum<BLK>(sm.partA, s);
-        if (wantB) xb[s] = slot_group_sum<BLK>(sm.partB, s);
+        put_tagged_d(xa + 2 * s, tag, slot_group_sum<BLK>(sm.partA, s));
+        if (wantB) put_tagged_d(xb + 2 * s, tag, slot_group_sum<BLK>(sm.partB, s));
     }
-    const bool ok = group_barrier(sm, grp);
+    // every slot's totals, once the member that swept it has published them
+    int ok = 1;
     if (tid < nslots) {
-        const double a = __hip_atomic_load(&xa[tid], __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+        const uint64_t t0 = (uint64_t)wall_clock64();
+        double a = 0.0, bv = 0.0;
+        ok = get_tagged_d(xa + 2 * tid, tag, a, t0, grp.wait) &&
+             (!wantB || get_tagged_d(xb + 2 * tid, tag, bv, t0, grp.wait));
         sm.slotA[tid] = a;
-        sm.slotB[tid] = wantB ? __hip_atomic_load(&xb[tid], __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT) : 0.0;
+        sm.slotB[tid] = bv;
         if (keepP) sm.slotP[tid] = a;
     }
-    __syncthreads();
-    return ok;
+    return __syncthreads_and(ok) != 0;
 }
 
 template <typename In, int VEC, int UNR, int MODE, int BLK, bool SPLIT, typename Emit>
@@ -651,19 +670,31 @@ __device__ __forceinline__ void verify_row(const KParams& P, Smem& sm, const int
                 m1 = fmaxf(m1, sm.wmax[1][w]);
             }
             if (SPLIT && grp.S > 1) {   // the maxima of the whole row, from every member
+                const uint32_t tag = ++grp.epoch;
+                unsigned long long* xm = grp.xm + (size_t)(tag & 1u) * (kMaxGroup * 2);
                 if (tid == 0) {
-                    grp.xmax[2 * grp.w] = m0;
-                    grp.xmax[2 * grp.w + 1] = m1;
+                    put_tagged(xm + 2 * grp.w, tag, __float_as_uint(m0));
+                    put_tagged(xm + 2 * grp.w + 1, tag, __float_as_uint(m1));
                 }
-                if (!group_barrier(sm, grp)) {
+                __syncthreads();   // every thread has read the waves' maxima
+                int ok = 1;
+                if (tid < grp.S) {
+                    const uint64_t t0 = (uint64_t)wall_clock64();
+                    uint32_t v0 = 0, v1 = 0;
+                    ok = get_tagged(xm + 2 * tid, tag, v0, t0, grp.wait) &&
+                         get_tagged(xm + 2 * tid + 1, tag, v1, t0, grp.wait);
+                    sm.wmax[0][tid] = __uint_as_float(v0);
+                    sm.wmax[1][tid] = __uint_as_float(v1);
+                }
+                if (!__syncthreads_and(ok)) {
                     if (tid == 0) emit(-1, -1, RS_SEQ_GROUP_TIMEOUT);
                     zero_residual_row(P, row);
                     return;
                 }
                 m0 = m1 = -FLT_MAX;
                 for (int q = 0; q < grp.S; ++q) {
-                    m0 = fmaxf(m0, __hip_atomic_load(&grp.xmax[2 * q], __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT));
-                    m1 = fmaxf(m1, __hip_atomic_load(&grp.xmax[2 * q + 1], __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT));
+                    m0 = fmaxf(m0, sm.wmax[0][q]);
+                    m1 = fmaxf(m1, sm.wmax[1][q]);
                 }
             }
             Kt = kref(m0, c2h);
@@ -1148,7 +1179,7 @@ __global__ void __launch_bounds__(kBlock) __attribute__((amdgpu_waves_per_eu(4))
         b = g - n * P.B;
         row = (int64_t)b * P.N + n;
     }
-    RowGroup solo{1, 0, nullptr, nullptr, nullptr, 0u, kGroupWaitTicks};
+    RowGroup solo{1, 0, nullptr, nullptr, 0u, kGroupWaitTicks};
     verify_row<In, VEC, UNR, MODE, kBlock, false>(P, sm, row, b, n, [&](int32_t child, int32_t tok, int32_t st) {
         write_outcome(P, row, child, tok, st);
     }, solo);
@@ -1161,7 +1192,7 @@ __global__ void __launch_bounds__(kBlock) __attribute__((amdgpu_waves_per_eu(4))
 struct GroupArgs {
     int32_t S;
     char* ws;
-    uint64_t wait;       // barrier time limit (ticks)
+    uint64_t wait;       // exchange time limit (ticks)
     uint64_t form_wait;  // formation time limit (ticks)
     int32_t groups;      // groups with work (sequences or rows)
     int32_t xcd;         // 1: the XCD layout below
@@ -1170,7 +1201,7 @@ struct GroupArgs {
 // Which group and member a workgroup is.  The dispatcher deals the workgroups of a launch
 // round-robin over the 8 XCDs (workgroup i runs on XCD i % 8), and each XCD has its own
 // L2.  In the XCD layout the S members of group g all run on XCD g % 8, so the traffic
-// of their barriers and exchanges stays within one L2: workgroup i = 8 k + x is member
+// of their exchanges stays within one L2: workgroup i = 8 k + x is member
 // k % S of group x + 8 (k / S).  The grid then holds a multiple of 8 groups, and the
 // workgroups of groups past the last return at once.  Without it, workgroup i is member
 // i % S of group i / S.  Returns false for a padding workgroup.
@@ -1207,16 +1238,15 @@ rs_path_kernel(const KParams P, int32_t max_depth, int32_t* __restrict__ out_tok
     const int32_t S = ga.S;
     int32_t b, member;
     if (!group_of(ga, b, member)) return;
-    RowGroup grp{S, member, nullptr, nullptr, nullptr, 0u, ga.wait};
+    RowGroup grp{S, member, nullptr, nullptr, 0u, ga.wait};
     bool lead = member == 0;
     if (S > 1) {
         char* base = ga.ws + (int64_t)b * kGroupStride;
-        grp.ctr = reinterpret_cast<uint32_t*>(base);
-        grp.xbuf = reinterpret_cast<double*>(base + kGroupXbuf);
-        grp.xmax = reinterpret_cast<float*>(base + kGroupXmax);
+        grp.xw = reinterpret_cast<unsigned long long*>(base + kGroupXw);
+        grp.xm = reinterpret_cast<unsigned long long*>(base + kGroupXm);
         const int form = form_group(sm, grp, base, ga.form_wait);
         if (form == 0) return;   // another member does this sequence's walk alone
-        if (form == 2) {         // this member does it alone: every slot, no barriers
+        if (form == 2) {         // this member does it alone: every slot, no exchanges
             grp.S = 1;
             grp.w = 0;
             lead = true;
@@ -1273,16 +1303,21 @@ rs_path_kernel(const KParams P, int32_t max_depth, int32_t* __restrict__ out_tok
     }
 }
 
-// The arrival counters of the row groups start at zero in every launch (one group state
-// of kGroupStride bytes per sequence or per row).
-__global__ void rs_group_reset(char* __restrict__ ws, int32_t count) {
-    const int64_t b = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;
-    if (b < count) {
-        char* base = ws + b * kGroupStride;
-        *reinterpret_cast<uint32_t*>(base) = 0u;
+// A row group's formation counters and exchange words start at zero in every launch (one
+// group state of kGroupStride bytes per sequence or per row; a block of 256 threads per
+// group).
+constexpr int kResetBlock = 256;
+__global__ void __launch_bounds__(kResetBlock) rs_group_reset(char* __restrict__ ws, int32_t count) {
+    const int64_t g = blockIdx.x;
+    if (g >= count) return;
+    char* base = ws + g * kGroupStride;
+    if (threadIdx.x == 0) {
         *reinterpret_cast<uint32_t*>(base + kGroupArrive) = 0u;
         *reinterpret_cast<uint32_t*>(base + kGroupState) = 0u;
     }
+    unsigned long long* words = reinterpret_cast<unsigned long long*>(base + kGroupXw);
+    constexpr int64_t nwords = (kGroupWordsEnd - kGroupXw) / (int64_t)sizeof(unsigned long long);
+    for (int64_t k = threadIdx.x; k < nwords; k += kResetBlock) words[k] = 0ull;
 }
 
 // All-nodes schedule with row groups, for batches of few rows: S workgroups per node row
@@ -1309,12 +1344,12 @@ rs_rowgroup_kernel(const KParams P, const GroupArgs ga) {
         row = (int64_t)b * P.N + n;
     }
     char* base = ga.ws + (int64_t)g * kGroupStride;
-    RowGroup grp{S, member, reinterpret_cast<uint32_t*>(base), reinterpret_cast<double*>(base + kGroupXbuf),
-                 reinterpret_cast<float*>(base + kGroupXmax), 0u, ga.wait};
+    RowGroup grp{S, member, reinterpret_cast<unsigned long long*>(base + kGroupXw),
+                 reinterpret_cast<unsigned long long*>(base + kGroupXm), 0u, ga.wait};
     bool lead = member == 0;
     const int form = form_group(sm, grp, base, ga.form_wait);
     if (form == 0) return;   // another member does this row alone
-    if (form == 2) {         // this member does it alone: every slot, no barriers
+    if (form == 2) {         // this member does it alone: every slot, no exchanges
         grp.S = 1;
         grp.w = 0;
         lead = true;
@@ -1413,7 +1448,7 @@ int cu_count() {
 }
 
 // Outputs of the path schedule (NULL: all-nodes schedule).
-// time limits of row-group barriers and formation for the next launches (a testing hook
+// time limits of row-group exchanges and formation for the next launches (a testing hook
 // sets them)
 std::atomic<uint64_t> g_group_wait{kGroupWaitTicks};
 std::atomic<uint64_t> g_form_wait{kFormWaitTicks};
@@ -1483,7 +1518,7 @@ hipError_t launch_path_kernel(KParams P, PathOut* path, hipStream_t s) {
     }
     // a row group per sequence: counters zeroed, then the members (which form their
     // groups themselves)
-    hipLaunchKernelGGL(rs_group_reset, dim3((unsigned)((P.B + 255) / 256)), dim3(256), 0, s, path->ws, P.B);
+    hipLaunchKernelGGL(rs_group_reset, dim3((unsigned)P.B), dim3(kResetBlock), 0, s, path->ws, P.B);
     const hipError_t e = hipGetLastError();
     if (e != hipSuccess) return e;
     KParams kp = P;
@@ -1520,7 +1555,7 @@ hipError_t launch_rowgroups(KParams P, int64_t nrows, RowGroupLaunch* rg, hipStr
         if (cap / nrows < smax) smax = cap / nrows;
         if (rg->group == 0) {
             // measured: beyond one workgroup per CU, four members per row or below 64 KiB
-            // of a row per member, the barriers cost more than the split passes save
+            // of a row per member, the exchanges cost more than the split passes save
             if (kAutoRowGroup < smax) smax = kAutoRowGroup;
             const int64_t by_bytes = (int64_t)P.V * (int64_t)sizeof(In) / 65536;
             if (by_bytes < smax) smax = by_bytes;
@@ -1542,8 +1577,7 @@ hipError_t launch_rowgroups(KParams P, int64_t nrows, RowGroupLaunch* rg, hipStr
         hipLaunchKernelGGL((rs_row_kernel<In, VEC, UNR, MODE>), dim3((unsigned)nrows), dim3(kBlock), 0, s, P);
         return hipGetLastError();
     }
-    hipLaunchKernelGGL(rs_group_reset, dim3((unsigned)((nrows + 255) / 256)), dim3(256), 0, s, rg->ws,
-                       (int32_t)nrows);
+    hipLaunchKernelGGL(rs_group_reset, dim3((unsigned)nrows), dim3(kResetBlock), 0, s, rg->ws, (int32_t)nrows);
     const hipError_t e = hipGetLastError();
     if (e != hipSuccess) return e;
     KParams kp = P;

@@ -398,8 +398,9 @@ def resispec_verify_tree_group(target_logits, draft_logits, node_token, parent, 
 
 def resispec_debug_set_group_waits(barrier=None, formation=None) -> None:
     """Testing hook: time limits of row groups in later launches (ticks of the 100 MHz
-    device clock): `barrier` for every barrier of a formed group, `formation` for its
-    workgroups to start.  None restores a default (20 ms, 20 us)."""
+    device clock): `barrier` for every wait of a formed group for its members' slot
+    totals, `formation` for its workgroups to start.  None restores a default (20 ms,
+    20 us)."""
     none = (1 << 64) - 1
     _check(lib.resispec_debug_set_group_waits(
         ctypes.c_uint64(none if barrier is None else int(barrier)),
