@@ -557,7 +557,11 @@ __device__ __forceinline__ void verify_row(const KParams& P, Smem& sm, const int
                     const uint32_t cw = sw == 0 ? cm0 : (sw == 1 ? cm1 : (sw == 2 ? cm2 : cm3));
                     if ((cw >> (slot & 31)) & 1u) {
                         // a slot holding a candidate (without replacement): its draft
-                        // elements are summed without the candidates
+                        // elements are summed without the candidates.  One ballot finds
+                        // the candidates inside this chunk (usually none or one).
+                        const int cstart = idx0 - lane * VEC;
+                        const int32_t my_cand = lane < nc ? sm.cand_tok[lane] : -1;   // lane c: candidate c
+                        const uint64_t hits = __ballot(my_cand >= cstart && my_cand < cstart + CHUNK);
 #pragma unroll
                         for (int u = 0; u < UNR; ++u)
 #pragma unroll
@@ -565,8 +569,8 @@ __device__ __forceinline__ void verify_row(const KParams& P, Smem& sm, const int
                                 fa += exp2_fast(expo(t[u][e], c2h, c2l, Kt));
                                 float q = exp2_fast(expo(d[u][e], c2h, c2l, Kd));
                                 const int j = idx0 + u * 64 * VEC + e;
-                                for (int c = 0; c < nc; ++c)
-                                    if (j == sm.cand_tok[c]) q = 0.0f;
+                                for (uint64_t h = hits; h; h &= h - 1)
+                                    if (j == __builtin_amdgcn_readlane(my_cand, __ffsll((long long)h) - 1)) q = 0.0f;
                                 fc += q;
                             }
                         return;
