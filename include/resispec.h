@@ -193,7 +193,7 @@ rs_status resispec_verify_tree_path(const void* target_logits, const void* draft
  * bounded: a workgroup that does not receive the others' totals within 20 ms reports
  * RS_SEQ_GROUP_TIMEOUT.
  *   group_size      : 0 = automatic (as many members as the device holds at once, up to
- *                     16 and to one per 8 slots of a row; 1 when that is under 2 or
+ *                     16 and to one per 4 slots of a row; 1 when that is under 2 or
  *                     workspace is NULL), 1 = one workgroup per sequence,
  *                     2..16 = that many (RS_ERR_UNSUPPORTED if B * group_size workgroups
  *                     cannot be resident at once or if a row has fewer slots than
@@ -221,9 +221,10 @@ rs_status resispec_verify_tree_path_group(const void* target_logits, const void*
  * workspace with bounded waits like the path schedule's row groups (a group that does not
  * form within 20 us is done by one of its workgroups alone; RS_SEQ_GROUP_TIMEOUT after 20
  * ms without the others' totals), then the walk runs as in resispec_verify_tree.
- *   group_size : 0 = automatic (at most one workgroup per CU for B * N rows, up to 4
- *                members per row, one per 8 slots of a row and one per 64 KiB of a row's
- *                logits; 1 = the ordinary one-workgroup row kernel when that is under 2),
+ *   group_size : 0 = automatic (at most one workgroup per CU for B * N rows, up to 8
+ *                members per row, one per 8 slots of a row and one per 40 KiB of a row's
+ *                logits, none below 160 KiB; 1 = the ordinary one-workgroup row kernel
+ *                when that is under 2),
  *                1 = the ordinary kernel,
  *                2..16 = that many (RS_ERR_UNSUPPORTED if B * N * group_size workgroups
  *                cannot be resident at once or a row has fewer slots than members)

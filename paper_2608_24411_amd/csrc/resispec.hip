@@ -193,7 +193,9 @@ constexpr int64_t kGroupXw = 256;
 constexpr int64_t kGroupXm = kGroupXw + 2 * 2 * kMaxSlots * 2 * (int64_t)sizeof(unsigned long long);
 constexpr int64_t kGroupWordsEnd = kGroupXm + 2 * kMaxGroup * 2 * (int64_t)sizeof(unsigned long long);
 constexpr int64_t kGroupStride = (kGroupWordsEnd + 255) / 256 * 256;
-constexpr int32_t kAutoRowGroup = 4;   // automatic members per row, all-nodes schedule
+constexpr int32_t kAutoRowGroup = 8;       // automatic members per row, all-nodes schedule, at most,
+constexpr int64_t kAutoRowBytes = 40960;   // at least this many bytes of a row's logits each,
+constexpr int64_t kAutoSplitBytes = 163840;   // for rows of at least this many bytes of logits
 // XCDs of the device, and when groups are placed on one XCD each: groups of at most 8
 // members, at least two groups per XCD (measured: a group that ends up alone on its XCD,
 // of 7 or of 15, is slower confined to that XCD's share of the chip)
@@ -1231,6 +1233,7 @@ __device__ __forceinline__ bool group_of(const GroupArgs& ga, int32_t& g, int32_
 // live across every row, so these workgroups take up to 256 registers per lane (two
 // waves per SIMD, one workgroup per CU) and nothing is spilled.
 constexpr int kPathBlock = 512;
+constexpr int kPathAutoSlots = 4;   // automatic path row groups: at least this many slots a member
 
 template <typename In, int VEC, int UNR, int MODE>
 __global__ void __launch_bounds__(kPathBlock) __attribute__((amdgpu_waves_per_eu(2)))
@@ -1497,7 +1500,8 @@ int32_t resolve_group(const KParams& P, const PathOut* path) {
     int64_t smax = (int64_t)kMaxGroup;
     if (cap / P.B < smax) smax = cap / P.B;
     if (path->group == 0) {
-        if (P.nslots / (kPathBlock / 64) < smax) smax = P.nslots / (kPathBlock / 64);
+        // measured: with the tagged exchange, members of 4 slots still gain
+        if (P.nslots / kPathAutoSlots < smax) smax = P.nslots / kPathAutoSlots;
         return smax >= 2 ? (int32_t)smax : 1;
     }
     if (P.nslots < smax) smax = P.nslots;
@@ -1558,10 +1562,12 @@ hipError_t launch_rowgroups(KParams P, int64_t nrows, RowGroupLaunch* rg, hipStr
         int64_t smax = (int64_t)kMaxGroup;
         if (cap / nrows < smax) smax = cap / nrows;
         if (rg->group == 0) {
-            // measured: beyond one workgroup per CU, four members per row or below 64 KiB
-            // of a row per member, the exchanges cost more than the split passes save
+            // measured: beyond one workgroup per CU, eight members per row or below 40 KiB
+            // of a row per member, and for rows under 160 KiB, the exchanges cost more than
+            // the split passes save
             if (kAutoRowGroup < smax) smax = kAutoRowGroup;
-            const int64_t by_bytes = (int64_t)P.V * (int64_t)sizeof(In) / 65536;
+            const int64_t row_bytes = (int64_t)P.V * (int64_t)sizeof(In);
+            const int64_t by_bytes = row_bytes < kAutoSplitBytes ? 1 : row_bytes / kAutoRowBytes;
             if (by_bytes < smax) smax = by_bytes;
             if ((int64_t)cu_count() / nrows < smax) smax = (int64_t)cu_count() / nrows;
             if (P.nslots / (kPathBlock / 64) < smax) smax = P.nslots / (kPathBlock / 64);

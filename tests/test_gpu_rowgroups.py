@@ -140,16 +140,17 @@ def test_row_groups_formation_fallback(gpu_lib):
 
 
 def test_row_groups_automatic_size(gpu_lib):
-    """The automatic size keeps to one workgroup per CU, four members per row and 64 KiB
-    of a row's logits per member (256 CUs): one tree of 33 rows of V = 128,256 bf16 takes
-    3 (250 KiB rows), one of 26 rows of V = 151,936 bf16 takes 4, 21 rows of
-    V = 32,000 fp32 (125 KiB) none, and 60 rows of V = 128,256 fp32 four (256 / 60)."""
+    """The automatic size keeps to one workgroup per CU, eight members per row, 40 KiB of
+    a row's logits per member and rows of at least 160 KiB (256 CUs): one tree of 33 rows
+    of V = 128,256 bf16 takes 6 (250 KiB rows), one of 26 rows of V = 151,936 bf16 takes
+    7, 21 rows of V = 32,000 fp32 (125 KiB) none, and 60 rows of V = 128,256 fp32 four
+    (256 / 60)."""
     cus = torch.cuda.get_device_properties(0).multi_processor_count
     _log("CUs:", cus)
     if cus != 256:
         pytest.skip("the expected sizes assume 256 CUs")
-    assert gpu_lib.resispec_tree_group_size(1, 33, 128256, dtype="bf16") == 3
-    assert gpu_lib.resispec_tree_group_size(1, 26, 151936, dtype="bf16") == 4
+    assert gpu_lib.resispec_tree_group_size(1, 33, 128256, dtype="bf16") == 6
+    assert gpu_lib.resispec_tree_group_size(1, 26, 151936, dtype="bf16") == 7
     assert gpu_lib.resispec_tree_group_size(1, 21, 32000, dtype="f32") == 1
     assert gpu_lib.resispec_tree_group_size(1, 60, 128256, dtype="f32") == 4
     assert gpu_lib.resispec_tree_group_size(2, 60, 128256, dtype="f32") == 2
