@@ -519,7 +519,7 @@ def main():
                  w["u_resample"])
 
         # row groups where the batch leaves CUs free (the group size the library picks)
-        pws = torch.empty(max(1, native.resispec_path_workspace_bytes(B)), dtype=torch.uint8,
+        pws = torch.empty(max(1, native.resispec_path_workspace_bytes(B, V)), dtype=torch.uint8,
                           device="cuda")
         group = native.resispec_path_group_size(B, V, dtype="bf16" if esz == 2 else "f32",
                                                 mode=args.mode)

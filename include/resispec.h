@@ -43,7 +43,7 @@
 extern "C" {
 #endif
 
-#define RESISPEC_ABI_VERSION 1
+#define RESISPEC_ABI_VERSION 2
 
 /* Largest number of candidates (children) one node may have. */
 #define RS_MAX_CANDIDATES 64
@@ -198,11 +198,13 @@ rs_status resispec_verify_tree_path(const void* target_logits, const void* draft
  *                     2..16 = that many (RS_ERR_UNSUPPORTED if B * group_size workgroups
  *                     cannot be resident at once or if a row has fewer slots than
  *                     members)
- *   workspace       : device buffer of at least resispec_path_workspace_bytes(B) bytes,
+ *   workspace       : device buffer of at least resispec_path_workspace_bytes(B, V) bytes,
  *                     16-byte aligned, caller-owned; its counters and exchange words are
  *                     zeroed by the call itself (on `stream`) before the verification
- *                     kernel; NULL allowed
- *                     when group_size is 0 or 1.  Calls that overlap on one workspace race.
+ *                     kernel, and its residual rows need no initial contents; NULL allowed
+ *                     when group_size is 0 or 1 (the later rejection passes then re-derive
+ *                     the residual from the logits: same results).  Calls that overlap on
+ *                     one workspace race.
  * Other arguments, outputs and statuses as resispec_verify_tree_path.
  */
 rs_status resispec_verify_tree_path_group(const void* target_logits, const void* draft_logits,
@@ -261,8 +263,13 @@ int32_t resispec_tree_group_size(int32_t B, int32_t N, int32_t V, const rs_param
  * Not for concurrent use with launches on other threads.  Always RS_OK. */
 rs_status resispec_debug_set_group_waits(uint64_t barrier_ticks, uint64_t formation_ticks);
 
-/* Workspace bytes resispec_verify_tree_path_group needs for B sequences (0 if B <= 0). */
-size_t resispec_path_workspace_bytes(int32_t B);
+/* Workspace bytes resispec_verify_tree_path_group needs for B sequences of V-element rows
+ * (0 if B <= 0, V <= 0 or V > RS_MAX_VOCAB): one row-group state per sequence, then one
+ * fp32 residual row per sequence (V rounded up to a multiple of 1024), in which the
+ * ResiSpec rejection passes after a row's second rejection keep the residual of the
+ * previous pass instead of re-deriving it through the chain of earlier proxies
+ * (Algorithm 1 loop: each rejection updates R from the current R and D). */
+size_t resispec_path_workspace_bytes(int32_t B, int32_t V);
 
 /* The group size resispec_verify_tree_path_group chooses with group_size = 0 for B
  * sequences of V-element rows (16-byte aligned rows assumed), on the current device;

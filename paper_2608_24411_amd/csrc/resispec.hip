@@ -73,6 +73,10 @@ struct KParams {
     int32_t* node_tok;
     int32_t* node_status;
     float* residual_out;
+    // path schedule with a workspace: per-sequence fp32 residual of the running row
+    // (rc_stride floats per sequence), or null
+    float* rcache;
+    int64_t rc_stride;
     int32_t B, N;
     int32_t V;
     float T;
@@ -127,20 +131,24 @@ __device__ __forceinline__ void chain_terms(float R, float Q, int j, const Smem&
     Bv = x0 ? 0.0f : R;
 }
 
-// Scalar chain for the accept test of candidate i (fp64, normalised units).
+// Scalar chain for the accept test of candidate i (fp64, normalised units): R(x) and
+// D(x) of the candidate.  Returned by value (a call, if the compiler keeps one, passes
+// them in registers rather than through a stack slot).
+struct ResDraft {
+    double R, D;
+};
 template <int MODE>
-__device__ double scalar_residual(const Smem& sm, int i, double p, double q, int32_t x,
-                                  bool worep, double& Dout) {
+__device__ ResDraft scalar_residual(const Smem& sm, int i, double p, double q, int32_t x, bool worep) {
     bool removed = false;
     if (worep)
         for (int t = 0; t < i; ++t) removed |= x == sm.st_x[t];
-    Dout = removed ? 0.0 : q * sm.st_ds[i];
+    const double Dout = removed ? 0.0 : q * sm.st_ds[i];
     if (MODE == RS_MODE_SPECINFER) {
         // the standard recurrence max(R - D, 0) / S applied i times equals
         // max(p - C q, 0) / Tot (every factor is positive)
-        if (i == 0) return p;
+        if (i == 0) return {p, Dout};
         const double w = p - sm.st_C[i - 1] * q;
-        return w > 0.0 ? w / sm.st_tot[i - 1] : 0.0;
+        return {w > 0.0 ? w / sm.st_tot[i - 1] : 0.0, Dout};
     }
     double R = p;
     removed = false;
@@ -155,7 +163,7 @@ __device__ double scalar_residual(const Smem& sm, int i, double p, double q, int
         }
         if (worep && x == sm.st_x[t]) removed = true;
     }
-    return R;
+    return {R, Dout};
 }
 
 // ------------------------------------------------------------ row kernel ----
@@ -324,7 +332,106 @@ __device__ __forceinline__ bool pass_totals(Smem& sm, RowGroup& grp, int nslots,
     return __syncthreads_and(ok) != 0;
 }
 
-template <typename In, int VEC, int UNR, int MODE, int BLK, bool SPLIT, typename Emit>
+// Residual cache of the path schedule: one fp32 value per element of a row, at the
+// element's index, in a per-sequence buffer padded to a multiple of kRcPad elements (so
+// every chunk of every layout lies inside it and the 16-byte accesses stay aligned).  A
+// lane reads and writes the same VEC consecutive elements it takes from the logits rows.
+constexpr int64_t kRcPad = 1024;
+
+template <int VEC>
+__device__ __forceinline__ void rc_load(const float* __restrict__ p, float (&v)[VEC]) {
+    if constexpr (VEC % 4 == 0) {
+#pragma unroll
+        for (int k = 0; k < VEC / 4; ++k) {
+            const float4 x = reinterpret_cast<const float4*>(p)[k];
+            v[4 * k] = x.x; v[4 * k + 1] = x.y; v[4 * k + 2] = x.z; v[4 * k + 3] = x.w;
+        }
+    } else {
+#pragma unroll
+        for (int e = 0; e < VEC; ++e) v[e] = p[e];
+    }
+}
+
+template <int VEC>
+__device__ __forceinline__ void rc_store(float* __restrict__ p, const float (&v)[VEC]) {
+    if constexpr (VEC % 4 == 0) {
+#pragma unroll
+        for (int k = 0; k < VEC / 4; ++k)
+            reinterpret_cast<float4*>(p)[k] = make_float4(v[4 * k], v[4 * k + 1], v[4 * k + 2], v[4 * k + 3]);
+    } else {
+#pragma unroll
+        for (int e = 0; e < VEC; ++e) p[e] = v[e];
+    }
+}
+
+// One pass over the draft row and the residual cache, with the slots, chunk order, wave
+// schedule and one-chunk prefetch of wave_sweep (the cache takes the target row's place):
+// body(r, d, idx0, slot) gets the cached residual values (which it may overwrite) and the
+// raw draft words of a chunk, flush(slot) runs after a slot's last chunk.
+template <typename In, int VEC, int UNR, bool NT, typename Body, typename Flush>
+__device__ __forceinline__ void wave_sweep_rc(const float* __restrict__ rc, const In* __restrict__ dg, int V,
+                                              int G, int nslots, int sbase, bool reverse, int* counter,
+                                              Body&& body, Flush&& flush) {
+    using W = Vec<In, VEC>;
+    using raw = typename W::raw;
+    constexpr int CHUNK = 64 * VEC * UNR;
+    const int lane = threadIdx.x & 63;
+    const int wid = threadIdx.x >> 6;
+    const int lane0 = lane * VEC;
+    auto chunk_start = [&](int slot, int j) -> int {
+        return (slot * G + (reverse ? G - 1 - j : j)) * CHUNK;
+    };
+    int slot = wid < nslots ? sbase + (reverse ? nslots - 1 - wid : wid) : -1;
+    if (slot < 0) return;
+    auto take = [&]() -> int {
+        int v = 0;
+        if (lane == 0) v = atomicAdd(counter, 1);
+        v = __builtin_amdgcn_readfirstlane(v);
+        return v < nslots ? sbase + (reverse ? nslots - 1 - v : v) : -1;
+    };
+    int ahead = take();
+    auto advance = [&](int& s, int& j) {
+        if (++j == G) {
+            s = ahead;
+            j = 0;
+            if (s >= 0) ahead = take();
+        }
+    };
+    auto load = [&](int s, int j, float (&r)[UNR][VEC], raw (&d)[UNR]) {
+        const int c0 = chunk_start(s, j) + lane0;
+        const bool full = chunk_start(s, j) + CHUNK <= V;
+#pragma unroll
+        for (int u = 0; u < UNR; ++u) {
+            rc_load<VEC>(rc + c0 + u * 64 * VEC, r[u]);
+            d[u] = full ? W::template load_full<NT>(dg, c0 + u * 64 * VEC) : W::template load<NT>(dg, c0 + u * 64 * VEC, V);
+        }
+    };
+    auto process = [&](float (&r)[UNR][VEC], const raw (&cd)[UNR], int s, int j) {
+        body(r, cd, chunk_start(s, j) + lane0, s);
+        if (j == G - 1) flush(s);
+    };
+    float ar[UNR][VEC], br[UNR][VEC];
+    raw ad[UNR], bd[UNR];
+    int sa = slot, ja = 0;
+    load(sa, ja, ar, ad);
+    for (;;) {
+        int sb = sa, jb = ja;
+        advance(sb, jb);
+        if (sb >= 0) load(sb, jb, br, bd);
+        process(ar, ad, sa, ja);
+        if (sb < 0) break;
+        sa = sb;
+        ja = jb;
+        advance(sa, ja);
+        if (sa >= 0) load(sa, ja, ar, ad);
+        process(br, bd, sb, jb);
+        if (sa < 0) break;
+    }
+}
+
+// RC: the path schedule, whose later ResiSpec rejection passes keep the row's residual
+// in P.rcache when the caller's workspace holds it (see the rejection passes below).
+template <typename In, int VEC, int UNR, int MODE, int BLK, bool SPLIT, bool RC = false, typename Emit>
 __device__ __forceinline__ void verify_row(const KParams& P, Smem& sm, const int64_t row,
                                            const int32_t b, const int32_t n, Emit&& emit,
                                            RowGroup& grp) {
@@ -345,6 +452,7 @@ __device__ __forceinline__ void verify_row(const KParams& P, Smem& sm, const int
 
     const In* __restrict__ tg = reinterpret_cast<const In*>(P.tgt) + row * V;
     const In* __restrict__ dg = reinterpret_cast<const In*>(P.dft) + row * V;
+    float* const rc = (RC && MODE == RS_MODE_RESISPEC && P.rcache) ? P.rcache + (int64_t)b * P.rc_stride : nullptr;
 
     using W = Vec<In, VEC>;
     // This wave's first target chunk is requested before anything else, so its latency
@@ -750,8 +858,8 @@ __device__ __forceinline__ void verify_row(const KParams& P, Smem& sm, const int
                 sm.status = RS_SEQ_BAD_UNIFORM;
                 dec = -2;
             } else {
-                double Dx;
-                const double Rx = scalar_residual<MODE>(sm, i, sm.cand_p[i], sm.cand_q[i], x, worep, Dx);
+                const ResDraft rd = scalar_residual<MODE>(sm, i, sm.cand_p[i], sm.cand_q[i], x, worep);
+                const double Rx = rd.R, Dx = rd.D;
                 if (!(Dx > 0.0)) {
                     sm.status = RS_SEQ_ZERO_DRAFT;
                     dec = -2;
@@ -856,6 +964,74 @@ __device__ __forceinline__ void verify_row(const KParams& P, Smem& sm, const int
                         accA += fa;
                     },
                     flush);
+            } else if (RC && rc) {
+                // Later rejections with the residual cache.  Pass i applies step i - 1 of
+                // the chain to the residual the previous pass left in the cache (pass 1
+                // starts from the target row), stores the result for the next pass when
+                // a candidate is left, and sums as below: one step per element instead of
+                // i, with the same fp32 operations in the same order as the chain, so the
+                // values are bit for bit those of the other schedules.
+                const float kc = sm.st_kc[ii - 1], k1 = sm.st_k1[ii - 1], inv = sm.st_i[ii - 1];
+                const int xp = sm.st_x[ii - 1];
+                const bool keep = ii + 1 < nc;
+                // one load's elements (u) at a time; the sums add them in the chain's order
+                auto step = [&](float (&R)[VEC], const float (&Q)[VEC], int i0, bool hit, float& fa, float& fb) {
+#pragma unroll
+                    for (int e = 0; e < VEC; ++e) R[e] = fminf(fmaf(kc, Q[e], k1 * R[e]), inv * R[e]);
+                    if (hit) {
+#pragma unroll
+                        for (int e = 0; e < VEC; ++e)
+                            if (i0 + e == xp) R[e] = 0.0f;
+                    }
+                    if (keep) rc_store<VEC>(rc + i0, R);
+                    if (hit) {
+#pragma unroll
+                        for (int e = 0; e < VEC; ++e)
+                            if (i0 + e == xi) R[e] = 0.0f;
+                    }
+#pragma unroll
+                    for (int e = 0; e < VEC; ++e) {
+                        fa += fminf(ci * Q[e], R[e]);
+                        fb += R[e];
+                    }
+                };
+                if (ii == 1) {
+                    wave_sweep<In, VEC, UNR, true, 0, kNtRej>(tg, dg, V, G, nl, s0, reverse, pre, pre, &sm.next_slot,
+                        [&](const float (&t)[UNR][VEC], const float (&d)[UNR][VEC], int idx0, int slot) {
+                            const bool hit = slot_hit(slot);
+                            float fa = 0.0f, fb = 0.0f;
+#pragma unroll
+                            for (int u = 0; u < UNR; ++u) {
+                                float R[VEC], Q[VEC];
+#pragma unroll
+                                for (int e = 0; e < VEC; ++e) {
+                                    R[e] = exp2_fast(expo(t[u][e], c2h, c2l, Kt));
+                                    Q[e] = exp2_fast(expo(d[u][e], c2h, c2l, Kd));
+                                }
+                                step(R, Q, idx0 + u * 64 * VEC, hit, fa, fb);
+                            }
+                            accA += fa;
+                            accB += fb;
+                        },
+                        flush);
+                } else {
+                    wave_sweep_rc<In, VEC, UNR, kNtRej>(rc, dg, V, G, nl, s0, reverse, &sm.next_slot,
+                        [&](float (&r)[UNR][VEC], const typename W::raw (&dr)[UNR], int idx0, int slot) {
+                            const bool hit = slot_hit(slot);
+                            float fa = 0.0f, fb = 0.0f;
+#pragma unroll
+                            for (int u = 0; u < UNR; ++u) {
+                                float d[VEC], Q[VEC];
+                                W::unpack(dr[u], d);
+#pragma unroll
+                                for (int e = 0; e < VEC; ++e) Q[e] = exp2_fast(expo(d[e], c2h, c2l, Kd));
+                                step(r[u], Q, idx0 + u * 64 * VEC, hit, fa, fb);
+                            }
+                            accA += fa;
+                            accB += fb;
+                        },
+                        flush);
+                }
             } else {
                 wave_sweep<In, VEC, UNR, true, 0, kNtRej>(tg, dg, V, G, nl, s0, reverse, pre, pre, &sm.next_slot,
                     [&](const float (&t)[UNR][VEC], const float (&d)[UNR][VEC], int idx0, int slot) {
@@ -1004,6 +1180,46 @@ __device__ __forceinline__ void verify_row(const KParams& P, Smem& sm, const int
         if (MODE == RS_MODE_SPECINFER) return A;
         return fmaf(a_last, Bv - A, A);
     };
+    // The same values for VEC consecutive elements from j0: the chain's per-step constants
+    // are read once per step for all of them (each element takes the operations of
+    // final_value, in the same order).
+    auto final_values = [&](const float (&lt)[VEC], const float (&ld)[VEC], int j0, float (&out)[VEC]) {
+        if (!internal || first_only) {
+#pragma unroll
+            for (int e = 0; e < VEC; ++e) out[e] = final_value(lt[e], ld[e], j0 + e);
+            return;
+        }
+        float R[VEC], Q[VEC];
+#pragma unroll
+        for (int e = 0; e < VEC; ++e) {
+            R[e] = exp2_fast(expo(lt[e], c2h, c2l, Kt));
+            Q[e] = exp2_fast(expo(ld[e], c2h, c2l, Kd));
+        }
+        if (MODE == RS_MODE_SPECINFER) {
+            const float ci = sm.st_c[last];
+#pragma unroll
+            for (int e = 0; e < VEC; ++e) out[e] = fmaxf(fmaf(-ci, Q[e], R[e]), 0.0f);
+            return;
+        }
+        for (int t = 0; t < last; ++t) {
+            const float kc = sm.st_kc[t], k1 = sm.st_k1[t], inv = sm.st_i[t];
+            const int32_t xt = sm.st_x[t];
+#pragma unroll
+            for (int e = 0; e < VEC; ++e) {
+                R[e] = fminf(fmaf(kc, Q[e], k1 * R[e]), inv * R[e]);
+                if (j0 + e == xt) R[e] = 0.0f;
+            }
+        }
+        const float ci = sm.st_c[last];
+        const int32_t xl = sm.st_x[last];
+#pragma unroll
+        for (int e = 0; e < VEC; ++e) {
+            const bool at = j0 + e == xl;
+            const float A = at ? 0.0f : fminf(ci * Q[e], R[e]);
+            const float Bv = at ? 0.0f : R[e];
+            out[e] = fmaf(a_last, Bv - A, A);
+        }
+    };
     if (wid == 0) {
         // slot totals in vocabulary order; lane l holds slots 4l .. 4l+3
         double Ts[4];
@@ -1079,10 +1295,16 @@ __device__ __forceinline__ void verify_row(const KParams& P, Smem& sm, const int
                     load_vec<In, VEC>(tg, t0 + c + VEC, V, tn);
                     if (internal) load_vec<In, VEC>(dg, t0 + c + VEC, V, dn);
                 }
+                float vals[VEC];
+                if (!internal) {
+#pragma unroll
+                    for (int e = 0; e < VEC; ++e) dv[e] = 0.0f;
+                }
+                final_values(tv, dv, t0 + c, vals);
 #pragma unroll
                 for (int e = 0; e < VEC; ++e) {
                     const int j = t0 + c + e;
-                    const float v = j < V ? final_value(tv[e], internal ? dv[e] : 0.0f, j) : 0.0f;
+                    const float v = j < V ? vals[e] : 0.0f;
                     if (staged) sm.partA[lane][c + e] = v;
                     own2 += (double)v;
                 }
@@ -1266,7 +1488,7 @@ rs_path_kernel(const KParams P, int32_t max_depth, int32_t* __restrict__ out_tok
         for (int64_t i = tid; i < W; i += kBlock) out[i] = -1;
     int32_t n = 0, len = 0, status = RS_SEQ_OK;
     for (int32_t steps = 0; steps <= N; ++steps) {
-        verify_row<In, VEC, UNR, MODE, kBlock, true>(P, sm, (int64_t)b * N + n, b, n,
+        verify_row<In, VEC, UNR, MODE, kBlock, true, true>(P, sm, (int64_t)b * N + n, b, n,
                                                      [&](int32_t child, int32_t tok, int32_t st) {
             sm.res_child = child;
             sm.res_tok = tok;
@@ -1901,6 +2123,11 @@ int32_t resispec_tree_group_size(int32_t B, int32_t N, int32_t V, const rs_param
     return e == hipSuccess ? rg.used_group : -1;
 }
 
+// Path workspace: one group state per sequence, then the residual cache (rc_stride(V)
+// floats per sequence, starting on a 256-byte boundary).
+static size_t path_states_bytes(int32_t B) { return ((size_t)B * (size_t)kGroupStride + 255) & ~(size_t)255; }
+static int64_t rc_stride(int32_t V) { return ((int64_t)V + kRcPad - 1) / kRcPad * kRcPad; }
+
 static rs_status verify_tree_path_impl(const void* target_logits, const void* draft_logits,
                                        const int32_t* node_token, const int32_t* parent,
                                        const float* u_accept, const float* u_resample, int32_t B,
@@ -1913,12 +2140,17 @@ static rs_status verify_tree_path_impl(const void* target_logits, const void* dr
                                          out_accepted_len);
     if (as != RS_OK) return as;
     if (group_size < 0 || group_size > kMaxGroup) return RS_ERR_INVALID_ARG;
-    if (workspace && (workspace_bytes < resispec_path_workspace_bytes(B) || !aligned16(workspace)))
+    if (workspace && (workspace_bytes < resispec_path_workspace_bytes(B, V) || !aligned16(workspace)))
         return RS_ERR_WORKSPACE;
     if (group_size >= 2 && !workspace) return RS_ERR_WORKSPACE;
     if (B == 0) return RS_OK;
-    const KParams P = tree_params(target_logits, draft_logits, node_token, parent, u_accept,
-                                  u_resample, B, N, V, prm, nullptr, nullptr, nullptr, nullptr);
+    KParams P = tree_params(target_logits, draft_logits, node_token, parent, u_accept,
+                            u_resample, B, N, V, prm, nullptr, nullptr, nullptr, nullptr);
+    if (workspace) {
+        // the residual cache follows the group states
+        P.rcache = reinterpret_cast<float*>(static_cast<char*>(workspace) + path_states_bytes(B));
+        P.rc_stride = rc_stride(V);
+    }
     const bool vec = vector_ok(target_logits, draft_logits, V, prm->logits_dtype);
     PathOut path{max_depth, out_tokens, out_accepted_len, out_status, group_size,
                  static_cast<char*>(workspace), 0, 1, 0};
@@ -1957,9 +2189,9 @@ rs_status resispec_debug_set_group_waits(uint64_t barrier_ticks, uint64_t format
     return RS_OK;
 }
 
-size_t resispec_path_workspace_bytes(int32_t B) {
-    if (B <= 0) return 0;
-    return (size_t)B * (size_t)kGroupStride;
+size_t resispec_path_workspace_bytes(int32_t B, int32_t V) {
+    if (B <= 0 || V <= 0 || V > RS_MAX_VOCAB) return 0;
+    return path_states_bytes(B) + (size_t)B * (size_t)rc_stride(V) * sizeof(float);
 }
 
 int32_t resispec_path_group_size(int32_t B, int32_t V, const rs_params* prm) {

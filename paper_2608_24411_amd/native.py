@@ -65,7 +65,7 @@ def _load():
     lib.resispec_verify_tree_path_group.argtypes = [P, P, P, P, P, P, i32, i32, i32, i32, prm, P,
                                                     P, P, i32, P, sz, P]
     lib.resispec_verify_tree_path_group.restype = i32
-    lib.resispec_path_workspace_bytes.argtypes = [i32]
+    lib.resispec_path_workspace_bytes.argtypes = [i32, i32]
     lib.resispec_path_workspace_bytes.restype = sz
     lib.resispec_path_group_size.argtypes = [i32, i32, prm]
     lib.resispec_path_group_size.restype = i32
@@ -335,8 +335,8 @@ def resispec_verify_tree_path(target_logits, draft_logits, node_token, parent, u
     return out_tokens, out_accepted_len, out_status
 
 
-def resispec_path_workspace_bytes(B: int) -> int:
-    return lib.resispec_path_workspace_bytes(int(B))
+def resispec_path_workspace_bytes(B: int, V: int) -> int:
+    return lib.resispec_path_workspace_bytes(int(B), int(V))
 
 
 def resispec_path_group_size(B: int, V: int, *, dtype, mode="resispec") -> int:
@@ -426,7 +426,7 @@ def resispec_verify_tree_path_group(target_logits, draft_logits, node_token, par
     if out_status is None:
         out_status = torch.empty(B, dtype=torch.int32, device=dev)
     if workspace is None:
-        workspace = torch.empty(max(1, resispec_path_workspace_bytes(B)), dtype=torch.uint8,
+        workspace = torch.empty(max(1, resispec_path_workspace_bytes(B, V)), dtype=torch.uint8,
                                 device=dev)
     _shape(out_tokens, (B, max_depth + 1), "out_tokens")
     _shape(out_accepted_len, (B,), "out_accepted_len")

@@ -20,7 +20,7 @@ int main(void) {
     CHECK(strcmp(resispec_status_string(RS_OK), resispec_status_string(RS_ERR_INVALID_ARG)) != 0);
     CHECK(resispec_workspace_bytes(0, 5) == 0);
     CHECK(resispec_workspace_bytes(4, 33) >= 3 * 4 * 33 * sizeof(int32_t));
-    CHECK(resispec_path_workspace_bytes(8) > 0);
+    CHECK(resispec_path_workspace_bytes(8, 1000) > 0);
 
     /* two trees of five nodes: a valid batch, then a parent that is not earlier */
     int32_t parent[10] = {-1, 0, 0, 1, 1, -1, 0, 1, 2, 3};

@@ -40,7 +40,7 @@ def test_library_exports_every_declared_symbol(native):
 
 
 def test_abi_version_and_status_strings(native):
-    assert native.resispec_abi_version() == 1
+    assert native.resispec_abi_version() == 2
     for code in range(5):
         s = native.resispec_status_string(code)
         assert s.startswith("RS_")
@@ -138,8 +138,11 @@ def test_argument_errors_return_before_launch(native):
                                          ctypes.byref(ok), None, None, None, None) == native.RS_OK
     # path schedule with row groups: group size and workspace are checked before launch
     pg = lib.resispec_verify_tree_path_group
-    pws = native.resispec_path_workspace_bytes(4)
-    assert pws > 0 and native.resispec_path_workspace_bytes(0) == 0
+    pws = native.resispec_path_workspace_bytes(4, 100)
+    assert pws > 0 and native.resispec_path_workspace_bytes(0, 100) == 0
+    assert native.resispec_path_workspace_bytes(4, 0) == 0
+    # one residual row per sequence, padded to 1024 elements, after the group states
+    assert native.resispec_path_workspace_bytes(4, 1025) - pws == 4 * 1024 * 4
     wsp = ctypes.c_void_p(0x10000)
     for g in (-1, 17):
         assert pg(*args, 4, 5, 100, 2, ctypes.byref(ok), i32p, i32p, None, g, wsp, pws,

@@ -94,7 +94,7 @@ def test_graph_path_groups(gpu_lib, mode):
     """The path schedule with row groups: the counter-clearing kernel and the group launch
     are both in the graph."""
     w = synth.make_workload(4, device="cuda", B=3, V=40000)
-    ws = torch.empty(gpu_lib.resispec_path_workspace_bytes(w["B"]), dtype=torch.uint8,
+    ws = torch.empty(gpu_lib.resispec_path_workspace_bytes(w["B"], w["V"]), dtype=torch.uint8,
                      device="cuda")
 
     def step(out):

@@ -144,7 +144,7 @@ def test_path_groups_full_size(gpu_lib):
     one workspace (its counters are reset by every call)."""
     w = synth.make_workload(2, device="cuda")
     B = w["B"]
-    ws = torch.empty(gpu_lib.resispec_path_workspace_bytes(B), dtype=torch.uint8, device="cuda")
+    ws = torch.empty(gpu_lib.resispec_path_workspace_bytes(B, w["V"]), dtype=torch.uint8, device="cuda")
     g = gpu_lib.resispec_path_group_size(B, w["V"], dtype="bf16")
     _log("path group full size, automatic group", g)
     assert g >= 1
