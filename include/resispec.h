@@ -203,8 +203,10 @@ rs_status resispec_verify_tree_path(const void* target_logits, const void* draft
  *                     zeroed by the call itself (on `stream`) before the verification
  *                     kernel, and its residual rows need no initial contents; NULL allowed
  *                     when group_size is 0 or 1 (the later rejection passes then re-derive
- *                     the residual from the logits: same results).  Calls that overlap on
- *                     one workspace race.
+ *                     the residual from the logits: same results; they also do so when B *
+ *                     group_size exceeds the device's compute units, where the cache's
+ *                     traffic costs more than it saves).  Calls that overlap on one
+ *                     workspace race.
  * Other arguments, outputs and statuses as resispec_verify_tree_path.
  */
 rs_status resispec_verify_tree_path_group(const void* target_logits, const void* draft_logits,
@@ -264,11 +266,12 @@ int32_t resispec_tree_group_size(int32_t B, int32_t N, int32_t V, const rs_param
 rs_status resispec_debug_set_group_waits(uint64_t barrier_ticks, uint64_t formation_ticks);
 
 /* Workspace bytes resispec_verify_tree_path_group needs for B sequences of V-element rows
- * (0 if B <= 0, V <= 0 or V > RS_MAX_VOCAB): one row-group state per sequence, then one
- * fp32 residual row per sequence (V rounded up to a multiple of 1024), in which the
- * ResiSpec rejection passes after a row's second rejection keep the residual of the
- * previous pass instead of re-deriving it through the chain of earlier proxies
- * (Algorithm 1 loop: each rejection updates R from the current R and D). */
+ * (0 if B <= 0, V <= 0 or V > RS_MAX_VOCAB): one row-group state per sequence, then two
+ * fp32 rows per sequence (V rounded up to a multiple of 1024 each), in which the ResiSpec
+ * rejection passes after a row's second rejection keep the residual of the previous pass
+ * and the draft's masses instead of re-deriving them from the logits through the chain
+ * of earlier proxies (Algorithm 1 loop: each rejection updates R from the current R and
+ * D). */
 size_t resispec_path_workspace_bytes(int32_t B, int32_t V);
 
 /* The group size resispec_verify_tree_path_group chooses with group_size = 0 for B

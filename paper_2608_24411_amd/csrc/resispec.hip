@@ -221,19 +221,30 @@ __device__ __forceinline__ void put_tagged(unsigned long long* w, uint32_t tag, 
     __hip_atomic_store(w, ((unsigned long long)tag << 32) | v, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
 }
 
-// The value of word w once it carries `tag`; false if it does not within `limit` ticks
-// of t0.
-__device__ __forceinline__ bool get_tagged(const unsigned long long* w, uint32_t tag, uint32_t& v, uint64_t t0,
-                                           uint64_t limit) {
+// The values of words w[0..N) once every one of them carries `tag`; false if they do not
+// within `limit` ticks of t0.  All N loads are in flight together on every poll.
+template <int N>
+__device__ __forceinline__ bool get_tagged_all(const unsigned long long* const (&w)[N], uint32_t tag,
+                                               uint32_t (&v)[N], uint64_t t0, uint64_t limit) {
     for (;;) {
-        const unsigned long long x = __hip_atomic_load(w, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
-        if ((uint32_t)(x >> 32) == tag) {
-            v = (uint32_t)x;
+        unsigned long long x[N];
+#pragma unroll
+        for (int k = 0; k < N; ++k) x[k] = __hip_atomic_load(w[k], __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+        bool all = true;
+#pragma unroll
+        for (int k = 0; k < N; ++k) all = all && (uint32_t)(x[k] >> 32) == tag;
+        if (all) {
+#pragma unroll
+            for (int k = 0; k < N; ++k) v[k] = (uint32_t)x[k];
             return true;
         }
         if ((uint64_t)wall_clock64() - t0 > limit) return false;
         __builtin_amdgcn_s_sleep(1);
     }
+}
+
+__device__ __forceinline__ double join_halves(uint32_t lo, uint32_t hi) {
+    return __longlong_as_double((long long)(((unsigned long long)hi << 32) | lo));
 }
 
 __device__ __forceinline__ void put_tagged_d(unsigned long long* w, uint32_t tag, double v) {
@@ -242,13 +253,6 @@ __device__ __forceinline__ void put_tagged_d(unsigned long long* w, uint32_t tag
     put_tagged(w + 1, tag, (uint32_t)(bits >> 32));
 }
 
-__device__ __forceinline__ bool get_tagged_d(const unsigned long long* w, uint32_t tag, double& v, uint64_t t0,
-                                             uint64_t limit) {
-    uint32_t lo = 0, hi = 0;
-    const bool ok = get_tagged(w, tag, lo, t0, limit) && get_tagged(w + 1, tag, hi, t0, limit);
-    v = __longlong_as_double((long long)(((unsigned long long)hi << 32) | lo));
-    return ok;
-}
 
 // Group formation, before a group's first row.  Members are launched as ordinary
 // workgroups, so they need not all be resident at once: each counts its arrival, and
@@ -318,13 +322,24 @@ __device__ __forceinline__ bool pass_totals(Smem& sm, RowGroup& grp, int nslots,
         put_tagged_d(xa + 2 * s, tag, slot_group_sum<BLK>(sm.partA, s));
         if (wantB) put_tagged_d(xb + 2 * s, tag, slot_group_sum<BLK>(sm.partB, s));
     }
-    // every slot's totals, once the member that swept it has published them
+    // every slot's totals, once the member that swept it has published them (the words
+    // of a slot are polled together)
     int ok = 1;
     if (tid < nslots) {
         const uint64_t t0 = (uint64_t)wall_clock64();
         double a = 0.0, bv = 0.0;
-        ok = get_tagged_d(xa + 2 * tid, tag, a, t0, grp.wait) &&
-             (!wantB || get_tagged_d(xb + 2 * tid, tag, bv, t0, grp.wait));
+        if (wantB) {
+            const unsigned long long* const w[4] = {xa + 2 * tid, xa + 2 * tid + 1, xb + 2 * tid, xb + 2 * tid + 1};
+            uint32_t v[4] = {0u, 0u, 0u, 0u};
+            ok = get_tagged_all<4>(w, tag, v, t0, grp.wait);
+            a = join_halves(v[0], v[1]);
+            bv = join_halves(v[2], v[3]);
+        } else {
+            const unsigned long long* const w[2] = {xa + 2 * tid, xa + 2 * tid + 1};
+            uint32_t v[2] = {0u, 0u};
+            ok = get_tagged_all<2>(w, tag, v, t0, grp.wait);
+            a = join_halves(v[0], v[1]);
+        }
         sm.slotA[tid] = a;
         sm.slotB[tid] = bv;
         if (keepP) sm.slotP[tid] = a;
@@ -332,10 +347,11 @@ __device__ __forceinline__ bool pass_totals(Smem& sm, RowGroup& grp, int nslots,
     return __syncthreads_and(ok) != 0;
 }
 
-// Residual cache of the path schedule: one fp32 value per element of a row, at the
-// element's index, in a per-sequence buffer padded to a multiple of kRcPad elements (so
-// every chunk of every layout lies inside it and the 16-byte accesses stay aligned).  A
-// lane reads and writes the same VEC consecutive elements it takes from the logits rows.
+// Residual cache of the path schedule: two fp32 values per element of a row (the residual
+// and the unnormalised draft mass), each at the element's index in a per-sequence array
+// padded to a multiple of kRcPad elements (so every chunk of every layout lies inside it
+// and the 16-byte accesses stay aligned).  A lane reads and writes the same VEC
+// consecutive elements it takes from the logits rows.
 constexpr int64_t kRcPad = 1024;
 
 template <int VEC>
@@ -364,16 +380,18 @@ __device__ __forceinline__ void rc_store(float* __restrict__ p, const float (&v)
     }
 }
 
-// One pass over the draft row and the residual cache, with the slots, chunk order, wave
-// schedule and one-chunk prefetch of wave_sweep (the cache takes the target row's place):
-// body(r, d, idx0, slot) gets the cached residual values (which it may overwrite) and the
-// raw draft words of a chunk, flush(slot) runs after a slot's last chunk.
-template <typename In, int VEC, int UNR, bool NT, typename Body, typename Flush>
-__device__ __forceinline__ void wave_sweep_rc(const float* __restrict__ rc, const In* __restrict__ dg, int V,
-                                              int G, int nslots, int sbase, bool reverse, int* counter,
-                                              Body&& body, Flush&& flush) {
-    using W = Vec<In, VEC>;
-    using raw = typename W::raw;
+// One pass over the residual cache, with the slots, chunk order and wave schedule of
+// wave_sweep: the residual R and the unnormalised draft mass Q of every element take the
+// logits rows' place.  The sweep works in units of one load per lane and row (a chunk is
+// UNR units) and keeps four unit buffers, so three units are in flight while one is
+// processed; units are processed in the order they are requested.  body(r, q, i0, slot,
+// u) gets R (which it may overwrite) and Q of unit u of a chunk (element e has index
+// i0 + e); chunk_end(slot) runs after a chunk's last unit and flush(slot) after a slot's
+// last chunk.
+template <int VEC, int UNR, typename Body, typename ChunkEnd, typename Flush>
+__device__ __forceinline__ void wave_sweep_rc(const float* __restrict__ rc, const float* __restrict__ qc, int G,
+                                              int nslots, int sbase, bool reverse, int* counter, Body&& body,
+                                              ChunkEnd&& chunk_end, Flush&& flush) {
     constexpr int CHUNK = 64 * VEC * UNR;
     const int lane = threadIdx.x & 63;
     const int wid = threadIdx.x >> 6;
@@ -390,42 +408,59 @@ __device__ __forceinline__ void wave_sweep_rc(const float* __restrict__ rc, cons
         return v < nslots ? sbase + (reverse ? nslots - 1 - v : v) : -1;
     };
     int ahead = take();
-    auto advance = [&](int& s, int& j) {
-        if (++j == G) {
-            s = ahead;
-            j = 0;
-            if (s >= 0) ahead = take();
+    // a unit is (slot, chunk j of the slot, load u of the chunk); slot -1: none left
+    struct Unit {
+        int s, j, u;
+    };
+    auto next = [&](Unit x) -> Unit {
+        if (++x.u < UNR) return x;
+        x.u = 0;
+        if (++x.j < G) return x;
+        x.j = 0;
+        x.s = ahead;
+        if (x.s >= 0) ahead = take();
+        return x;
+    };
+    auto index = [&](const Unit& x) -> int { return chunk_start(x.s, x.j) + lane0 + x.u * 64 * VEC; };
+    auto load = [&](const Unit& x, float (&r)[VEC], float (&q)[VEC]) {
+        const int i0 = index(x);
+        rc_load<VEC>(rc + i0, r);
+        rc_load<VEC>(qc + i0, q);
+    };
+    auto process = [&](float (&r)[VEC], const float (&q)[VEC], const Unit& x) {
+        body(r, q, index(x), x.s, x.u);
+        if (x.u == UNR - 1) {
+            chunk_end(x.s);
+            if (x.j == G - 1) flush(x.s);
         }
     };
-    auto load = [&](int s, int j, float (&r)[UNR][VEC], raw (&d)[UNR]) {
-        const int c0 = chunk_start(s, j) + lane0;
-        const bool full = chunk_start(s, j) + CHUNK <= V;
-#pragma unroll
-        for (int u = 0; u < UNR; ++u) {
-            rc_load<VEC>(rc + c0 + u * 64 * VEC, r[u]);
-            d[u] = full ? W::template load_full<NT>(dg, c0 + u * 64 * VEC) : W::template load<NT>(dg, c0 + u * 64 * VEC, V);
-        }
+    float r0[VEC], r1[VEC], r2[VEC], r3[VEC];
+    float q0[VEC], q1[VEC], q2[VEC], q3[VEC];
+    Unit x0{slot, 0, 0};
+    load(x0, r0, q0);
+    Unit last = x0;
+    auto refill = [&](Unit& x, float (&r)[VEC], float (&q)[VEC]) {
+        if (last.s >= 0) last = next(last);
+        x = last;
+        if (x.s >= 0) load(x, r, q);
     };
-    auto process = [&](float (&r)[UNR][VEC], const raw (&cd)[UNR], int s, int j) {
-        body(r, cd, chunk_start(s, j) + lane0, s);
-        if (j == G - 1) flush(s);
-    };
-    float ar[UNR][VEC], br[UNR][VEC];
-    raw ad[UNR], bd[UNR];
-    int sa = slot, ja = 0;
-    load(sa, ja, ar, ad);
+    Unit x1, x2, x3;
+    refill(x1, r1, q1);
+    refill(x2, r2, q2);
+    refill(x3, r3, q3);
     for (;;) {
-        int sb = sa, jb = ja;
-        advance(sb, jb);
-        if (sb >= 0) load(sb, jb, br, bd);
-        process(ar, ad, sa, ja);
-        if (sb < 0) break;
-        sa = sb;
-        ja = jb;
-        advance(sa, ja);
-        if (sa >= 0) load(sa, ja, ar, ad);
-        process(br, bd, sb, jb);
-        if (sa < 0) break;
+        process(r0, q0, x0);
+        refill(x0, r0, q0);
+        if (x1.s < 0) break;
+        process(r1, q1, x1);
+        refill(x1, r1, q1);
+        if (x2.s < 0) break;
+        process(r2, q2, x2);
+        refill(x2, r2, q2);
+        if (x3.s < 0) break;
+        process(r3, q3, x3);
+        refill(x3, r3, q3);
+        if (x0.s < 0) break;
     }
 }
 
@@ -795,8 +830,11 @@ __device__ __forceinline__ void verify_row(const KParams& P, Smem& sm, const int
                 if (tid < grp.S) {
                     const uint64_t t0 = (uint64_t)wall_clock64();
                     uint32_t v0 = 0, v1 = 0;
-                    ok = get_tagged(xm + 2 * tid, tag, v0, t0, grp.wait) &&
-                         get_tagged(xm + 2 * tid + 1, tag, v1, t0, grp.wait);
+                    const unsigned long long* const wm[2] = {xm + 2 * tid, xm + 2 * tid + 1};
+                    uint32_t vm[2] = {0u, 0u};
+                    ok = get_tagged_all<2>(wm, tag, vm, t0, grp.wait);
+                    v0 = vm[0];
+                    v1 = vm[1];
                     sm.wmax[0][tid] = __uint_as_float(v0);
                     sm.wmax[1][tid] = __uint_as_float(v1);
                 }
@@ -970,10 +1008,13 @@ __device__ __forceinline__ void verify_row(const KParams& P, Smem& sm, const int
                 // starts from the target row), stores the result for the next pass when
                 // a candidate is left, and sums as below: one step per element instead of
                 // i, with the same fp32 operations in the same order as the chain, so the
-                // values are bit for bit those of the other schedules.
+                // values are bit for bit those of the other schedules.  Pass 1 also
+                // stores the draft masses Q, so the later passes read no logits and take
+                // no exponentials.
                 const float kc = sm.st_kc[ii - 1], k1 = sm.st_k1[ii - 1], inv = sm.st_i[ii - 1];
                 const int xp = sm.st_x[ii - 1];
                 const bool keep = ii + 1 < nc;
+                const int64_t rcq = P.rc_stride / 2;   // Q's half of the sequence's cache
                 // one load's elements (u) at a time; the sums add them in the chain's order
                 auto step = [&](float (&R)[VEC], const float (&Q)[VEC], int i0, bool hit, float& fa, float& fb) {
 #pragma unroll
@@ -984,6 +1025,7 @@ __device__ __forceinline__ void verify_row(const KParams& P, Smem& sm, const int
                             if (i0 + e == xp) R[e] = 0.0f;
                     }
                     if (keep) rc_store<VEC>(rc + i0, R);
+                    if (keep && ii == 1) rc_store<VEC>(rc + rcq + i0, Q);
                     if (hit) {
 #pragma unroll
                         for (int e = 0; e < VEC; ++e)
@@ -1015,20 +1057,18 @@ __device__ __forceinline__ void verify_row(const KParams& P, Smem& sm, const int
                         },
                         flush);
                 } else {
-                    wave_sweep_rc<In, VEC, UNR, kNtRej>(rc, dg, V, G, nl, s0, reverse, &sm.next_slot,
-                        [&](float (&r)[UNR][VEC], const typename W::raw (&dr)[UNR], int idx0, int slot) {
-                            const bool hit = slot_hit(slot);
-                            float fa = 0.0f, fb = 0.0f;
-#pragma unroll
-                            for (int u = 0; u < UNR; ++u) {
-                                float d[VEC], Q[VEC];
-                                W::unpack(dr[u], d);
-#pragma unroll
-                                for (int e = 0; e < VEC; ++e) Q[e] = exp2_fast(expo(d[e], c2h, c2l, Kd));
-                                step(r[u], Q, idx0 + u * 64 * VEC, hit, fa, fb);
-                            }
+                    // the chunk's sums run across its units in the order above
+                    float fa = 0.0f, fb = 0.0f;
+                    bool hit = false;   // the chunk's slot holds a rejected token (read at its first unit)
+                    wave_sweep_rc<VEC, UNR>(rc, rc + rcq, G, nl, s0, reverse, &sm.next_slot,
+                        [&](float (&r)[VEC], const float (&q)[VEC], int i0, int slot, int u) {
+                            if (u == 0) hit = slot_hit(slot);
+                            step(r, q, i0, hit, fa, fb);
+                        },
+                        [&](int) {
                             accA += fa;
                             accB += fb;
+                            fa = fb = 0.0f;
                         },
                         flush);
                 }
@@ -1740,6 +1780,11 @@ hipError_t launch_path_kernel(KParams P, PathOut* path, hipStream_t s) {
         return hipErrorInvalidConfiguration;
     }
     if (path->dry_run) return hipSuccess;
+    // The residual cache shortens the long walks, which set the step's time when the
+    // launch leaves CUs free.  With more workgroups than CUs the step is bound by the
+    // device's bandwidth instead, and the cache's extra traffic costs more than it saves
+    // (measured on 1024 serving trees: 0.53 ms without, 0.58 ms with).
+    if ((int64_t)P.B * S > (int64_t)cu_count()) P.rcache = nullptr;
     if (S == 1) {
         hipLaunchKernelGGL((rs_path_kernel<In, VEC, UNR, MODE>), dim3((unsigned)P.B), dim3(kPathBlock), 0, s,
                            P, path->max_depth, path->out_tokens, path->out_len, path->out_status,
@@ -2124,9 +2169,10 @@ int32_t resispec_tree_group_size(int32_t B, int32_t N, int32_t V, const rs_param
 }
 
 // Path workspace: one group state per sequence, then the residual cache (rc_stride(V)
-// floats per sequence, starting on a 256-byte boundary).
+// floats per sequence, starting on a 256-byte boundary: the residual R, then the draft
+// masses Q, each V rounded up to a multiple of kRcPad).
 static size_t path_states_bytes(int32_t B) { return ((size_t)B * (size_t)kGroupStride + 255) & ~(size_t)255; }
-static int64_t rc_stride(int32_t V) { return ((int64_t)V + kRcPad - 1) / kRcPad * kRcPad; }
+static int64_t rc_stride(int32_t V) { return 2 * (((int64_t)V + kRcPad - 1) / kRcPad * kRcPad); }
 
 static rs_status verify_tree_path_impl(const void* target_logits, const void* draft_logits,
                                        const int32_t* node_token, const int32_t* parent,

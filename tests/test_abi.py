@@ -141,8 +141,8 @@ def test_argument_errors_return_before_launch(native):
     pws = native.resispec_path_workspace_bytes(4, 100)
     assert pws > 0 and native.resispec_path_workspace_bytes(0, 100) == 0
     assert native.resispec_path_workspace_bytes(4, 0) == 0
-    # one residual row per sequence, padded to 1024 elements, after the group states
-    assert native.resispec_path_workspace_bytes(4, 1025) - pws == 4 * 1024 * 4
+    # two cache rows per sequence, padded to 1024 elements, after the group states
+    assert native.resispec_path_workspace_bytes(4, 1025) - pws == 4 * 2 * 1024 * 4
     wsp = ctypes.c_void_p(0x10000)
     for g in (-1, 17):
         assert pg(*args, 4, 5, 100, 2, ctypes.byref(ok), i32p, i32p, None, g, wsp, pws,
