@@ -227,6 +227,7 @@ struct Smem {
     int32_t status;
     int32_t decision;     // -1 continue, >= 0 accepted candidate, -2 fault
     int32_t next_slot;    // slot counter of the running sweep
+    int32_t nt_hint;      // pass 1 may stream the rest of the row nontemporally (a cache hint)
     int32_t nc;           // rows with more nodes than threads only
     float ur;
     double St, Sd;        // sums of exp2(l c2 + K)
@@ -386,13 +387,18 @@ __device__ __forceinline__ void load_chunk(const In* __restrict__ tg, const In* 
 // after a slot's last chunk.  reverse: slots in descending order, chunks descending
 // inside a slot.  The sweep covers slots [sbase, sbase + nslots) of the row (a share of
 // them when several workgroups verify one row; the waves' first slots are sbase + w).
+//
+// nt_hint (ordinary loads only, NT = false): a shared flag that a wave reads each time it
+// takes a slot; once it is set, the wave's further loads are nontemporal.  Only the cache
+// policy changes, never the elements or their order.
 template <typename In, int VEC, int UNR, bool PAIR, int PRE, bool NT, bool RING4 = false, typename Body,
           typename Flush>
 __device__ __forceinline__ void wave_sweep(const In* __restrict__ tg, const In* __restrict__ dg,
                                            int V, int G, int nslots, int sbase, bool reverse,
                                            const typename Vec<In, VEC>::raw (&pre_t)[UNR],
                                            const typename Vec<In, VEC>::raw (&pre_d)[UNR],
-                                           int* counter, Body&& body, Flush&& flush) {
+                                           int* counter, Body&& body, Flush&& flush,
+                                           const int32_t* nt_hint = nullptr) {
     using W = Vec<In, VEC>;
     using raw = typename W::raw;
     constexpr int CHUNK = 64 * VEC * UNR;
@@ -406,10 +412,12 @@ __device__ __forceinline__ void wave_sweep(const In* __restrict__ tg, const In* 
     int slot = wid < nslots ? sbase + (reverse ? nslots - 1 - wid : wid) : -1;
     if (slot < 0) return;
     // the counter is read one slot ahead, so its latency overlaps a chunk's work
+    bool nt_now = false;
     auto take = [&]() -> int {
         int v = 0;
         if (lane == 0) v = atomicAdd(counter, 1);
         v = __builtin_amdgcn_readfirstlane(v);
+        if (!NT && nt_hint) nt_now = __builtin_amdgcn_readfirstlane(*nt_hint) != 0;
         return v < nslots ? sbase + (reverse ? nslots - 1 - v : v) : -1;
     };
     int ahead = take();
@@ -421,7 +429,10 @@ __device__ __forceinline__ void wave_sweep(const In* __restrict__ tg, const In* 
         }
     };
     auto load = [&](int s, int j, raw (&t)[UNR], raw (&d)[UNR]) {
-        load_chunk<In, VEC, UNR, PAIR, NT>(tg, dg, chunk_start(s, j), V, t, d);
+        if (!NT && nt_now)
+            load_chunk<In, VEC, UNR, PAIR, true>(tg, dg, chunk_start(s, j), V, t, d);
+        else
+            load_chunk<In, VEC, UNR, PAIR, NT>(tg, dg, chunk_start(s, j), V, t, d);
     };
     auto process = [&](const raw (&ct)[UNR], const raw (&cd)[UNR], int s, int j) {
         float t[UNR][VEC], d[UNR][VEC];

@@ -502,6 +502,7 @@ __device__ __forceinline__ void verify_row(const KParams& P, Smem& sm, const int
     if (tid == 0) {
         sm.decision = -1;
         sm.next_slot = kWaves;
+        sm.nt_hint = 0;
         sm.ur = P.flat ? P.ur_flat[row] : P.ur[row];
     }
     for (int w = tid; w < kMaxSlots / 32; w += kBlock) {
@@ -662,6 +663,11 @@ __device__ __forceinline__ void verify_row(const KParams& P, Smem& sm, const int
         if (hx >= 0 && hx < V) {
             pe = exp2((double)hlt * c2d + (double)Kt);
             qe = exp2((double)hld * c2d + (double)Kd);
+            // Cache hint for pass 1 of a row with one candidate: when the candidate looks
+            // accepted (its test taken with the two rows' sums assumed equal), no
+            // rejection pass is expected to re-read the row, so the waves stream the rest
+            // of it nontemporally.  The results do not depend on it.
+            if (nc == 1 && (double)hu * qe < pe) sm.nt_hint = 1;
         }
         sm.cand_tok[hrank] = hx;
         sm.cand_u[hrank] = hu;
@@ -728,7 +734,7 @@ __device__ __forceinline__ void verify_row(const KParams& P, Smem& sm, const int
                             fc += exp2_fast(expo(d[u][e], c2h, c2l, Kd));
                         }
                 },
-                flush);
+                flush, &sm.nt_hint);
         } else {
             wave_sweep<In, VEC, UNR, false, 1, kNtLeaf, true>(tg, dg, V, G, nl, s0, false, pre, pre, &sm.next_slot,
                 [&](const float (&t)[UNR][VEC], const float (&)[UNR][VEC], int, int) {
