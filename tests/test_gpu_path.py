@@ -7,7 +7,7 @@ import pytest
 import torch
 
 from paper_2608_24411_amd import synth
-from parity_util import compare_walk, gpu_tree, host_tree, oracle_walk
+from parity_util import compare_walk, gpu_tree, host_tree, oracle_nodes, oracle_walk
 
 pytestmark = pytest.mark.gpu
 MODES = ("resispec", "specinfer")
@@ -137,6 +137,65 @@ def test_path_groups_equal_path(gpu_lib, cfg, over, mode):
         same(group_tree(gpu_lib, w, mode, g), ref)
     h = host_tree(w)
     compare_walk(ref, oracle_walk(h, w, mode), h, w, mode)
+
+
+def _chain_workload(V, dtype, worep, seed):
+    """Trees whose walked nodes reject many candidates in a row: a root with 12 children
+    and two nodes with 6, candidates taken where the draft over-weights the target
+    (Gumbel-top-k of d - t), accept uniforms in [0.97, 1), and in sequence b the target
+    row masked (-inf) at its first 3 + b candidates, which are then rejected whatever the
+    residual: the later ResiSpec rejection passes (the ones that read the workspace's
+    residual) run."""
+    g = torch.Generator().manual_seed(seed)
+    par = [-1] + [0] * 12 + [1] * 6 + [13] * 6
+    B, N = 6, len(par)
+    t = 2.0 * torch.randn((B, N, V), generator=g)
+    d = 0.3 * t + 2.0 * torch.randn((B, N, V), generator=g)
+    if dtype == "bf16":
+        t, d = t.to(torch.bfloat16), d.to(torch.bfloat16)
+    parent = torch.tensor(par, dtype=torch.int32).repeat(B, 1)
+    tok = torch.zeros((B, N), dtype=torch.int32)
+    kids_of = {n: [m for m in range(N) if par[m] == n] for n in range(N)}
+    for b in range(B):
+        for n, kids in kids_of.items():
+            if kids:
+                gum = -torch.log(-torch.log(torch.rand(V, generator=g).clamp_(min=1e-20)))
+                pick = torch.topk(d[b, n].float() - t[b, n].float() + gum, len(kids)).indices
+                tok[b, torch.as_tensor(kids)] = pick.to(torch.int32)
+                t[b, n, pick[:3 + b]] = float("-inf")
+    ua = 0.97 + 0.03 * torch.rand((B, N), generator=g)
+    return dict(target=t.cuda(), draft=d.cuda(), node_token=tok.cuda(), parent=parent.cuda(),
+                u_accept=ua.clamp_(max=0.9999).cuda(),
+                u_resample=torch.rand((B, N), generator=g).cuda(), temperature=1.0,
+                without_replacement=worep, max_depth=3), kids_of
+
+
+@pytest.mark.parametrize("worep", [False, True])
+@pytest.mark.parametrize("V,dtype", [(10007, "f32"), (12288, "bf16"), (12289, "bf16")])
+def test_path_residual_cache(gpu_lib, worep, V, dtype):
+    """The workspace's residual rows: the later ResiSpec rejection passes read the
+    residual and draft masses the earlier passes stored instead of re-deriving them from
+    the logits.  One workgroup with the workspace, groups of 2 and 3 and the automatic
+    size give the results of the path without a workspace and of the all-nodes
+    schedule, bit for bit, and the oracle's walk; the walked roots reject at least three
+    candidates in a row, so the stored rows are read."""
+    w, kids_of = _chain_workload(V, dtype, worep, V + 3 * worep)
+    h = host_tree(w)
+    for mode in MODES:
+        _log("residual cache", V, dtype, "worep", worep, mode)
+        ref = path_tree(gpu_lib, w, mode)
+        same(ref, gpu_tree(gpu_lib, w, mode))
+        ws = torch.empty(gpu_lib.resispec_path_workspace_bytes(6, V), dtype=torch.uint8, device="cuda")
+        for g in (1, 2, 3, 0):
+            same(group_tree(gpu_lib, w, mode, g, workspace=ws), ref)
+        orc = oracle_walk(h, w, mode)
+        compare_walk(ref, orc, h, w, mode)
+        # rejections at the walked roots (every walk starts there)
+        nodes = oracle_nodes(h, w, mode, rows=np.arange(6) * len(kids_of))
+        child = nodes["child"]
+        rej = [12 if c < 0 else c - kids_of[0][0] for c in child]
+        _log("  root rejections", rej)
+        assert all(r >= 3 + b for b, r in enumerate(rej)), rej
 
 
 def test_path_groups_full_size(gpu_lib):
