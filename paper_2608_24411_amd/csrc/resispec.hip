@@ -1636,26 +1636,48 @@ rs_rowgroup_kernel(const KParams P, const GroupArgs ga) {
 
 // ----------------------------------------------------------- walk kernel ----
 
-__global__ void rs_walk_kernel(const int32_t* __restrict__ node_child,
-                               const int32_t* __restrict__ node_tok,
-                               const int32_t* __restrict__ node_status,
-                               const int32_t* __restrict__ node_token, int32_t B, int32_t N,
-                               int32_t max_depth, int32_t* __restrict__ out_tokens,
-                               int32_t* __restrict__ out_len, int32_t* __restrict__ out_status) {
-    const int32_t b = blockIdx.x * blockDim.x + threadIdx.x;
-    if (b >= B) return;
+// One wave per sequence.  The walk itself is sequential, so the wave's lanes first load
+// the outcomes of 64 consecutive nodes at once (one round trip instead of one per step);
+// the walk then reads them across lanes, and loads the next 64 when it moves past them
+// (children have larger indices than their parents).  Lane 0 writes the outputs.
+constexpr int kWalkBlock = 256;
+__global__ void __launch_bounds__(kWalkBlock) rs_walk_kernel(const int32_t* __restrict__ node_child,
+                                                             const int32_t* __restrict__ node_tok,
+                                                             const int32_t* __restrict__ node_status,
+                                                             const int32_t* __restrict__ node_token, int32_t B,
+                                                             int32_t N, int32_t max_depth,
+                                                             int32_t* __restrict__ out_tokens,
+                                                             int32_t* __restrict__ out_len,
+                                                             int32_t* __restrict__ out_status) {
+    const int lane = threadIdx.x & 63;
+    const int32_t b = (int32_t)(blockIdx.x * (kWalkBlock / 64) + (threadIdx.x >> 6));
+    if (b >= B) return;   // the whole wave
     const int64_t W = (int64_t)max_depth + 1;
     int32_t* out = out_tokens + (int64_t)b * W;
     const int64_t base = (int64_t)b * N;
-    for (int64_t i = 0; i < W; ++i) out[i] = -1;
+    int32_t wbase = 0, wc = -1, wt = -1, ws = RS_SEQ_OK, wk = -1;
+    auto window = [&](int32_t nb) {
+        wbase = nb;
+        const int32_t m = nb + lane;
+        const bool in = m < N;
+        wc = in ? node_child[base + m] : -1;
+        wt = in ? node_tok[base + m] : -1;
+        ws = in ? node_status[base + m] : RS_SEQ_OK;
+        wk = in ? node_token[base + m] : -1;
+    };
+    window(0);
+    if (lane == 0)
+        for (int64_t i = 0; i < W; ++i) out[i] = -1;
     int32_t n = 0, len = 0, status = RS_SEQ_OK;
     for (int32_t steps = 0; steps <= N; ++steps) {
-        const int32_t st = node_status[base + n];
+        if (n - wbase >= 64) window(n);
+        const int k = n - wbase;
+        const int32_t st = __builtin_amdgcn_readlane(ws, k);
         if (st != RS_SEQ_OK) {
             status = st;
             break;
         }
-        const int32_t c = node_child[base + n];
+        const int32_t c = __builtin_amdgcn_readlane(wc, k);
         if (c >= 0) {
             if (c <= n || c >= N) {
                 status = RS_SEQ_BAD_TREE;
@@ -1665,14 +1687,18 @@ __global__ void rs_walk_kernel(const int32_t* __restrict__ node_child,
                 status = RS_SEQ_DEPTH_EXCEEDED;
                 break;
             }
-            out[len++] = node_token[base + c];
+            if (c - wbase >= 64) window(c);
+            const int32_t tk = __builtin_amdgcn_readlane(wk, c - wbase);
+            if (lane == 0) out[len] = tk;
+            ++len;
             n = c;
             continue;
         }
-        const int32_t t = node_tok[base + n];
-        if (t >= 0) out[len] = t;
+        const int32_t t = __builtin_amdgcn_readlane(wt, k);
+        if (t >= 0 && lane == 0) out[len] = t;
         break;
     }
+    if (lane != 0) return;
     if (status != RS_SEQ_OK) {
         for (int64_t i = 0; i < W; ++i) out[i] = -1;
         len = -1;
@@ -1687,7 +1713,6 @@ __global__ void rs_walk_kernel(const int32_t* __restrict__ node_child,
 
 namespace {
 
-constexpr int kWalkBlock = 256;
 
 // compute units of the current device (queried once per device)
 // Workgroups of kPathBlock threads of kernel K that one CU holds at once, per device
@@ -1933,7 +1958,8 @@ hipError_t launch_walk(const int32_t* node_child, const int32_t* node_tok,
                        const int32_t* node_status, const int32_t* node_token, int32_t B, int32_t N,
                        int32_t max_depth, int32_t* out_tokens, int32_t* out_len,
                        int32_t* out_status, hipStream_t s) {
-    hipLaunchKernelGGL(rs_walk_kernel, dim3((unsigned)((B + kWalkBlock - 1) / kWalkBlock)),
+    constexpr int per_block = kWalkBlock / 64;   // one wave per sequence
+    hipLaunchKernelGGL(rs_walk_kernel, dim3((unsigned)((B + per_block - 1) / per_block)),
                        dim3(kWalkBlock), 0, s, node_child, node_tok, node_status, node_token, B, N,
                        max_depth, out_tokens, out_len, out_status);
     return hipGetLastError();
