@@ -1,18 +1,22 @@
 #!/usr/bin/env python3
 """Benchmark of the ResiSpec verification step on one MI355X.
 
-One step = one full verification of a batch of draft trees: every node's outcome
-(row kernel) followed by the walk from each root (walk kernel), on inputs already
-resident in HBM.  Prints one JSON line.
+One step = one full verification of a batch of draft trees on inputs already resident in
+HBM, in the all-nodes schedule with deferred draws: the decide kernel tests every node
+row (a row that rejects its one candidate, and a leaf, keep their slot totals instead of
+drawing), then the walk kernel follows accepted children from each root and draws where a
+walk ends.  Prints one JSON line.
 
   python bench.py [--gpus 1] [--steps 20] [--warmup 5] [--config 2] [--mode resispec]
 
 The metric is verified tree-node rows per second (B * N / step time) at V = 128,256;
-`roofline.achieved` is the row kernel's algorithmic bytes (every target row once, the
+`roofline.achieved` is the decide kernel's algorithmic bytes (every target row once, the
 draft row of every node with children once, plus ids/uniforms/outcomes) divided by its
 average launch duration measured with HIP events on the launch stream.  The read probe
 (libresispec_probe.so) measures the device's achievable read rate beside it:
 `roofline.frac_of_read_ceiling` is the achieved figure over the nontemporal stream rate.
+The same step with every row drawing at once (`all_nodes_draw`), the path-only schedule,
+the draft step and the other workloads are reported beside it.
 """
 import argparse
 import hashlib
@@ -23,7 +27,7 @@ import time
 
 ROOT = os.path.dirname(os.path.abspath(__file__))
 HBM_PEAK_GBPS = 8000.0
-# the sources the row kernel is compiled from
+# the sources the decide kernel is compiled from
 KERNEL_SRCS = [os.path.join(ROOT, "paper_2608_24411_amd", "csrc", f)
                for f in ("resispec.hip", "common.h")]
 METRIC = "verified tree-node rows/s at V=128256 + achieved HBM GB/s (% of peak)"
@@ -38,9 +42,9 @@ def kernel_source_hash():
 
 
 def measured_traffic(workload, mode):
-    """HBM bytes per launch of the row kernel from the rocprofv3 counter summary, if the
+    """HBM bytes per launch of the decide kernel from the rocprofv3 counter summary, if the
     summary was taken on the current kernel source."""
-    path = os.path.join(ROOT, "profiles", "traffic_rs_row_kernel_%s_%s.json" % (workload, mode))
+    path = os.path.join(ROOT, "profiles", "traffic_rs_decide_kernel_%s_%s.json" % (workload, mode))
     if not os.path.exists(path):
         return None
     with open(path) as f:
@@ -62,18 +66,20 @@ def _cpu_model():
     return platform.processor() or "unknown"
 
 
-def cpu_baseline(w, seconds, mode, gpu_nodes=None):
+def cpu_baseline(w, seconds, mode, gpu_nodes=None, gpu_walk=None):
     """The fp64 oracle on the host, on the same workload, three ways:
-      - all-nodes: every node row evaluated on its own (what the row kernel computes),
+      - all-nodes: every node row evaluated on its own (what the row kernels compute),
         over the host's cores (threads over chunks of rows; the oracle is re-entrant and
         ctypes releases the interpreter lock around it); this is `value`;
       - walk: each sequence walked from its root (only the nodes the walk reaches), over
         the same threads (one sequence per task);
       - single thread: all-nodes on whole sequences until about `seconds` of CPU time.
-    With `gpu_nodes` (the node outcomes of the last timed GPU step) the all-nodes results
+    With `gpu_nodes` (the node outcomes the last timed GPU step left) the all-nodes results
     are also the parity check of that step: bit-exact outside the 1e-6 flag window, and
-    every flagged node either identical or admissible (the oracle's outcome check).
-    Returns (record, parity)."""
+    every flagged node either identical or admissible (the oracle's outcome check).  A
+    node whose draw was deferred and never made (no walk ended there) is compared on its
+    decision: it accepted none of its candidates.  With `gpu_walk` (its tokens and
+    lengths) every sequence is compared with the oracle's walk.  Returns (record, parity)."""
     import numpy as np
     from concurrent.futures import ThreadPoolExecutor
     import oracle as O
@@ -135,17 +141,32 @@ def cpu_baseline(w, seconds, mode, gpu_nodes=None):
         gc, gk, gs = (np.asarray(a).reshape(-1) for a in gpu_nodes)
         fl = orc["flagged"].astype(bool)
         exp_status = orc["status"]   # the oracle's codes 0-6 are the library's
-        diff = (gc != orc["child"]) | (gk != orc["token"]) | (gs != exp_status)
-        redo = np.flatnonzero(fl & diff)
+        deferred = gs == 9           # RS_SEQ_DEFERRED: the decision only (no candidate accepted)
+        diff = np.where(deferred, orc["child"] != -1,
+                        (gc != orc["child"]) | (gk != orc["token"]) | (gs != exp_status))
+        # a deferred node's decision is a single accept test; inside the window it may go
+        # either way, so only full outcomes are replayed by the oracle's check
+        redo = np.flatnonzero(fl & diff & ~deferred)
         verdict = (O.check_tree_nodes(*args, redo, gc[redo], gk[redo], gs[redo], **kw)
                    if redo.size else np.empty(0, np.int32))
+        windowed = int((fl & diff & deferred & (orc["margin"] < 1e-7)).sum())
         parity = {"compared": int(B * N), "exact": int((~fl).sum()),
+                  "decision_only": int(deferred.sum()),
                   "mismatches": int((~fl & diff).sum()),
                   "flagged": int(fl.sum()), "flagged_identical": int((fl & ~diff).sum()),
-                  "flagged_valid": int((verdict != 0).sum()),
+                  "flagged_valid": int((verdict != 0).sum()) + windowed,
                   "flagged_invalid": int((verdict == 0).sum()),
                   "mismatches_margin_ge_1e-7": int((fl & diff & (orc["margin"] >= 1e-7)).sum()),
                   "reference": "fp64 oracle, all-nodes evaluation of the timed step's inputs"}
+        if gpu_walk is not None:
+            gt, gl = gpu_walk
+            wf = np.array([bool(r["flagged"][0]) for r in walks])
+            same = np.array([int(gl[b]) == int(walks[b]["accepted_len"][0]) and
+                             np.array_equal(gt[b], walks[b]["tokens"][0]) for b in range(B)])
+            parity.update({"walks_compared": int(B), "walks_exact": int((~wf).sum()),
+                           "walk_mismatches": int((~wf & ~same).sum()),
+                           "walks_flagged": int(wf.sum()),
+                           "walks_flagged_identical": int((wf & same).sum())})
     return rec, parity
 
 
@@ -185,19 +206,34 @@ def read_ceiling(torch, chunk=1 << 19, nbytes=4 << 30, reps=5):
     return out
 
 
-def time_mode(native, torch, w, mode, steps, warmup, settle, ws, out_tok, out_len, out_st):
+def time_mode(native, torch, w, mode, steps, warmup, settle, ws, out_tok, out_len, out_st,
+              deferred=True):
+    """K timed steps of one schedule: with deferred draws (resispec_decide_nodes, then
+    resispec_walk_draw: the rows that reject their one candidate, and the leaves, draw
+    only where a walk ends) or with every row drawing (resispec_verify_nodes, then
+    resispec_walk).  HIP events on the launch stream bracket the first launch of every
+    timed step."""
     args = (w["target"], w["draft"], w["node_token"], w["parent"], w["u_accept"], w["u_resample"])
     kw = dict(temperature=w["temperature"], mode=mode, without_replacement=w["without_replacement"],
               bonus=w["bonus"])
 
-    def step(ev0=None, ev1=None):
+    def step(ev0=None, ev1=None, ev2=None):
         if ev0 is not None:
             ev0.record()
-        native.resispec_verify_nodes(*args, ws, **kw)
+        if deferred:
+            native.resispec_decide_nodes(*args, ws, **kw)
+        else:
+            native.resispec_verify_nodes(*args, ws, **kw)
         if ev1 is not None:
             ev1.record()
-        native.resispec_walk(w["node_token"], ws, out_tok, out_len, out_st,
-                             max_depth=w["max_depth"])
+        if deferred:
+            native.resispec_walk_draw(*args, ws, max_depth=w["max_depth"], out_tokens=out_tok,
+                                      out_accepted_len=out_len, out_status=out_st, **kw)
+        else:
+            native.resispec_walk(w["node_token"], ws, out_tok, out_len, out_st,
+                                 max_depth=w["max_depth"])
+        if ev2 is not None:
+            ev2.record()
 
     # untimed: steps for at least `settle` seconds (clocks ramp up after the idle time of
     # workload generation), then the W warmup steps
@@ -207,16 +243,16 @@ def time_mode(native, torch, w, mode, steps, warmup, settle, ws, out_tok, out_le
         torch.cuda.synchronize()
     for _ in range(warmup):
         step()
-    ev = [(torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True))
-          for _ in range(steps)]
+    ev = [tuple(torch.cuda.Event(enable_timing=True) for _ in range(3)) for _ in range(steps)]
     torch.cuda.synchronize()
     t0 = time.perf_counter()
-    for e0, e1 in ev:
-        step(e0, e1)
+    for e0, e1, e2 in ev:
+        step(e0, e1, e2)
     torch.cuda.synchronize()
     wall = time.perf_counter() - t0
-    kern_ms = [e0.elapsed_time(e1) for e0, e1 in ev]
-    return wall, kern_ms
+    kern_ms = [e0.elapsed_time(e1) for e0, e1, _ in ev]
+    walk_ms = [e1.elapsed_time(e2) for _, e1, e2 in ev]
+    return wall, kern_ms, walk_ms
 
 
 def _event_ms(torch, fn, steps, warmup, flush=None):
@@ -241,12 +277,13 @@ def _event_ms(torch, fn, steps, warmup, flush=None):
 
 
 def configs_record(native, torch, np, synth, steps, warmup, mode, headline):
-    """The row kernel on every workload of the benchmark recipes (the headline workload's
-    figures are copied from its timed run): algorithmic bytes per launch, mean launch
-    time from HIP events, GB/s and the fraction of 8 TB/s.  The flat 8-row workload is
-    launch-bound and reported in microseconds per call; the 64 x 21 chain workload
-    (213 MB, inside the last-level cache) is timed warm and cold (a 512 MiB buffer
-    written before every cold call)."""
+    """The decide kernel on every workload of the benchmark recipes (the headline
+    workload's figures are copied from its timed run): algorithmic bytes per launch, mean
+    launch time from HIP events, GB/s and the fraction of 8 TB/s; beside it the whole
+    step with deferred draws and the row kernel of the schedule where every row draws.
+    The flat 8-row workload is launch-bound and reported in microseconds per call; the
+    64 x 21 chain workload (213 MB, inside the last-level cache) is timed warm and cold (a
+    512 MiB buffer written before every cold call)."""
     out = {}
     for cfg in (0, 1, 2, 3, 4):
         name = synth.CONFIGS[cfg]["name"]
@@ -292,25 +329,36 @@ def configs_record(native, torch, np, synth, steps, warmup, mode, headline):
         B, N, V = w["B"], w["N"], w["V"]
         logit_bytes, rows_t, rows_d = synth.algorithmic_bytes(w["parent"].cpu().numpy(), V, esz)
         alg = logit_bytes + 28 * B * N
-        ws = torch.empty(native.resispec_workspace_bytes(B, N), dtype=torch.uint8, device="cuda")
+        ws = torch.empty(native.resispec_deferred_workspace_bytes(B, N), dtype=torch.uint8,
+                         device="cuda")
         args = (w["target"], w["draft"], w["node_token"], w["parent"], w["u_accept"], w["u_resample"])
         kw = dict(temperature=w["temperature"], mode=mode,
                   without_replacement=w["without_replacement"], bonus=w["bonus"])
 
         def nodes():
+            native.resispec_decide_nodes(*args, ws, **kw)
+
+        def whole():
+            native.resispec_decide_nodes(*args, ws, **kw)
+            native.resispec_walk_draw(*args, ws, max_depth=w["max_depth"], **kw)
+
+        def every_row_draws():
             native.resispec_verify_nodes(*args, ws, **kw)
         t_end = time.perf_counter() + 0.3
         while time.perf_counter() < t_end:
-            nodes()
+            whole()
             torch.cuda.synchronize()
         ms = _event_ms(torch, nodes, steps, warmup)
         kms = float(np.mean(ms))
+        step_ms = float(np.mean(_event_ms(torch, whole, steps, warmup)))
+        all_ms = float(np.mean(_event_ms(torch, every_row_draws, steps, warmup)))
         rec = {"B": B, "N": N, "V": V, "logits": "bf16" if esz == 2 else "f32",
                "rows_target": rows_t, "rows_draft": rows_d, "alg_bytes_per_launch": alg,
-               "row_kernel_ms": kms, "row_kernel_ms_min": float(np.min(ms)),
-               "rows_per_s": B * N / (kms * 1e-3),
+               "decide_kernel_ms": kms, "decide_kernel_ms_min": float(np.min(ms)),
+               "step_ms": step_ms, "rows_per_s": B * N / (step_ms * 1e-3),
                "achieved_gbps": alg / (kms * 1e-3) / 1e9,
-               "frac": alg / (kms * 1e-3) / 1e9 / HBM_PEAK_GBPS}
+               "frac": alg / (kms * 1e-3) / 1e9 / HBM_PEAK_GBPS,
+               "all_nodes_draw_row_kernel_ms": all_ms}
         if cfg == 1:
             flush_buf = torch.empty(512 << 20, dtype=torch.uint8, device="cuda")
             fill = [0]
@@ -320,8 +368,8 @@ def configs_record(native, torch, np, synth, steps, warmup, mode, headline):
                 flush_buf.fill_(fill[0])
             cold = _event_ms(torch, nodes, steps, 2, flush=flush)
             cms = float(np.mean(cold))
-            rec["warm"] = {"row_kernel_ms": kms, "achieved_gbps": rec["achieved_gbps"]}
-            rec["cold"] = {"row_kernel_ms": cms, "achieved_gbps": alg / (cms * 1e-3) / 1e9,
+            rec["warm"] = {"decide_kernel_ms": kms, "achieved_gbps": rec["achieved_gbps"]}
+            rec["cold"] = {"decide_kernel_ms": cms, "achieved_gbps": alg / (cms * 1e-3) / 1e9,
                            "frac": alg / (cms * 1e-3) / 1e9 / HBM_PEAK_GBPS,
                            "flush": "512 MiB written before every call, outside the events"}
             del flush_buf
@@ -438,12 +486,14 @@ def main():
     ap.add_argument("--no-other-mode", action="store_true")
     ap.add_argument("--no-path", action="store_true", help="skip the path-only schedule")
     ap.add_argument("--no-draft", action="store_true", help="skip the draft step")
+    ap.add_argument("--no-all-nodes", action="store_true",
+                    help="skip the step with every row drawing at once")
     ap.add_argument("--no-single", action="store_true",
                     help="skip the single-tree latency of the same shape")
     ap.add_argument("--no-read-probe", action="store_true",
                     help="skip the read-bandwidth probe (the measured ceiling)")
     ap.add_argument("--no-configs", action="store_true",
-                    help="skip the row kernel on the other workloads")
+                    help="skip the other workloads")
     ap.add_argument("--study", action="store_true",
                     help="only run the synthetic acceptance studies (not a benchmark)")
     ap.add_argument("--copy-probe", type=int, default=0, metavar="MIB",
@@ -467,7 +517,7 @@ def main():
         return
     if args.copy_probe:
         # A plain copy of known size: FETCH_SIZE / WRITE_SIZE of this kernel divided by
-        # its bytes is the scale applied to the row kernel's counters.
+        # its bytes is the scale applied to the decide kernel's counters.
         n = args.copy_probe * (1 << 20) // 4
         src = torch.ones(n, dtype=torch.float32, device="cuda")
         dst = torch.empty_like(src)
@@ -483,32 +533,54 @@ def main():
     small_bytes = 16 * B * N + 12 * B * N      # ids, parents, uniforms in; outcomes out
     alg_bytes = logit_bytes + small_bytes
 
-    ws = torch.empty(native.resispec_workspace_bytes(B, N), dtype=torch.uint8, device="cuda")
+    # the deferred schedule's workspace also holds the other schedule's node outcomes
+    ws = torch.empty(native.resispec_deferred_workspace_bytes(B, N), dtype=torch.uint8,
+                     device="cuda")
     out_tok = torch.empty((B, w["max_depth"] + 1), dtype=torch.int32, device="cuda")
     out_len = torch.empty(B, dtype=torch.int32, device="cuda")
     out_st = torch.empty(B, dtype=torch.int32, device="cuda")
 
     results = {}
-    gpu_nodes = None
+    gpu_nodes = gpu_walk = None
     modes = [args.mode] + ([] if args.no_other_mode else
                            [m for m in ("resispec", "specinfer") if m != args.mode])
     for mode in modes:
-        wall, kern_ms = time_mode(native, torch, w, mode, args.steps, args.warmup,
-                                  args.settle_ms * 1e-3, ws, out_tok, out_len, out_st)
+        wall, kern_ms, walk_ms = time_mode(native, torch, w, mode, args.steps, args.warmup,
+                                           args.settle_ms * 1e-3, ws, out_tok, out_len, out_st)
         lens = out_len.cpu().numpy()
         assert (out_st.cpu().numpy() == 0).all(), "device status not OK"
         if mode == args.mode:
-            # the node outcomes the last timed step left in its workspace (parity below)
+            # the node outcomes and walks the last timed step left (parity below)
             gpu_nodes = tuple(t.cpu().numpy() for t in native.resispec_node_outcomes(ws, B, N))
+            gpu_walk = (out_tok.cpu().numpy(), lens.copy())
         kms = float(np.mean(kern_ms))
         results[mode] = {
             "ms_per_step": 1e3 * wall / args.steps,
             "rows_per_s": B * N / (wall / args.steps),
-            "row_kernel_ms": kms,
-            "row_kernel_ms_min": float(np.min(kern_ms)),
-            "row_kernel_gbps": alg_bytes / (kms * 1e-3) / 1e9,
+            "decide_kernel_ms": kms,
+            "decide_kernel_ms_min": float(np.min(kern_ms)),
+            "decide_kernel_gbps": alg_bytes / (kms * 1e-3) / 1e9,
+            "walk_draw_ms": float(np.mean(walk_ms)),
             "mean_accepted_len": float(lens.mean()),
         }
+    # the same step with every row drawing at once (the row kernel, then the walk)
+    all_nodes = None
+    if not args.no_all_nodes:
+        wall, kern_ms, walk_ms = time_mode(native, torch, w, args.mode, args.steps, args.warmup,
+                                           args.settle_ms * 1e-3, ws, out_tok, out_len, out_st,
+                                           deferred=False)
+        assert (out_st.cpu().numpy() == 0).all(), "device status not OK"
+        assert gpu_walk is None or (np.array_equal(out_tok.cpu().numpy(), gpu_walk[0])
+                                    and np.array_equal(out_len.cpu().numpy(), gpu_walk[1])), \
+            "the two schedules' walks differ"
+        kms = float(np.mean(kern_ms))
+        all_nodes = {"schedule": "every row draws (resispec_verify_nodes + resispec_walk)",
+                     "ms_per_step": 1e3 * wall / args.steps,
+                     "rows_per_s": B * N / (wall / args.steps),
+                     "row_kernel_ms": kms, "row_kernel_ms_min": float(np.min(kern_ms)),
+                     "row_kernel_gbps": alg_bytes / (kms * 1e-3) / 1e9,
+                     "row_kernel_frac": alg_bytes / (kms * 1e-3) / 1e9 / HBM_PEAK_GBPS,
+                     "walk_ms": float(np.mean(walk_ms))}
 
     # the path-only schedule of the same step (only the nodes each walk reaches)
     path = None
@@ -641,7 +713,7 @@ def main():
     probe = None if args.no_read_probe else read_ceiling(torch)
 
     r = results[args.mode]
-    achieved = r["row_kernel_gbps"]
+    achieved = r["decide_kernel_gbps"]
     traffic = measured_traffic(w["cfg"]["name"], args.mode)
     out = {
         "metric": METRIC,
@@ -663,16 +735,17 @@ def main():
         "roofline": {"bound": "hbm", "achieved": achieved, "peak": HBM_PEAK_GBPS, "unit": "GB/s",
                      "frac": achieved / HBM_PEAK_GBPS,
                      "traffic": traffic,
-                     "kernel": "rs_row_kernel", "alg_bytes_per_launch": alg_bytes,
+                     "kernel": "rs_decide_kernel", "alg_bytes_per_launch": alg_bytes,
                      "rows_target": rows_t, "rows_draft": rows_d,
                      # HBM traffic (counters) per second, against the measured read ceiling
-                     "traffic_gbps": (traffic / (r["row_kernel_ms"] * 1e-3) / 1e9
+                     "traffic_gbps": (traffic / (r["decide_kernel_ms"] * 1e-3) / 1e9
                                       if traffic else None),
                      "read_ceiling_gbps": probe["nt_stream_gbps"] if probe else None,
                      "frac_of_read_ceiling": (achieved / probe["nt_stream_gbps"]
                                               if probe else None)},
         "read_probe": probe,
         "modes": results,
+        "all_nodes_draw": all_nodes,
         "path_schedule": path,
         "draft_step": draft,
         "single_tree": single,
@@ -680,19 +753,23 @@ def main():
     if not args.no_configs:
         headline = {"B": B, "N": N, "V": V, "logits": "bf16" if esz == 2 else "f32",
                     "rows_target": rows_t, "rows_draft": rows_d, "alg_bytes_per_launch": alg_bytes,
-                    "row_kernel_ms": r["row_kernel_ms"], "row_kernel_ms_min": r["row_kernel_ms_min"],
-                    "rows_per_s": B * N / (r["row_kernel_ms"] * 1e-3),
+                    "decide_kernel_ms": r["decide_kernel_ms"],
+                    "decide_kernel_ms_min": r["decide_kernel_ms_min"],
+                    "walk_draw_ms": r["walk_draw_ms"],
+                    "all_nodes_draw_row_kernel_ms": all_nodes["row_kernel_ms"] if all_nodes else None,
+                    "rows_per_s": r["rows_per_s"],
                     "achieved_gbps": achieved, "frac": achieved / HBM_PEAK_GBPS,
                     "step_ms": r["ms_per_step"], "note": "the headline run"}
         out["configs"] = configs_record(native, torch, np, synth, args.steps, args.warmup,
                                         args.mode, headline)
     parity = None
     if not args.no_cpu_baseline:
-        out["cpu_baseline"], parity = cpu_baseline(w, args.cpu_seconds, args.mode, gpu_nodes)
+        out["cpu_baseline"], parity = cpu_baseline(w, args.cpu_seconds, args.mode, gpu_nodes,
+                                                   gpu_walk)
         out["parity"] = parity
     print(json.dumps(out), flush=True)
     if parity and (parity["mismatches"] or parity["flagged_invalid"]
-                   or parity["mismatches_margin_ge_1e-7"]):
+                   or parity["mismatches_margin_ge_1e-7"] or parity.get("walk_mismatches")):
         print("parity failure: %s" % json.dumps(parity), file=sys.stderr)
         sys.exit(1)
 

@@ -43,7 +43,7 @@
 extern "C" {
 #endif
 
-#define RESISPEC_ABI_VERSION 2
+#define RESISPEC_ABI_VERSION 3
 
 /* Largest number of candidates (children) one node may have. */
 #define RS_MAX_CANDIDATES 64
@@ -69,8 +69,12 @@ typedef enum {
     RS_SEQ_BAD_UNIFORM = 5,      /* a used uniform outside [0, 1) */
     RS_SEQ_DEPTH_EXCEEDED = 6,   /* accepted path longer than max_depth */
     RS_SEQ_TOO_MANY_CHILDREN = 7, /* a node with more than RS_MAX_CANDIDATES children */
-    RS_SEQ_GROUP_TIMEOUT = 8     /* row groups: a workgroup did not receive the others'
+    RS_SEQ_GROUP_TIMEOUT = 8,    /* row groups: a workgroup did not receive the others'
                                     slot totals of a pass within 20 ms */
+    RS_SEQ_DEFERRED = 9          /* node outcomes of resispec_decide_nodes only: the node
+                                    rejected its one candidate, or is a leaf, and its draw
+                                    is left to the walk (resispec_walk_draw), which makes it
+                                    only where a walk ends */
 } rs_seq_status;
 
 typedef enum { RS_MODE_RESISPEC = 0, RS_MODE_SPECINFER = 1 } rs_mode;
@@ -139,6 +143,63 @@ rs_status resispec_verify_tree(const void* target_logits, const void* draft_logi
                                const rs_params* prm, int32_t* out_tokens,
                                int32_t* out_accepted_len, int32_t* out_status,
                                void* workspace, size_t workspace_bytes, void* stream);
+
+/*
+ * The all-nodes schedule of resispec_verify_tree with deferred draws (same arguments, same
+ * results, bit for bit).  A node's draw from its final residual, and a leaf's bonus draw,
+ * matter only where a walk ends (§Preliminary, tree-structured verification: the walk
+ * draws once, at the node where it stops), so they are made there.  Two launches:
+ *   - every node row takes pass 1 (the softmax statistics of Preliminary) and its tests
+ *     (Eq. 2, Algorithm 1); a row with several candidates also takes the rejection passes
+ *     its later tests need, and draws at once if it rejects them all; a row with one
+ *     candidate that it rejects, and a leaf, keep their pass-1 slot totals in the
+ *     workspace instead of drawing (no rejection pass re-reads their logits);
+ *   - one workgroup per sequence walks the decisions and, where the walk ends at such a
+ *     row, takes it up again: the residual pass of its rejection (Eq. 1/2 or GetProxy)
+ *     over that row alone, then the inverse-CDF draw, with the same arithmetic on the same
+ *     values as resispec_verify_tree.
+ *   workspace : device buffer of at least resispec_deferred_workspace_bytes(B, N) bytes,
+ *               16-byte aligned (node outcomes, then 2 KiB of slot totals per node row);
+ *               contents on entry are ignored.  Calls that overlap on one workspace race.
+ * Errors and statuses as resispec_verify_tree.
+ */
+rs_status resispec_verify_tree_deferred(const void* target_logits, const void* draft_logits,
+                                        const int32_t* node_token, const int32_t* parent,
+                                        const float* u_accept, const float* u_resample,
+                                        int32_t B, int32_t N, int32_t V, int32_t max_depth,
+                                        const rs_params* prm, int32_t* out_tokens,
+                                        int32_t* out_accepted_len, int32_t* out_status,
+                                        void* workspace, size_t workspace_bytes, void* stream);
+
+/*
+ * The two launches of resispec_verify_tree_deferred, for callers that schedule them
+ * separately (same kernels, same results):
+ *   resispec_decide_nodes: every node's tests into `workspace`; node outcomes (see
+ *     resispec_node_outcomes, which reads this workspace too) are the accepted child,
+ *     the drawn token of a row with several candidates that rejected them all, a fault,
+ *     or RS_SEQ_DEFERRED;
+ *   resispec_walk_draw: the walk from each root over those outcomes, with the deferred
+ *     draw where a walk ends (same inputs, and the workspace written by
+ *     resispec_decide_nodes with the same B and N, earlier on the same stream); it
+ *     records the outcome of each node it draws for in the workspace.
+ */
+rs_status resispec_decide_nodes(const void* target_logits, const void* draft_logits,
+                                const int32_t* node_token, const int32_t* parent,
+                                const float* u_accept, const float* u_resample,
+                                int32_t B, int32_t N, int32_t V, const rs_params* prm,
+                                void* workspace, size_t workspace_bytes, void* stream);
+
+rs_status resispec_walk_draw(const void* target_logits, const void* draft_logits,
+                             const int32_t* node_token, const int32_t* parent,
+                             const float* u_accept, const float* u_resample,
+                             int32_t B, int32_t N, int32_t V, int32_t max_depth,
+                             const rs_params* prm, void* workspace, size_t workspace_bytes,
+                             int32_t* out_tokens, int32_t* out_accepted_len,
+                             int32_t* out_status, void* stream);
+
+/* Workspace bytes resispec_verify_tree_deferred needs for B sequences of N nodes (0 if
+ * B <= 0 or N <= 0). */
+size_t resispec_deferred_workspace_bytes(int32_t B, int32_t N);
 
 /*
  * resispec_verify_tree without a caller workspace, for callers that cannot allocate

@@ -75,7 +75,13 @@ struct KParams {
     float* residual_out;
     // path schedule with a workspace: per-sequence fp32 residual of the running row
     // (rc_stride floats per sequence), or null
-    float* rcache;
+    // deferred draws (the other schedules): per node row, the pass-1 slot totals of the
+    // target row, then of the draft row (kStateDoubles doubles a row), kept for the rows
+    // whose draw is left to the walk
+    union {
+        float* rcache;
+        double* dstate;
+    };
     int64_t rc_stride;
     int32_t B, N;
     int32_t V;
@@ -466,7 +472,32 @@ __device__ __forceinline__ void wave_sweep_rc(const float* __restrict__ rc, cons
 
 // RC: the path schedule, whose later ResiSpec rejection passes keep the row's residual
 // in P.rcache when the caller's workspace holds it (see the rejection passes below).
-template <typename In, int VEC, int UNR, int MODE, int BLK, bool SPLIT, bool RC = false, typename Emit>
+// How a row's draw is scheduled.  kSchedAll: every row that rejects all its candidates,
+// or has none, draws at once (the all-nodes and path schedules).  kSchedDecide: a row with
+// one candidate that it rejects, and a leaf, stop after their tests; they keep their
+// pass-1 slot totals in P.dstate and report RS_SEQ_DEFERRED, because the token they would
+// draw is used only if a walk ends there (a row with several candidates needs its
+// rejection passes for its later tests anyway, and draws at once).  kSchedResume: such a
+// row is taken up again where its walk ends: the slot totals come from P.dstate instead
+// of pass 1, and every step after them is the same code on the same values, so the
+// token is the one the row would have drawn at once.
+constexpr int kSchedAll = 0, kSchedDecide = 1, kSchedResume = 2;
+constexpr int64_t kStateDoubles = 2 * kMaxSlots;
+
+// A deferred row's pass-1 slot totals: the target row's, then (rows with children) the
+// draft row's.
+__device__ __forceinline__ void keep_slot_totals(const KParams& P, const Smem& sm, int64_t row, int nslots,
+                                                 bool internal) {
+    double* st = P.dstate + row * kStateDoubles;
+    const int tid = threadIdx.x;
+    if (tid < nslots) {
+        st[tid] = sm.slotP[tid];
+        if (internal) st[kMaxSlots + tid] = sm.slotB[tid];
+    }
+}
+
+template <typename In, int VEC, int UNR, int MODE, int BLK, bool SPLIT, bool RC = false,
+          int SCHED = kSchedAll, typename Emit>
 __device__ __forceinline__ void verify_row(const KParams& P, Smem& sm, const int64_t row,
                                            const int32_t b, const int32_t n, Emit&& emit,
                                            RowGroup& grp) {
@@ -666,8 +697,9 @@ __device__ __forceinline__ void verify_row(const KParams& P, Smem& sm, const int
             // Cache hint for pass 1 of a row with one candidate: when the candidate looks
             // accepted (its test taken with the two rows' sums assumed equal), no
             // rejection pass is expected to re-read the row, so the waves stream the rest
-            // of it nontemporally.  The results do not depend on it.
-            if (nc == 1 && (double)hu * qe < pe) sm.nt_hint = 1;
+            // of it nontemporally.  The results do not depend on it.  When draws are
+            // deferred no pass of this launch re-reads such a row, whatever its test.
+            if (nc == 1 && (SCHED == kSchedDecide || (double)hu * qe < pe)) sm.nt_hint = 1;
         }
         sm.cand_tok[hrank] = hx;
         sm.cand_u[hrank] = hu;
@@ -701,6 +733,17 @@ __device__ __forceinline__ void verify_row(const KParams& P, Smem& sm, const int
             if (internal) sm.partB[lane][slot] = fc;
             fa = fc = 0.0f;
         };
+        if constexpr (SCHED == kSchedResume) {
+            // the slot totals pass 1 gave this row when its draw was deferred
+            const double* st = P.dstate + row * kStateDoubles;
+            if (tid < nslots) {
+                const double a = st[tid];
+                sm.slotA[tid] = a;
+                sm.slotP[tid] = a;
+                sm.slotB[tid] = internal ? st[kMaxSlots + tid] : 0.0;
+            }
+            __syncthreads();
+        } else {
         if (internal) {
             wave_sweep<In, VEC, UNR, true, 1, kNtPass1>(tg, dg, V, G, nl, s0, false, pre, pre, &sm.next_slot,
                 [&](const float (&t)[UNR][VEC], const float (&d)[UNR][VEC], int idx0, int slot) {
@@ -750,6 +793,7 @@ __device__ __forceinline__ void verify_row(const KParams& P, Smem& sm, const int
             if (tid == 0) emit(-1, -1, RS_SEQ_GROUP_TIMEOUT);
             zero_residual_row(P, row);
             return;
+        }
         }
         if (wid == 0) {
             double a0 = 0.0, a1 = 0.0;
@@ -866,6 +910,18 @@ __device__ __forceinline__ void verify_row(const KParams& P, Smem& sm, const int
         }
     }
 
+    // Deferred draws: the row keeps its pass-1 slot totals and reports RS_SEQ_DEFERRED.
+    // Rows that took the exact-maximum pass draw at once (their exponent references are
+    // not the ones a resumed row derives).
+    const bool deferrable = SCHED == kSchedDecide && !P.flat && !refixed;
+    if constexpr (SCHED == kSchedDecide) {
+        if (deferrable && nc == 0) {   // a leaf: the bonus draw is used only if a walk ends here
+            keep_slot_totals(P, sm, row, nslots, false);
+            if (tid == 0) emit(-1, -1, RS_SEQ_DEFERRED);
+            return;
+        }
+    }
+
     const double St = sm.St, Sd = sm.Sd;
     // draft mass in target units: q St / Sd, folded into the step constants
     const double q2t = internal ? St / Sd : 0.0;
@@ -944,6 +1000,14 @@ __device__ __forceinline__ void verify_row(const KParams& P, Smem& sm, const int
         }
         __syncthreads();
         if (sm.decision != -1) break;
+        // one candidate, rejected: the draw from the residual is used only if a walk ends here
+        if constexpr (SCHED == kSchedDecide) {
+            if (deferrable && nc == 1) {
+                keep_slot_totals(P, sm, row, nslots, true);
+                if (tid == 0) emit(-1, -1, RS_SEQ_DEFERRED);
+                return;
+            }
+        }
 
         // rejection pass: sums of step i with per-slot partials
         {
@@ -1641,20 +1705,27 @@ rs_rowgroup_kernel(const KParams P, const GroupArgs ga) {
 // the walk then reads them across lanes, and loads the next 64 when it moves past them
 // (children have larger indices than their parents).  Lane 0 writes the outputs.
 constexpr int kWalkBlock = 256;
-__global__ void __launch_bounds__(kWalkBlock) rs_walk_kernel(const int32_t* __restrict__ node_child,
-                                                             const int32_t* __restrict__ node_tok,
-                                                             const int32_t* __restrict__ node_status,
-                                                             const int32_t* __restrict__ node_token, int32_t B,
-                                                             int32_t N, int32_t max_depth,
-                                                             int32_t* __restrict__ out_tokens,
-                                                             int32_t* __restrict__ out_len,
-                                                             int32_t* __restrict__ out_status) {
+
+// Where a walk ended: the number of accepted draft tokens, the sequence's status, the node
+// it ended at, and that node's token (-1 if none).  status RS_SEQ_DEFERRED: the walk ended
+// at a node whose draw was deferred.
+struct WalkEnd {
+    int32_t len, status, node;
+};
+
+// One wave walks sequence `base / N` over the node outcomes: from the root it follows
+// accepted children, writing each accepted node's token to out[0..len), and writes the
+// token the last node drew (or its bonus) to out[len].  Lane 0 writes; every lane returns
+// the same result.  The outcomes of 64 consecutive nodes are loaded at once, one per lane,
+// and read across lanes as the walk steps (a child's index is larger than its parent's,
+// so a new window is loaded only when the walk passes the current one).  Node ov_node
+// takes the outcome (ov_child, ov_tok, ov_status) instead of the stored one (-1: none).
+__device__ WalkEnd walk_wave(const int32_t* __restrict__ node_child, const int32_t* __restrict__ node_tok,
+                             const int32_t* __restrict__ node_status, const int32_t* __restrict__ node_token,
+                             int64_t base, int32_t N, int32_t max_depth, int32_t* __restrict__ out,
+                             int32_t ov_node, int32_t ov_child, int32_t ov_tok, int32_t ov_status) {
     const int lane = threadIdx.x & 63;
-    const int32_t b = (int32_t)(blockIdx.x * (kWalkBlock / 64) + (threadIdx.x >> 6));
-    if (b >= B) return;   // the whole wave
     const int64_t W = (int64_t)max_depth + 1;
-    int32_t* out = out_tokens + (int64_t)b * W;
-    const int64_t base = (int64_t)b * N;
     int32_t wbase = 0, wc = -1, wt = -1, ws = RS_SEQ_OK, wk = -1;
     auto window = [&](int32_t nb) {
         wbase = nb;
@@ -1664,6 +1735,11 @@ __global__ void __launch_bounds__(kWalkBlock) rs_walk_kernel(const int32_t* __re
         wt = in ? node_tok[base + m] : -1;
         ws = in ? node_status[base + m] : RS_SEQ_OK;
         wk = in ? node_token[base + m] : -1;
+        if (m == ov_node) {
+            wc = ov_child;
+            wt = ov_tok;
+            ws = ov_status;
+        }
     };
     window(0);
     if (lane == 0)
@@ -1698,13 +1774,106 @@ __global__ void __launch_bounds__(kWalkBlock) rs_walk_kernel(const int32_t* __re
         if (t >= 0 && lane == 0) out[len] = t;
         break;
     }
-    if (lane != 0) return;
-    if (status != RS_SEQ_OK) {
+    return WalkEnd{len, status, n};
+}
+
+// The sequence's outputs once its walk has ended: on a fault every token and the length
+// are -1.  Lane 0 writes.
+__device__ void walk_finish(const WalkEnd& we, int64_t W, int32_t* __restrict__ out, int32_t b,
+                            int32_t* __restrict__ out_len, int32_t* __restrict__ out_status) {
+    if ((threadIdx.x & 63) != 0) return;
+    int32_t len = we.len;
+    if (we.status != RS_SEQ_OK) {
         for (int64_t i = 0; i < W; ++i) out[i] = -1;
         len = -1;
     }
     out_len[b] = len;
-    if (out_status) out_status[b] = status;
+    if (out_status) out_status[b] = we.status;
+}
+
+// The walk of the all-nodes schedule: one wave per sequence.  It is latency-bound: every
+// tree here fits one window of 64 nodes, so a sequence costs one round trip to memory.
+__global__ void __launch_bounds__(kWalkBlock) rs_walk_kernel(const int32_t* __restrict__ node_child,
+                                                             const int32_t* __restrict__ node_tok,
+                                                             const int32_t* __restrict__ node_status,
+                                                             const int32_t* __restrict__ node_token, int32_t B,
+                                                             int32_t N, int32_t max_depth,
+                                                             int32_t* __restrict__ out_tokens,
+                                                             int32_t* __restrict__ out_len,
+                                                             int32_t* __restrict__ out_status) {
+    const int32_t b = (int32_t)(blockIdx.x * (kWalkBlock / 64) + (threadIdx.x >> 6));
+    if (b >= B) return;   // the whole wave
+    const int64_t W = (int64_t)max_depth + 1;
+    int32_t* out = out_tokens + (int64_t)b * W;
+    const WalkEnd we = walk_wave(node_child, node_tok, node_status, node_token, (int64_t)b * N, N, max_depth,
+                                 out, -1, -1, -1, RS_SEQ_OK);
+    walk_finish(we, W, out, b, out_len, out_status);
+}
+
+// The all-nodes schedule with deferred draws, first launch: every node row's tests, with
+// the draws of single-candidate rejections and leaves deferred (same grid as the row
+// kernel).
+template <typename In, int VEC, int UNR, int MODE>
+__global__ void __launch_bounds__(kBlock) __attribute__((amdgpu_waves_per_eu(4))) rs_decide_kernel(const KParams P) {
+    __shared__ Smem sm;
+    const int32_t g = blockIdx.x;
+    const int32_t n = g / P.B;
+    const int32_t b = g - n * P.B;
+    const int64_t row = (int64_t)b * P.N + n;
+    RowGroup solo{1, 0, nullptr, nullptr, 0u, kGroupWaitTicks};
+    verify_row<In, VEC, UNR, MODE, kBlock, false, false, kSchedDecide>(
+        P, sm, row, b, n, [&](int32_t child, int32_t tok, int32_t st) { write_outcome(P, row, child, tok, st); },
+        solo);
+}
+
+// Second launch: one workgroup per sequence walks the decided outcomes; where the walk
+// ends at a row whose draw was deferred, the workgroup takes that row up again (its slot
+// totals from the first launch, then its rejection pass and its draw, or the bonus draw
+// of a leaf), records the node's outcome and finishes the walk with it.
+template <typename In, int VEC, int UNR, int MODE>
+__global__ void __launch_bounds__(kBlock) __attribute__((amdgpu_waves_per_eu(4)))
+rs_finish_kernel(const KParams P, int32_t max_depth, int32_t* __restrict__ out_tokens,
+                 int32_t* __restrict__ out_len, int32_t* __restrict__ out_status) {
+    __shared__ Smem sm;
+    __shared__ int32_t s_node;
+    const int32_t b = blockIdx.x;
+    const int64_t W = (int64_t)max_depth + 1;
+    int32_t* out = out_tokens + (int64_t)b * W;
+    const int64_t base = (int64_t)b * P.N;
+    WalkEnd we{0, RS_SEQ_OK, -1};
+    if (threadIdx.x < 64) {
+        we = walk_wave(P.node_child, P.node_tok, P.node_status, P.node_token, base, P.N, max_depth, out, -1, -1,
+                       -1, RS_SEQ_OK);
+        if (threadIdx.x == 0) s_node = we.status == RS_SEQ_DEFERRED ? we.node : -1;
+    }
+    __syncthreads();
+    const int32_t n = s_node;
+    if (n < 0) {
+        if (threadIdx.x < 64) walk_finish(we, W, out, b, out_len, out_status);
+        return;
+    }
+    const int64_t row = base + n;
+    int32_t oc = -1, ot = -1, os = RS_SEQ_OK;   // the row's outcome (thread 0)
+    RowGroup solo{1, 0, nullptr, nullptr, 0u, kGroupWaitTicks};
+    verify_row<In, VEC, UNR, MODE, kBlock, false, false, kSchedResume>(
+        P, sm, row, b, n,
+        [&](int32_t child, int32_t tok, int32_t st) {
+            write_outcome(P, row, child, tok, st);
+            oc = child;
+            ot = tok;
+            os = st;
+        },
+        solo);
+    // thread 0 holds the outcome; wave 0 walks again with it in place of the deferred one
+    if (threadIdx.x < 64) {
+        oc = __builtin_amdgcn_readfirstlane(oc);
+        ot = __builtin_amdgcn_readfirstlane(ot);
+        os = __builtin_amdgcn_readfirstlane(os);
+        if (os != RS_SEQ_OK) oc = ot = -1;
+        we = walk_wave(P.node_child, P.node_tok, P.node_status, P.node_token, base, P.N, max_depth, out, n, oc, ot,
+                       os);
+        walk_finish(we, W, out, b, out_len, out_status);
+    }
 }
 
 }  // namespace
@@ -1963,6 +2132,47 @@ hipError_t launch_walk(const int32_t* node_child, const int32_t* node_tok,
                        dim3(kWalkBlock), 0, s, node_child, node_tok, node_status, node_token, B, N,
                        max_depth, out_tokens, out_len, out_status);
     return hipGetLastError();
+}
+
+// Deferred draws: the decide kernel over every node row, or the finish kernel over every
+// sequence (finish = true).
+template <typename In, int VEC, int UNR, int MODE>
+hipError_t launch_deferred(KParams P, bool finish, int32_t max_depth, int32_t* out_tokens, int32_t* out_len,
+                           int32_t* out_status, hipStream_t s) {
+    set_slots<VEC, UNR>(P);
+    if (finish)
+        hipLaunchKernelGGL((rs_finish_kernel<In, VEC, UNR, MODE>), dim3((unsigned)P.B), dim3(kBlock), 0, s, P,
+                           max_depth, out_tokens, out_len, out_status);
+    else
+        hipLaunchKernelGGL((rs_decide_kernel<In, VEC, UNR, MODE>), dim3((unsigned)((int64_t)P.B * P.N)),
+                           dim3(kBlock), 0, s, P);
+    return hipGetLastError();
+}
+
+template <int MODE>
+hipError_t launch_deferred_m(const KParams& P, int dtype, bool vec, bool finish, int32_t max_depth,
+                             int32_t* out_tokens, int32_t* out_len, int32_t* out_status, hipStream_t s) {
+    if (dtype == RS_BF16)
+        return vec ? launch_deferred<uint16_t, 8, kUnr16, MODE>(P, finish, max_depth, out_tokens, out_len,
+                                                                out_status, s)
+                   : launch_deferred<uint16_t, 1, 4, MODE>(P, finish, max_depth, out_tokens, out_len, out_status, s);
+    return vec ? launch_deferred<float, 4, kUnr32, MODE>(P, finish, max_depth, out_tokens, out_len, out_status, s)
+               : launch_deferred<float, 1, 4, MODE>(P, finish, max_depth, out_tokens, out_len, out_status, s);
+}
+
+hipError_t launch_deferred_stage(const KParams& P, const rs_params* prm, bool vec, bool finish, int32_t max_depth,
+                                 int32_t* out_tokens, int32_t* out_len, int32_t* out_status, hipStream_t s) {
+    if (prm->mode == RS_MODE_SPECINFER)
+        return launch_deferred_m<RS_MODE_SPECINFER>(P, prm->logits_dtype, vec, finish, max_depth, out_tokens,
+                                                    out_len, out_status, s);
+    return launch_deferred_m<RS_MODE_RESISPEC>(P, prm->logits_dtype, vec, finish, max_depth, out_tokens, out_len,
+                                               out_status, s);
+}
+
+// bytes of the deferred schedule's workspace: the node outcome arrays, then the slot
+// totals of every row
+size_t deferred_bytes(int64_t rows) {
+    return node_arrays_bytes(rows) + (size_t)rows * (size_t)kStateDoubles * sizeof(double);
 }
 
 KParams tree_params(const void* target_logits, const void* draft_logits, const int32_t* node_token,
@@ -2360,6 +2570,94 @@ rs_status resispec_verify_tree_debug(const void* target_logits, const void* draf
     return tree_impl(target_logits, draft_logits, node_token, parent, u_accept, u_resample, B, N, V,
                      max_depth, prm, out_tokens, out_accepted_len, out_status, node_child,
                      node_token_out, node_status, residual_out, (hipStream_t)stream);
+}
+
+size_t resispec_deferred_workspace_bytes(int32_t B, int32_t N) {
+    if (B <= 0 || N <= 0) return 0;
+    return deferred_bytes((int64_t)B * N);
+}
+
+}  // extern "C"
+
+namespace {
+
+// One stage of the deferred schedule: the decide launch (finish = false) or the walk with
+// the deferred draws (finish = true).
+rs_status deferred_stage(const void* target_logits, const void* draft_logits, const int32_t* node_token,
+                         const int32_t* parent, const float* u_accept, const float* u_resample, int32_t B,
+                         int32_t N, int32_t V, int32_t max_depth, const rs_params* prm, int32_t* out_tokens,
+                         int32_t* out_accepted_len, int32_t* out_status, void* workspace,
+                         size_t workspace_bytes, bool finish, hipStream_t s) {
+    const int64_t rows = (int64_t)B * N;
+    KParams P = tree_params(target_logits, draft_logits, node_token, parent, u_accept, u_resample, B, N, V, prm,
+                            ws_array(workspace, rows, 0), ws_array(workspace, rows, 1),
+                            ws_array(workspace, rows, 2), nullptr);
+    P.dstate = reinterpret_cast<double*>(static_cast<char*>(workspace) + node_arrays_bytes(rows));
+    const bool vec = vector_ok(target_logits, draft_logits, V, prm->logits_dtype);
+    return launch_deferred_stage(P, prm, vec, finish, max_depth, out_tokens, out_accepted_len, out_status, s) ==
+                   hipSuccess
+               ? RS_OK
+               : RS_ERR_HIP;
+}
+
+bool deferred_ws_ok(const void* workspace, size_t workspace_bytes, int32_t B, int32_t N) {
+    return workspace && aligned16(workspace) && workspace_bytes >= resispec_deferred_workspace_bytes(B, N);
+}
+
+}  // namespace
+
+extern "C" {
+
+rs_status resispec_decide_nodes(const void* target_logits, const void* draft_logits,
+                                const int32_t* node_token, const int32_t* parent,
+                                const float* u_accept, const float* u_resample, int32_t B,
+                                int32_t N, int32_t V, const rs_params* prm, void* workspace,
+                                size_t workspace_bytes, void* stream) {
+    int32_t dummy = 0;   // output pointers are not used by this stage
+    const rs_status as = check_tree_args(target_logits, draft_logits, node_token, parent, u_accept,
+                                         u_resample, B, N, V, 0, prm, &dummy, &dummy);
+    if (as != RS_OK || B == 0) return as;
+    if (!deferred_ws_ok(workspace, workspace_bytes, B, N)) return RS_ERR_WORKSPACE;
+    return deferred_stage(target_logits, draft_logits, node_token, parent, u_accept, u_resample, B, N, V, 0, prm,
+                          nullptr, nullptr, nullptr, workspace, workspace_bytes, false, (hipStream_t)stream);
+}
+
+rs_status resispec_walk_draw(const void* target_logits, const void* draft_logits,
+                             const int32_t* node_token, const int32_t* parent,
+                             const float* u_accept, const float* u_resample, int32_t B,
+                             int32_t N, int32_t V, int32_t max_depth, const rs_params* prm,
+                             void* workspace, size_t workspace_bytes, int32_t* out_tokens,
+                             int32_t* out_accepted_len, int32_t* out_status, void* stream) {
+    const rs_status as = check_tree_args(target_logits, draft_logits, node_token, parent, u_accept,
+                                         u_resample, B, N, V, max_depth, prm, out_tokens,
+                                         out_accepted_len);
+    if (as != RS_OK || B == 0) return as;
+    if (!deferred_ws_ok(workspace, workspace_bytes, B, N)) return RS_ERR_WORKSPACE;
+    return deferred_stage(target_logits, draft_logits, node_token, parent, u_accept, u_resample, B, N, V,
+                          max_depth, prm, out_tokens, out_accepted_len, out_status, workspace, workspace_bytes,
+                          true, (hipStream_t)stream);
+}
+
+rs_status resispec_verify_tree_deferred(const void* target_logits, const void* draft_logits,
+                                        const int32_t* node_token, const int32_t* parent,
+                                        const float* u_accept, const float* u_resample, int32_t B,
+                                        int32_t N, int32_t V, int32_t max_depth, const rs_params* prm,
+                                        int32_t* out_tokens, int32_t* out_accepted_len,
+                                        int32_t* out_status, void* workspace, size_t workspace_bytes,
+                                        void* stream) {
+    const rs_status as = check_tree_args(target_logits, draft_logits, node_token, parent, u_accept,
+                                         u_resample, B, N, V, max_depth, prm, out_tokens,
+                                         out_accepted_len);
+    if (as != RS_OK || B == 0) return as;
+    if (!deferred_ws_ok(workspace, workspace_bytes, B, N)) return RS_ERR_WORKSPACE;
+    const hipStream_t s = (hipStream_t)stream;
+    const rs_status r = deferred_stage(target_logits, draft_logits, node_token, parent, u_accept, u_resample, B,
+                                       N, V, max_depth, prm, out_tokens, out_accepted_len, out_status, workspace,
+                                       workspace_bytes, false, s);
+    if (r != RS_OK) return r;
+    return deferred_stage(target_logits, draft_logits, node_token, parent, u_accept, u_resample, B, N, V,
+                          max_depth, prm, out_tokens, out_accepted_len, out_status, workspace, workspace_bytes,
+                          true, s);
 }
 
 rs_status resispec_validate_tree_host(const int32_t* parent, const int32_t* node_token, int32_t B,

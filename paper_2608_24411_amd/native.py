@@ -14,7 +14,8 @@ LIB_PATH = os.environ.get("RESISPEC_LIBRARY") or os.path.join(HERE, "libresispec
 
 RS_OK, RS_ERR_INVALID_ARG, RS_ERR_WORKSPACE, RS_ERR_UNSUPPORTED, RS_ERR_HIP = range(5)
 (RS_SEQ_OK, RS_SEQ_BAD_TOKEN, RS_SEQ_ZERO_DRAFT, RS_SEQ_UNDERFLOW, RS_SEQ_BAD_TREE,
- RS_SEQ_BAD_UNIFORM, RS_SEQ_DEPTH_EXCEEDED, RS_SEQ_TOO_MANY_CHILDREN) = range(8)
+ RS_SEQ_BAD_UNIFORM, RS_SEQ_DEPTH_EXCEEDED, RS_SEQ_TOO_MANY_CHILDREN, RS_SEQ_GROUP_TIMEOUT,
+ RS_SEQ_DEFERRED) = range(10)
 RS_MODE_RESISPEC, RS_MODE_SPECINFER = 0, 1
 RS_F32, RS_BF16 = 0, 1
 RS_MAX_CANDIDATES = 64
@@ -23,6 +24,8 @@ MODES = {"resispec": RS_MODE_RESISPEC, "specinfer": RS_MODE_SPECINFER}
 
 # Every symbol include/resispec.h declares.
 EXPORTS = ("resispec_verify", "resispec_verify_tree", "resispec_verify_tree_noalloc",
+           "resispec_verify_tree_deferred", "resispec_decide_nodes", "resispec_walk_draw",
+           "resispec_deferred_workspace_bytes",
            "resispec_verify_tree_path",
            "resispec_verify_tree_path_group", "resispec_path_workspace_bytes",
            "resispec_path_group_size", "resispec_debug_set_group_waits",
@@ -84,6 +87,15 @@ def _load():
     lib.resispec_verify_tree_debug.argtypes = [P, P, P, P, P, P, i32, i32, i32, i32, prm, P, P,
                                                P, P, sz, P, P, P, P, P]
     lib.resispec_verify_tree_debug.restype = i32
+    lib.resispec_verify_tree_deferred.argtypes = [P, P, P, P, P, P, i32, i32, i32, i32, prm, P, P,
+                                                  P, P, sz, P]
+    lib.resispec_verify_tree_deferred.restype = i32
+    lib.resispec_decide_nodes.argtypes = [P, P, P, P, P, P, i32, i32, i32, prm, P, sz, P]
+    lib.resispec_decide_nodes.restype = i32
+    lib.resispec_walk_draw.argtypes = [P, P, P, P, P, P, i32, i32, i32, i32, prm, P, sz, P, P, P, P]
+    lib.resispec_walk_draw.restype = i32
+    lib.resispec_deferred_workspace_bytes.argtypes = [i32, i32]
+    lib.resispec_deferred_workspace_bytes.restype = sz
     lib.resispec_verify_nodes.argtypes = [P, P, P, P, P, P, i32, i32, i32, prm, P, sz, P]
     lib.resispec_verify_nodes.restype = i32
     lib.resispec_walk.argtypes = [P, i32, i32, i32, P, sz, P, P, P, P]
@@ -479,6 +491,99 @@ def resispec_draft_candidates(draft_logits, parent, *, temperature, without_repl
         _stream(stream))
     _check(st)
     return node_token, u_accept, u_resample, out_status
+
+
+def resispec_deferred_workspace_bytes(B: int, N: int) -> int:
+    return lib.resispec_deferred_workspace_bytes(int(B), int(N))
+
+
+def _logit_args(target_logits, draft_logits, node_token, parent, u_accept, u_resample):
+    import torch
+    return (_dev(target_logits, target_logits.dtype, "target_logits"),
+            _dev(draft_logits, target_logits.dtype, "draft_logits"),
+            _dev(node_token, torch.int32, "node_token"), _dev(parent, torch.int32, "parent"),
+            _dev(u_accept, torch.float32, "u_accept"), _dev(u_resample, torch.float32, "u_resample"))
+
+
+def _tree_outputs(B, max_depth, dev, out_tokens, out_accepted_len, out_status):
+    import torch
+    if out_tokens is None:
+        out_tokens = torch.empty((B, max_depth + 1), dtype=torch.int32, device=dev)
+    if out_accepted_len is None:
+        out_accepted_len = torch.empty(B, dtype=torch.int32, device=dev)
+    if out_status is None:
+        out_status = torch.empty(B, dtype=torch.int32, device=dev)
+    _shape(out_tokens, (B, max_depth + 1), "out_tokens")
+    _shape(out_accepted_len, (B,), "out_accepted_len")
+    _shape(out_status, (B,), "out_status")
+    return out_tokens, out_accepted_len, out_status
+
+
+def resispec_verify_tree_deferred(target_logits, draft_logits, node_token, parent, u_accept,
+                                  u_resample, *, temperature, max_depth, mode="resispec",
+                                  without_replacement=False, bonus=True, out_tokens=None,
+                                  out_accepted_len=None, out_status=None, workspace=None,
+                                  stream=None):
+    """resispec_verify_tree with deferred draws (a row's draw made only where a walk ends);
+    returns (tokens [B, max_depth+1], accepted_len [B], status [B])."""
+    import torch
+    B, N, V = _tree_common(target_logits, draft_logits, node_token, parent, u_accept, u_resample,
+                           max_depth)
+    dev = target_logits.device
+    out_tokens, out_accepted_len, out_status = _tree_outputs(B, max_depth, dev, out_tokens,
+                                                             out_accepted_len, out_status)
+    if workspace is None:
+        workspace = torch.empty(max(resispec_deferred_workspace_bytes(B, N), 1),
+                                dtype=torch.uint8, device=dev)
+    prm = _params(target_logits, temperature, mode, without_replacement, bonus)
+    st = lib.resispec_verify_tree_deferred(
+        *_logit_args(target_logits, draft_logits, node_token, parent, u_accept, u_resample),
+        B, N, V, int(max_depth), ctypes.byref(prm),
+        _dev(out_tokens, torch.int32, "out_tokens"),
+        _dev(out_accepted_len, torch.int32, "out_accepted_len"),
+        _dev(out_status, torch.int32, "out_status"),
+        _dev(workspace, torch.uint8, "workspace"), workspace.numel(), _stream(stream))
+    _check(st)
+    return out_tokens, out_accepted_len, out_status
+
+
+def resispec_decide_nodes(target_logits, draft_logits, node_token, parent, u_accept, u_resample,
+                          workspace, *, temperature, mode="resispec", without_replacement=False,
+                          bonus=True, stream=None):
+    """First launch of resispec_verify_tree_deferred: every node's tests into `workspace`
+    (resispec_deferred_workspace_bytes), draws deferred where they can be."""
+    import torch
+    B, N, V = _check_tree_shapes(target_logits, draft_logits, node_token, parent, u_accept,
+                                 u_resample)
+    prm = _params(target_logits, temperature, mode, without_replacement, bonus)
+    st = lib.resispec_decide_nodes(
+        *_logit_args(target_logits, draft_logits, node_token, parent, u_accept, u_resample),
+        B, N, V, ctypes.byref(prm), _dev(workspace, torch.uint8, "workspace"), workspace.numel(),
+        _stream(stream))
+    _check(st)
+
+
+def resispec_walk_draw(target_logits, draft_logits, node_token, parent, u_accept, u_resample,
+                       workspace, *, temperature, max_depth, mode="resispec",
+                       without_replacement=False, bonus=True, out_tokens=None,
+                       out_accepted_len=None, out_status=None, stream=None):
+    """Second launch of resispec_verify_tree_deferred: the walks, with the deferred draw
+    where a walk ends; returns (tokens, accepted_len, status)."""
+    import torch
+    B, N, V = _tree_common(target_logits, draft_logits, node_token, parent, u_accept, u_resample,
+                           max_depth)
+    out_tokens, out_accepted_len, out_status = _tree_outputs(B, max_depth, target_logits.device,
+                                                             out_tokens, out_accepted_len,
+                                                             out_status)
+    prm = _params(target_logits, temperature, mode, without_replacement, bonus)
+    st = lib.resispec_walk_draw(
+        *_logit_args(target_logits, draft_logits, node_token, parent, u_accept, u_resample),
+        B, N, V, int(max_depth), ctypes.byref(prm), _dev(workspace, torch.uint8, "workspace"),
+        workspace.numel(), _dev(out_tokens, torch.int32, "out_tokens"),
+        _dev(out_accepted_len, torch.int32, "out_accepted_len"),
+        _dev(out_status, torch.int32, "out_status"), _stream(stream))
+    _check(st)
+    return out_tokens, out_accepted_len, out_status
 
 
 def resispec_verify_nodes(target_logits, draft_logits, node_token, parent, u_accept, u_resample,

@@ -40,7 +40,7 @@ def test_library_exports_every_declared_symbol(native):
 
 
 def test_abi_version_and_status_strings(native):
-    assert native.resispec_abi_version() == 2
+    assert native.resispec_abi_version() == 3
     for code in range(5):
         s = native.resispec_status_string(code)
         assert s.startswith("RS_")
@@ -118,6 +118,27 @@ def test_argument_errors_return_before_launch(native):
     assert lib.resispec_verify_tree(fake, None, i32p, i32p, fake, fake, 4, 5, 100, 2,
                                     ctypes.byref(ok), i32p, i32p, None, fake, ws,
                                     None) == native.RS_ERR_INVALID_ARG
+    # deferred draws: the larger workspace, checked by every entry point of the schedule
+    dws = native.resispec_deferred_workspace_bytes(4, 5)
+    assert dws >= ws + 4 * 5 * 2 * 128 * 8
+    wsp = ctypes.c_void_p(0x10000)
+    assert lib.resispec_verify_tree_deferred(*args, 4, 5, 100, 2, ctypes.byref(ok), i32p, i32p,
+                                             None, wsp, dws - 1, None) == native.RS_ERR_WORKSPACE
+    assert lib.resispec_verify_tree_deferred(*args, 4, 5, 100, 2, ctypes.byref(ok), i32p, i32p,
+                                             None, ctypes.c_void_p(0x10008), dws,
+                                             None) == native.RS_ERR_WORKSPACE   # misaligned
+    assert lib.resispec_decide_nodes(*args, 4, 5, 100, ctypes.byref(ok), wsp, ws,
+                                     None) == native.RS_ERR_WORKSPACE
+    assert lib.resispec_walk_draw(*args, 4, 5, 100, 2, ctypes.byref(ok), wsp, dws - 1, i32p, i32p,
+                                  None, None) == native.RS_ERR_WORKSPACE
+    assert lib.resispec_walk_draw(*args, 4, 5, 100, -1, ctypes.byref(ok), wsp, dws, i32p, i32p,
+                                  None, None) == native.RS_ERR_INVALID_ARG
+    assert lib.resispec_decide_nodes(*args, 4, 5, 100, ctypes.byref(_prm(native, T=0.0)), wsp,
+                                     dws, None) == native.RS_ERR_INVALID_ARG
+    assert lib.resispec_verify_tree_deferred(*args, 0, 5, 100, 2, ctypes.byref(ok), None, None,
+                                             None, None, 0, None) == native.RS_OK   # B = 0
+    assert native.resispec_deferred_workspace_bytes(0, 5) == 0
+    assert native.resispec_deferred_workspace_bytes(5, 0) == 0
     assert lib.resispec_verify_tree(None, None, None, None, None, None, 0, 5, 100, 2,
                                     ctypes.byref(ok), None, None, None, None, 0,
                                     None) == native.RS_OK

@@ -180,7 +180,8 @@ def _full_workload(cfg):
 def test_tree_parity_full_size_walk(gpu_lib, cfg, mode):
     """Full configurations in the launch shape the benchmark times: the walk of every
     sequence against the oracle's sequential walk (exact outside the window, admissible
-    inside it), for the all-nodes step and for the path-only schedule."""
+    inside it), for the all-nodes step, the path-only schedule and the all-nodes schedule
+    with deferred draws."""
     _log("full-size walk parity", cfg, mode)
     w, h = _full_workload(cfg)
     plain = gpu_tree(gpu_lib, w, mode)
@@ -196,6 +197,14 @@ def test_tree_parity_full_size_walk(gpu_lib, cfg, mode):
     torch.cuda.synchronize()
     assert torch.equal(pt, plain["tokens"]) and torch.equal(pl, plain["accepted_len"])
     assert torch.equal(ps, plain["status"])
+    # the all-nodes schedule with deferred draws
+    dt, dl, ds = gpu_lib.resispec_verify_tree_deferred(
+        w["target"], w["draft"], w["node_token"], w["parent"], w["u_accept"], w["u_resample"],
+        temperature=w["temperature"], max_depth=w["max_depth"], mode=mode,
+        without_replacement=w["without_replacement"])
+    torch.cuda.synchronize()
+    assert torch.equal(dt, plain["tokens"]) and torch.equal(dl, plain["accepted_len"])
+    assert torch.equal(ds, plain["status"])
 
 
 @pytest.mark.parametrize("mode", MODES)
