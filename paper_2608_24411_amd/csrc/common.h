@@ -283,17 +283,17 @@ struct Smem {
 };
 
 // Per-slot sums of the lane partials of a pass, in a fixed order, so the totals are
-// bitwise reproducible whatever wave processed which slot.  Stage 1 (every thread, for
-// the slots in [s_lo, s_hi)): thread t adds lanes [g*GS, g*GS + GS) of slot
-// t % kMaxSlots, g = t / kMaxSlots, in fp64 and parks the sum in rows g*GS and
-// g*GS + 1 of that column as two 32-bit halves (no other thread touches those cells).  Stage 2, after a barrier
-// (slot_group_sum): the NG group sums of one slot are added in group order.
+// bitwise reproducible whatever wave processed which slot, and whatever the block size.
+// Stage 1 (the first NG * kMaxSlots threads, for the slots in [s_lo, s_hi)): thread t
+// adds lanes [g*GS, g*GS + GS) of slot t % kMaxSlots, g = t / kMaxSlots, in fp64 and
+// parks the sum in rows g*GS and g*GS + 1 of that column as two 32-bit halves (no other
+// thread touches those cells).  Stage 2, after a barrier (slot_group_sum): the NG group
+// sums of one slot are added in group order.
 template <int BLK>
 struct SlotGroups {
-    static constexpr int NG = BLK / kMaxSlots;
+    static constexpr int NG = 4;
     static constexpr int GS = 64 / NG;
-    static_assert(NG >= 1 && NG * kMaxSlots == BLK && NG * GS == 64 && GS >= 2,
-                  "the block must split the 64 lanes into equal groups per slot");
+    static_assert(NG * kMaxSlots <= BLK, "the block must hold a thread per group and slot");
 };
 
 __device__ __forceinline__ void park_double(float (&part)[64][kMaxSlots + 1], int r, int s, double v) {
@@ -306,7 +306,7 @@ template <int BLK>
 __device__ __forceinline__ void slot_sums_stage1(Smem& sm, int s_lo, int s_hi, bool wantB) {
     using SG = SlotGroups<BLK>;
     const int s = threadIdx.x % kMaxSlots, g = threadIdx.x / kMaxSlots;
-    if (s < s_lo || s >= s_hi) return;
+    if (g >= SG::NG || s < s_lo || s >= s_hi) return;
     double a = 0.0, c = 0.0;
 #pragma unroll
     for (int l = 0; l < SG::GS; ++l) a += (double)sm.partA[g * SG::GS + l][s];
@@ -323,7 +323,7 @@ template <int BLK>
 __device__ __forceinline__ void slot_sums_stage1_one(float (&part)[64][kMaxSlots + 1], int s_lo, int s_hi) {
     using SG = SlotGroups<BLK>;
     const int s = threadIdx.x % kMaxSlots, g = threadIdx.x / kMaxSlots;
-    if (s < s_lo || s >= s_hi) return;
+    if (g >= SG::NG || s < s_lo || s >= s_hi) return;
     double a = 0.0;
 #pragma unroll
     for (int l = 0; l < SG::GS; ++l) a += (double)part[g * SG::GS + l][s];

@@ -482,6 +482,9 @@ __device__ __forceinline__ void wave_sweep_rc(const float* __restrict__ rc, cons
 // of pass 1, and every step after them is the same code on the same values, so the
 // token is the one the row would have drawn at once.
 constexpr int kSchedAll = 0, kSchedDecide = 1, kSchedResume = 2;
+// waves whose first chunk enters the exponent reference (the waves of a 512-thread block;
+// larger blocks take the same chunks, so every kernel uses the same reference)
+constexpr int kRefWaves = 8;
 constexpr int64_t kStateDoubles = 2 * kMaxSlots;
 
 // A deferred row's pass-1 slot totals: the target row's, then (rows with children) the
@@ -540,7 +543,7 @@ __device__ __forceinline__ void verify_row(const KParams& P, Smem& sm, const int
         sm.hit_slots[w] = 0u;
         sm.cand_slots[w] = 0u;
     }
-    // The maximum over the first chunks of the first slots (chunk w * G for wave w) fixes
+    // The maximum over the first chunks of the first slots (chunk w * G for wave w < 8) fixes
     // the row's exponent reference, the same in every schedule and in every member of a
     // row group: each wave requested its chunk above, except in members whose slots start
     // later, which load those chunks' target parts here.  Elements past the row's end
@@ -549,6 +552,7 @@ __device__ __forceinline__ void verify_row(const KParams& P, Smem& sm, const int
         float mx = -FLT_MAX;
 #pragma unroll
         for (int u = 0; u < UNR; ++u) {
+            if (wid >= kRefWaves) break;   // the reference uses the first kRefWaves chunks
             const int idx = wid * G * CHUNK + lane * VEC + u * 64 * VEC;
             typename W::raw r = pre[u];
             if (SPLIT && s0 != 0) r = W::template load<false>(tg, idx, V);
@@ -1720,7 +1724,7 @@ struct WalkEnd {
 // and read across lanes as the walk steps (a child's index is larger than its parent's,
 // so a new window is loaded only when the walk passes the current one).  Node ov_node
 // takes the outcome (ov_child, ov_tok, ov_status) instead of the stored one (-1: none).
-__device__ WalkEnd walk_wave(const int32_t* __restrict__ node_child, const int32_t* __restrict__ node_tok,
+__device__ __forceinline__ WalkEnd walk_wave(const int32_t* __restrict__ node_child, const int32_t* __restrict__ node_tok,
                              const int32_t* __restrict__ node_status, const int32_t* __restrict__ node_token,
                              int64_t base, int32_t N, int32_t max_depth, int32_t* __restrict__ out,
                              int32_t ov_node, int32_t ov_child, int32_t ov_tok, int32_t ov_status) {
@@ -1779,7 +1783,7 @@ __device__ WalkEnd walk_wave(const int32_t* __restrict__ node_child, const int32
 
 // The sequence's outputs once its walk has ended: on a fault every token and the length
 // are -1.  Lane 0 writes.
-__device__ void walk_finish(const WalkEnd& we, int64_t W, int32_t* __restrict__ out, int32_t b,
+__device__ __forceinline__ void walk_finish(const WalkEnd& we, int64_t W, int32_t* __restrict__ out, int32_t b,
                             int32_t* __restrict__ out_len, int32_t* __restrict__ out_status) {
     if ((threadIdx.x & 63) != 0) return;
     int32_t len = we.len;
@@ -1829,11 +1833,16 @@ __global__ void __launch_bounds__(kBlock) __attribute__((amdgpu_waves_per_eu(4))
 // Second launch: one workgroup per sequence walks the decided outcomes; where the walk
 // ends at a row whose draw was deferred, the workgroup takes that row up again (its slot
 // totals from the first launch, then its rejection pass and its draw, or the bonus draw
-// of a leaf), records the node's outcome and finishes the walk with it.
+// of a leaf), records the node's outcome and finishes the walk with it.  Its workgroups
+// are few (one per sequence) and each streams one row alone, so they take 16 waves: twice
+// the row kernel's loads in flight.
+constexpr int kFinishBlock = 1024;
+
 template <typename In, int VEC, int UNR, int MODE>
-__global__ void __launch_bounds__(kBlock) __attribute__((amdgpu_waves_per_eu(4)))
+__global__ void __launch_bounds__(kFinishBlock)
 rs_finish_kernel(const KParams P, int32_t max_depth, int32_t* __restrict__ out_tokens,
                  int32_t* __restrict__ out_len, int32_t* __restrict__ out_status) {
+    constexpr int kBlock = kFinishBlock;
     __shared__ Smem sm;
     __shared__ int32_t s_node;
     const int32_t b = blockIdx.x;
@@ -1853,22 +1862,22 @@ rs_finish_kernel(const KParams P, int32_t max_depth, int32_t* __restrict__ out_t
         return;
     }
     const int64_t row = base + n;
-    int32_t oc = -1, ot = -1, os = RS_SEQ_OK;   // the row's outcome (thread 0)
     RowGroup solo{1, 0, nullptr, nullptr, 0u, kGroupWaitTicks};
     verify_row<In, VEC, UNR, MODE, kBlock, false, false, kSchedResume>(
         P, sm, row, b, n,
         [&](int32_t child, int32_t tok, int32_t st) {
             write_outcome(P, row, child, tok, st);
-            oc = child;
-            ot = tok;
-            os = st;
+            sm.res_child = child;
+            sm.res_tok = tok;
+            sm.res_status = st;
         },
         solo);
-    // thread 0 holds the outcome; wave 0 walks again with it in place of the deferred one
+    __syncthreads();
+    // wave 0 walks again with the row's outcome in place of the deferred one
     if (threadIdx.x < 64) {
-        oc = __builtin_amdgcn_readfirstlane(oc);
-        ot = __builtin_amdgcn_readfirstlane(ot);
-        os = __builtin_amdgcn_readfirstlane(os);
+        const int32_t os = __builtin_amdgcn_readfirstlane(sm.res_status);
+        int32_t oc = __builtin_amdgcn_readfirstlane(sm.res_child);
+        int32_t ot = __builtin_amdgcn_readfirstlane(sm.res_tok);
         if (os != RS_SEQ_OK) oc = ot = -1;
         we = walk_wave(P.node_child, P.node_tok, P.node_status, P.node_token, base, P.N, max_depth, out, n, oc, ot,
                        os);
@@ -2141,7 +2150,7 @@ hipError_t launch_deferred(KParams P, bool finish, int32_t max_depth, int32_t* o
                            int32_t* out_status, hipStream_t s) {
     set_slots<VEC, UNR>(P);
     if (finish)
-        hipLaunchKernelGGL((rs_finish_kernel<In, VEC, UNR, MODE>), dim3((unsigned)P.B), dim3(kBlock), 0, s, P,
+        hipLaunchKernelGGL((rs_finish_kernel<In, VEC, UNR, MODE>), dim3((unsigned)P.B), dim3(kFinishBlock), 0, s, P,
                            max_depth, out_tokens, out_len, out_status);
     else
         hipLaunchKernelGGL((rs_decide_kernel<In, VEC, UNR, MODE>), dim3((unsigned)((int64_t)P.B * P.N)),
