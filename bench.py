@@ -3,15 +3,17 @@
 
 One step = one full verification of a batch of draft trees on inputs already resident in
 HBM, in the all-nodes schedule with deferred draws: the decide kernel tests every node
-row (a row that rejects its one candidate, and a leaf, keep their slot totals instead of
-drawing), then the walk kernel follows accepted children from each root and draws where a
-walk ends.  Prints one JSON line.
+row (a row that rejects its one candidate keeps its slot totals instead of drawing, and a
+leaf's row, which serves only its bonus draw, is left whole), then the finish kernel
+follows accepted children from each root and draws where a walk ends.  Prints one JSON
+line.
 
   python bench.py [--gpus 1] [--steps 20] [--warmup 5] [--config 2] [--mode resispec]
 
 The metric is verified tree-node rows per second (B * N / step time) at V = 128,256;
-`roofline.achieved` is the decide kernel's algorithmic bytes (every target row once, the
-draft row of every node with children once, plus ids/uniforms/outcomes) divided by its
+`roofline.achieved` is the decide kernel's algorithmic bytes (the target and draft rows of
+every node with children once, plus ids/uniforms/outcomes; a leaf's row serves only its
+bonus draw and is read by the walk where it ends) divided by its
 average launch duration measured with HIP events on the launch stream.  The read probe
 (libresispec_probe.so) measures the device's achievable read rate beside it:
 `roofline.frac_of_read_ceiling` is the achieved figure over the nontemporal stream rate.
@@ -328,7 +330,8 @@ def configs_record(native, torch, np, synth, steps, warmup, mode, headline):
             continue
         B, N, V = w["B"], w["N"], w["V"]
         logit_bytes, rows_t, rows_d = synth.algorithmic_bytes(w["parent"].cpu().numpy(), V, esz)
-        alg = logit_bytes + 28 * B * N
+        alg = 2 * rows_d * V * esz + 28 * B * N        # the decide kernel's rows
+        alg_all = logit_bytes + 28 * B * N             # every row drawing
         ws = torch.empty(native.resispec_deferred_workspace_bytes(B, N), dtype=torch.uint8,
                          device="cuda")
         args = (w["target"], w["draft"], w["node_token"], w["parent"], w["u_accept"], w["u_resample"])
@@ -353,12 +356,13 @@ def configs_record(native, torch, np, synth, steps, warmup, mode, headline):
         step_ms = float(np.mean(_event_ms(torch, whole, steps, warmup)))
         all_ms = float(np.mean(_event_ms(torch, every_row_draws, steps, warmup)))
         rec = {"B": B, "N": N, "V": V, "logits": "bf16" if esz == 2 else "f32",
-               "rows_target": rows_t, "rows_draft": rows_d, "alg_bytes_per_launch": alg,
+               "rows_target": rows_d, "rows_draft": rows_d, "alg_bytes_per_launch": alg,
                "decide_kernel_ms": kms, "decide_kernel_ms_min": float(np.min(ms)),
                "step_ms": step_ms, "rows_per_s": B * N / (step_ms * 1e-3),
                "achieved_gbps": alg / (kms * 1e-3) / 1e9,
                "frac": alg / (kms * 1e-3) / 1e9 / HBM_PEAK_GBPS,
-               "all_nodes_draw_row_kernel_ms": all_ms}
+               "all_nodes_draw_row_kernel_ms": all_ms,
+               "all_nodes_draw_frac": alg_all / (all_ms * 1e-3) / 1e9 / HBM_PEAK_GBPS}
         if cfg == 1:
             flush_buf = torch.empty(512 << 20, dtype=torch.uint8, device="cuda")
             fill = [0]
@@ -531,7 +535,11 @@ def main():
     esz = 2 if w["target"].dtype == torch.bfloat16 else 4
     logit_bytes, rows_t, rows_d = synth.algorithmic_bytes(w["parent"].cpu().numpy(), V, esz)
     small_bytes = 16 * B * N + 12 * B * N      # ids, parents, uniforms in; outcomes out
-    alg_bytes = logit_bytes + small_bytes
+    # every row drawing: every target row and the draft row of every node with children
+    alg_bytes_all = logit_bytes + small_bytes
+    # the decide kernel: both rows of every node with children (a leaf's row serves only
+    # its bonus draw, which the walk makes where it ends)
+    alg_bytes = 2 * rows_d * V * esz + small_bytes
 
     # the deferred schedule's workspace also holds the other schedule's node outcomes
     ws = torch.empty(native.resispec_deferred_workspace_bytes(B, N), dtype=torch.uint8,
@@ -578,8 +586,9 @@ def main():
                      "ms_per_step": 1e3 * wall / args.steps,
                      "rows_per_s": B * N / (wall / args.steps),
                      "row_kernel_ms": kms, "row_kernel_ms_min": float(np.min(kern_ms)),
-                     "row_kernel_gbps": alg_bytes / (kms * 1e-3) / 1e9,
-                     "row_kernel_frac": alg_bytes / (kms * 1e-3) / 1e9 / HBM_PEAK_GBPS,
+                     "row_kernel_alg_bytes": alg_bytes_all,
+                     "row_kernel_gbps": alg_bytes_all / (kms * 1e-3) / 1e9,
+                     "row_kernel_frac": alg_bytes_all / (kms * 1e-3) / 1e9 / HBM_PEAK_GBPS,
                      "walk_ms": float(np.mean(walk_ms))}
 
     # the path-only schedule of the same step (only the nodes each walk reaches)
@@ -736,7 +745,7 @@ def main():
                      "frac": achieved / HBM_PEAK_GBPS,
                      "traffic": traffic,
                      "kernel": "rs_decide_kernel", "alg_bytes_per_launch": alg_bytes,
-                     "rows_target": rows_t, "rows_draft": rows_d,
+                     "rows_target": rows_d, "rows_draft": rows_d, "leaf_rows_left_to_the_walk": rows_t - rows_d,
                      # HBM traffic (counters) per second, against the measured read ceiling
                      "traffic_gbps": (traffic / (r["decide_kernel_ms"] * 1e-3) / 1e9
                                       if traffic else None),
@@ -752,7 +761,7 @@ def main():
     }
     if not args.no_configs:
         headline = {"B": B, "N": N, "V": V, "logits": "bf16" if esz == 2 else "f32",
-                    "rows_target": rows_t, "rows_draft": rows_d, "alg_bytes_per_launch": alg_bytes,
+                    "rows_target": rows_d, "rows_draft": rows_d, "alg_bytes_per_launch": alg_bytes,
                     "decide_kernel_ms": r["decide_kernel_ms"],
                     "decide_kernel_ms_min": r["decide_kernel_ms_min"],
                     "walk_draw_ms": r["walk_draw_ms"],

@@ -4,6 +4,7 @@ import os
 import re
 import subprocess
 import sys
+import tempfile
 
 HERE = os.path.dirname(os.path.abspath(__file__))
 ROOT = os.path.dirname(HERE)
@@ -22,9 +23,13 @@ FLAGS = [
 ]
 
 
-def _spills(report):
+def _spills(report, scratch_users=None):
     """Functions whose registers spill to scratch memory, from the compiler's resource
-    remarks: [(name, vgpr_spills, scratch_bytes_per_lane)]."""
+    remarks: [(name, vgpr_spills, scratch_bytes_per_lane)].  Any VGPR spill counts.  A
+    private segment without VGPR spills counts when the function's device assembly
+    accesses scratch memory (scratch_users: the names of such functions), or whenever the
+    assembly was not looked at (scratch_users None).  The register allocator sometimes
+    reserves a frame that no instruction uses."""
     bad, name, scratch = [], None, 0
     for line in report.splitlines():
         m = re.search(r"Function Name: (\S+)", line)
@@ -36,18 +41,45 @@ def _spills(report):
             scratch = int(m.group(1))
             continue
         m = re.search(r"VGPRs Spill: (\d+)", line)
-        if m and name and (int(m.group(1)) > 0 or scratch > 0):
-            bad.append((name, int(m.group(1)), scratch))
+        if m and name:
+            used = scratch > 0 and (scratch_users is None or name in scratch_users)
+            if int(m.group(1)) > 0 or used:
+                bad.append((name, int(m.group(1)), scratch))
     return bad
+
+
+_SCRATCH_OP = re.compile(r"^\s+(scratch_(load|store)|buffer_(load|store)|buffer_atomic)\w*\b")
+
+
+def _scratch_users(asm_text):
+    """Names of the functions of a device assembly listing whose instructions access
+    scratch (private) memory."""
+    users, name = set(), None
+    for line in asm_text.splitlines():
+        m = re.match(r"^([A-Za-z_][\w.$]*):", line)
+        if m and not m.group(1).startswith(".L"):
+            name = m.group(1)
+            continue
+        if name and _SCRATCH_OP.match(line):
+            users.add(name)
+    return users
 
 
 def _compile(srcs, lib, verbose, extra=()):
     tmp = lib + ".tmp%d" % os.getpid()
-    cmd = ([HIPCC] + FLAGS + list(extra) + ["-Rpass-analysis=kernel-resource-usage", "-I",
-                                            os.path.join(ROOT, "include"), "-o", tmp] + srcs)
+    # -save-temps keeps the device assembly (in a scratch directory) for the scratch check
+    cmd = ([HIPCC] + FLAGS + list(extra) + ["-Rpass-analysis=kernel-resource-usage", "-save-temps",
+                                            "-I", os.path.join(ROOT, "include"), "-o", tmp] + srcs)
     if verbose:
         print(" ".join(cmd), flush=True)
-    r = subprocess.run(cmd, capture_output=True, text=True)
+    with tempfile.TemporaryDirectory() as work:
+        r = subprocess.run(cmd, capture_output=True, text=True, cwd=work)
+        asm = [os.path.join(work, f) for f in os.listdir(work)
+               if f.endswith(".s") and "amdgcn" in f and "gfx950" in f]
+        users = set()
+        for path in asm:
+            with open(path) as fh:
+                users |= _scratch_users(fh.read())
     other = [l for l in r.stderr.splitlines()
              if "kernel-resource-usage" not in l and "packed-fp32-ops" not in l and l.strip()]
     if r.returncode != 0:
@@ -58,7 +90,7 @@ def _compile(srcs, lib, verbose, extra=()):
     # A register spilled inside a branch that only some lanes take is stored for those
     # lanes alone; a value that other lanes still hold would come back from stale
     # scratch.  Every kernel is built to fit its registers, and the build checks it.
-    bad = _spills(r.stderr)
+    bad = _spills(r.stderr, users if asm else None)
     if bad:
         os.remove(tmp)
         raise RuntimeError("registers spill to scratch in: " +

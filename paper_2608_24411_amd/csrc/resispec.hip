@@ -474,13 +474,14 @@ __device__ __forceinline__ void wave_sweep_rc(const float* __restrict__ rc, cons
 // in P.rcache when the caller's workspace holds it (see the rejection passes below).
 // How a row's draw is scheduled.  kSchedAll: every row that rejects all its candidates,
 // or has none, draws at once (the all-nodes and path schedules).  kSchedDecide: a row with
-// one candidate that it rejects, and a leaf, stop after their tests; they keep their
-// pass-1 slot totals in P.dstate and report RS_SEQ_DEFERRED, because the token they would
-// draw is used only if a walk ends there (a row with several candidates needs its
-// rejection passes for its later tests anyway, and draws at once).  kSchedResume: such a
-// row is taken up again where its walk ends: the slot totals come from P.dstate instead
-// of pass 1, and every step after them is the same code on the same values, so the
-// token is the one the row would have drawn at once.
+// one candidate that it rejects stops after its test, keeps its pass-1 slot totals in
+// P.dstate and reports RS_SEQ_DEFERRED, because the token it would draw is used only if
+// a walk ends there (a row with several candidates needs its rejection passes for its
+// later tests anyway, and draws at once); a leaf, whose row serves only its bonus draw,
+// reports RS_SEQ_DEFERRED without reading its row.  kSchedResume: such a row is taken up
+// again where its walk ends: the slot totals come from P.dstate instead of pass 1 (a leaf
+// takes its pass 1 then), and every step after them is the same code on the same values,
+// so the token is the one the row would have drawn at once.
 constexpr int kSchedAll = 0, kSchedDecide = 1, kSchedResume = 2;
 // waves whose first chunk enters the exponent reference (the waves of a 512-thread block;
 // larger blocks take the same chunks, so every kernel uses the same reference)
@@ -489,13 +490,12 @@ constexpr int64_t kStateDoubles = 2 * kMaxSlots;
 
 // A deferred row's pass-1 slot totals: the target row's, then (rows with children) the
 // draft row's.
-__device__ __forceinline__ void keep_slot_totals(const KParams& P, const Smem& sm, int64_t row, int nslots,
-                                                 bool internal) {
+__device__ __forceinline__ void keep_slot_totals(const KParams& P, const Smem& sm, int64_t row, int nslots) {
     double* st = P.dstate + row * kStateDoubles;
     const int tid = threadIdx.x;
     if (tid < nslots) {
         st[tid] = sm.slotP[tid];
-        if (internal) st[kMaxSlots + tid] = sm.slotB[tid];
+        st[kMaxSlots + tid] = sm.slotB[tid];
     }
 }
 
@@ -665,6 +665,14 @@ __device__ __forceinline__ void verify_row(const KParams& P, Smem& sm, const int
         zero_residual_row(P, row);
         return;
     }
+    if constexpr (SCHED == kSchedDecide) {
+        // A leaf: its row serves only the bonus draw, which is used only if a walk ends
+        // here, so the row is left whole to the walk (it is not read here).
+        if (nc == 0 && !P.flat) {
+            if (tid == 0) emit(-1, -1, RS_SEQ_DEFERRED);
+            return;
+        }
+    }
     if (tid == 0) sm.status = RS_SEQ_OK;
     // candidate logits (their latency overlaps the first chunk's)
     float hlt = 0.0f, hld = 0.0f;
@@ -674,6 +682,12 @@ __device__ __forceinline__ void verify_row(const KParams& P, Smem& sm, const int
     }
 
     const bool internal = nc > 0;
+    if constexpr (SCHED == kSchedDecide) {
+        // A row with several candidates may take many rejection passes, and the later
+        // ResiSpec ones re-derive the chain of earlier steps per element (ALU-bound): such
+        // rows end last.  Their waves issue ahead of the other workgroup's on the CU.
+        if (nc >= 2) __builtin_amdgcn_s_setprio(3);
+    }
     const float c2h = P.c2h, c2l = P.c2l;
 
     // ---- pass 1: softmax statistics.  Both rows are summed against one exponent
@@ -737,8 +751,9 @@ __device__ __forceinline__ void verify_row(const KParams& P, Smem& sm, const int
             if (internal) sm.partB[lane][slot] = fc;
             fa = fc = 0.0f;
         };
-        if constexpr (SCHED == kSchedResume) {
-            // the slot totals pass 1 gave this row when its draw was deferred
+        if (SCHED == kSchedResume && internal) {
+            // the slot totals pass 1 gave this row when its draw was deferred (a leaf takes
+            // its pass 1 here)
             const double* st = P.dstate + row * kStateDoubles;
             if (tid < nslots) {
                 const double a = st[tid];
@@ -914,17 +929,10 @@ __device__ __forceinline__ void verify_row(const KParams& P, Smem& sm, const int
         }
     }
 
-    // Deferred draws: the row keeps its pass-1 slot totals and reports RS_SEQ_DEFERRED.
-    // Rows that took the exact-maximum pass draw at once (their exponent references are
-    // not the ones a resumed row derives).
+    // Deferred draws: a row with one candidate that it rejects keeps its pass-1 slot totals
+    // and reports RS_SEQ_DEFERRED.  Rows that took the exact-maximum pass draw at once
+    // (their exponent references are not the ones a resumed row derives).
     const bool deferrable = SCHED == kSchedDecide && !P.flat && !refixed;
-    if constexpr (SCHED == kSchedDecide) {
-        if (deferrable && nc == 0) {   // a leaf: the bonus draw is used only if a walk ends here
-            keep_slot_totals(P, sm, row, nslots, false);
-            if (tid == 0) emit(-1, -1, RS_SEQ_DEFERRED);
-            return;
-        }
-    }
 
     const double St = sm.St, Sd = sm.Sd;
     // draft mass in target units: q St / Sd, folded into the step constants
@@ -1007,7 +1015,7 @@ __device__ __forceinline__ void verify_row(const KParams& P, Smem& sm, const int
         // one candidate, rejected: the draw from the residual is used only if a walk ends here
         if constexpr (SCHED == kSchedDecide) {
             if (deferrable && nc == 1) {
-                keep_slot_totals(P, sm, row, nslots, true);
+                keep_slot_totals(P, sm, row, nslots);
                 if (tid == 0) emit(-1, -1, RS_SEQ_DEFERRED);
                 return;
             }
@@ -1783,7 +1791,7 @@ __device__ __forceinline__ WalkEnd walk_wave(const int32_t* __restrict__ node_ch
 
 // The sequence's outputs once its walk has ended: on a fault every token and the length
 // are -1.  Lane 0 writes.
-__device__ __forceinline__ void walk_finish(const WalkEnd& we, int64_t W, int32_t* __restrict__ out, int32_t b,
+__device__ __forceinline__ void walk_finish(const WalkEnd we, int64_t W, int32_t* __restrict__ out, int32_t b,
                             int32_t* __restrict__ out_len, int32_t* __restrict__ out_status) {
     if ((threadIdx.x & 63) != 0) return;
     int32_t len = we.len;
@@ -1833,13 +1841,15 @@ __global__ void __launch_bounds__(kBlock) __attribute__((amdgpu_waves_per_eu(4))
 // Second launch: one workgroup per sequence walks the decided outcomes; where the walk
 // ends at a row whose draw was deferred, the workgroup takes that row up again (its slot
 // totals from the first launch, then its rejection pass and its draw, or the bonus draw
-// of a leaf), records the node's outcome and finishes the walk with it.  Its workgroups
-// are few (one per sequence) and each streams one row alone, so they take 16 waves: twice
-// the row kernel's loads in flight.
-constexpr int kFinishBlock = 1024;
+// of a leaf: pass 1, then the draw), records the node's outcome and finishes the walk
+// with it.  Its workgroups are few (one per sequence), each streaming a row alone, so
+// they take 12 waves (1.5 times the row kernel's loads in flight) and up to 168
+// registers per lane: the row's code for a leaf, a single-candidate rejection and a row
+// of several candidates is all in this kernel.
+constexpr int kFinishBlock = 768;
 
 template <typename In, int VEC, int UNR, int MODE>
-__global__ void __launch_bounds__(kFinishBlock)
+__global__ void __launch_bounds__(kFinishBlock) __attribute__((amdgpu_waves_per_eu(2)))
 rs_finish_kernel(const KParams P, int32_t max_depth, int32_t* __restrict__ out_tokens,
                  int32_t* __restrict__ out_len, int32_t* __restrict__ out_status) {
     constexpr int kBlock = kFinishBlock;

@@ -256,6 +256,15 @@ def test_build_rejects_register_spills():
         "x.hip:12:1: remark:     VGPRs Spill: 0 [-Rpass-analysis=kernel-resource-usage]",
     ])
     assert build._spills(report) == [("k_bad", 50, 204), ("k_stack", 0, 16)]
+    # with the device assembly: a frame that no instruction uses is not a spill
+    asm = "\n".join([
+        "k_ok:", "\ts_load_dwordx4 s[4:7], s[0:1], 0x0", "\tglobal_load_dwordx4 v[0:3], v4, s[4:5]",
+        "k_stack:", "\tv_mov_b32_e32 v1, 0", ".LBB2_1:", "\ts_endpgm",
+        "k_bad:", "\tscratch_store_dword off, v7, s33 offset:4", "\tbuffer_load_dword v3, off, s[0:3], 0",
+    ])
+    users = build._scratch_users(asm)
+    assert users == {"k_bad"}
+    assert build._spills(report, users) == [("k_bad", 50, 204)]
 
 
 def test_plain_c_caller(tmp_path):
