@@ -529,6 +529,16 @@ __device__ __forceinline__ void verify_row(const KParams& P, Smem& sm, const int
     typename W::raw pre[UNR];
 #pragma unroll
     for (int u = 0; u < UNR; ++u) pre[u] = W::template load<kNtPass1>(tg, (s0 + wid) * G * CHUNK + lane * VEC + u * 64 * VEC, V);
+    // A resumed row's stored slot totals are requested at once too (a leaf stored none;
+    // its values are not used).
+    double kept_a = 0.0, kept_b = 0.0;
+    if constexpr (SCHED == kSchedResume) {
+        if (tid < nslots) {
+            const double* st = P.dstate + row * kStateDoubles;
+            kept_a = st[tid];
+            kept_b = st[kMaxSlots + tid];
+        }
+    }
 
     // ---- row description.  "Holder" threads own one candidate each: node, token and
     // uniform, then the two logits of its token and their unnormalised masses, all
@@ -754,12 +764,10 @@ __device__ __forceinline__ void verify_row(const KParams& P, Smem& sm, const int
         if (SCHED == kSchedResume && internal) {
             // the slot totals pass 1 gave this row when its draw was deferred (a leaf takes
             // its pass 1 here)
-            const double* st = P.dstate + row * kStateDoubles;
             if (tid < nslots) {
-                const double a = st[tid];
-                sm.slotA[tid] = a;
-                sm.slotP[tid] = a;
-                sm.slotB[tid] = internal ? st[kMaxSlots + tid] : 0.0;
+                sm.slotA[tid] = kept_a;
+                sm.slotP[tid] = kept_a;
+                sm.slotB[tid] = kept_b;
             }
             __syncthreads();
         } else {
@@ -1883,14 +1891,20 @@ rs_finish_kernel(const KParams P, int32_t max_depth, int32_t* __restrict__ out_t
         },
         solo);
     __syncthreads();
-    // wave 0 walks again with the row's outcome in place of the deferred one
     if (threadIdx.x < 64) {
         const int32_t os = __builtin_amdgcn_readfirstlane(sm.res_status);
         int32_t oc = __builtin_amdgcn_readfirstlane(sm.res_child);
         int32_t ot = __builtin_amdgcn_readfirstlane(sm.res_tok);
         if (os != RS_SEQ_OK) oc = ot = -1;
-        we = walk_wave(P.node_child, P.node_tok, P.node_status, P.node_token, base, P.N, max_depth, out, n, oc, ot,
-                       os);
+        if (oc < 0) {
+            // the walk ends here: the row's token (or its fault) completes the first walk
+            if (os == RS_SEQ_OK && ot >= 0 && threadIdx.x == 0) out[we.len] = ot;
+            we.status = os;
+        } else {
+            // (a resumed row repeats the test that deferred it, so this does not happen)
+            we = walk_wave(P.node_child, P.node_tok, P.node_status, P.node_token, base, P.N, max_depth, out, n,
+                           oc, ot, os);
+        }
         walk_finish(we, W, out, b, out_len, out_status);
     }
 }
