@@ -805,7 +805,7 @@ __device__ __forceinline__ void verify_row(const KParams& P, Smem& sm, const int
                         }
                 },
                 flush, &sm.nt_hint);
-        } else {
+        } else if constexpr (SCHED != kSchedDecide) {   // (the decide kernel reads no leaf row)
             wave_sweep<In, VEC, UNR, false, 1, kNtLeaf, true>(tg, dg, V, G, nl, s0, false, pre, pre, &sm.next_slot,
                 [&](const float (&t)[UNR][VEC], const float (&)[UNR][VEC], int, int) {
 #pragma unroll

@@ -90,6 +90,22 @@ def test_graph_all_nodes(gpu_lib, mode):
 
 
 @pytest.mark.parametrize("mode", ["resispec", "specinfer"])
+def test_graph_deferred(gpu_lib, mode):
+    """The all-nodes schedule with deferred draws: both launches in the graph; replays whose
+    new uniforms move the walks' ends to other rows still agree with eager calls."""
+    w = synth.make_workload(2, device="cuda", B=4, V=40000)
+    ws = torch.empty(gpu_lib.resispec_deferred_workspace_bytes(w["B"], w["N"]), dtype=torch.uint8,
+                     device="cuda")
+
+    def step(out):
+        gpu_lib.resispec_verify_tree_deferred(*_tree_args(w), **_kw(w, mode), workspace=ws,
+                                              out_tokens=out["tokens"],
+                                              out_accepted_len=out["accepted_len"],
+                                              out_status=out["status"])
+    _check_replays(w, step, "deferred " + mode)
+
+
+@pytest.mark.parametrize("mode", ["resispec", "specinfer"])
 def test_graph_path_groups(gpu_lib, mode):
     """The path schedule with row groups: the counter-clearing kernel and the group launch
     are both in the graph."""
