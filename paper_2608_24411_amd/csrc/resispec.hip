@@ -696,7 +696,9 @@ __device__ __forceinline__ void verify_row(const KParams& P, Smem& sm, const int
         // A row with several candidates may take many rejection passes, and the later
         // ResiSpec ones re-derive the chain of earlier steps per element (ALU-bound): such
         // rows end last.  Their waves issue ahead of the other workgroup's on the CU.
-        if (nc >= 2) __builtin_amdgcn_s_setprio(3);
+        if (nc >= 4) __builtin_amdgcn_s_setprio(3);
+        else if (nc == 3) __builtin_amdgcn_s_setprio(2);
+        else if (nc == 2) __builtin_amdgcn_s_setprio(1);
     }
     const float c2h = P.c2h, c2l = P.c2l;
 
