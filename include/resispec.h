@@ -182,6 +182,8 @@ rs_status resispec_verify_tree_deferred(const void* target_logits, const void* d
  *     draw where a walk ends (same inputs, and the workspace written by
  *     resispec_decide_nodes with the same B and N, earlier on the same stream); it
  *     records the outcome of each node it draws for in the workspace.
+ * resispec_walk over such a workspace draws nothing: a walk that ends at a deferred node
+ * reports RS_SEQ_DEFERRED as its status.
  */
 rs_status resispec_decide_nodes(const void* target_logits, const void* draft_logits,
                                 const int32_t* node_token, const int32_t* parent,
@@ -389,7 +391,9 @@ rs_status resispec_walk(const int32_t* node_token, int32_t B, int32_t N, int32_t
  * Every node's own outcome as resispec_verify_nodes left it in `workspace` (the same
  * B and N, earlier on the same stream), copied into caller arrays (device-to-device,
  * stream-ordered, asynchronous): the outcome of Algorithm 1 at each node, as the debug
- * entry below reports it.
+ * entry below reports it.  The workspace of resispec_decide_nodes (and resispec_walk_draw)
+ * is read the same way; there, nodes whose draw was deferred and not made report
+ * RS_SEQ_DEFERRED.
  *   node_child, node_token_out, node_status : [B][N] int32 device out, as in
  *                 resispec_verify_tree_debug
  * RS_ERR_INVALID_ARG for B < 0, N <= 0 or NULL outputs (B > 0); RS_ERR_WORKSPACE for a

@@ -624,8 +624,10 @@ def resispec_walk(node_token, workspace, out_tokens, out_accepted_len, out_statu
 
 
 def resispec_node_outcomes(workspace, B: int, N: int, *, stream=None):
-    """Every node's outcome left in `workspace` by resispec_verify_nodes: (node_child,
-    node_token, node_status), [B, N] int32 each."""
+    """Every node's outcome left in `workspace` by resispec_verify_nodes, or by
+    resispec_decide_nodes (and resispec_walk_draw, which fills in the nodes it draws for;
+    the others report RS_SEQ_DEFERRED): (node_child, node_token, node_status), [B, N]
+    int32 each."""
     import torch
     dev = workspace.device
     out = [torch.empty((B, N), dtype=torch.int32, device=dev) for _ in range(3)]
