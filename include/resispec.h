@@ -149,15 +149,16 @@ rs_status resispec_verify_tree(const void* target_logits, const void* draft_logi
  * results, bit for bit).  A node's draw from its final residual, and a leaf's bonus draw,
  * matter only where a walk ends (§Preliminary, tree-structured verification: the walk
  * draws once, at the node where it stops), so they are made there.  Two launches:
- *   - every node row takes pass 1 (the softmax statistics of Preliminary) and its tests
- *     (Eq. 2, Algorithm 1); a row with several candidates also takes the rejection passes
- *     its later tests need, and draws at once if it rejects them all; a row with one
- *     candidate that it rejects, and a leaf, keep their pass-1 slot totals in the
- *     workspace instead of drawing (no rejection pass re-reads their logits);
+ *   - every node row with children takes pass 1 (the softmax statistics of Preliminary)
+ *     and its tests (Eq. 2, Algorithm 1); a row with several candidates also takes the
+ *     rejection passes its later tests need, and draws at once if it rejects them all; a
+ *     row with one candidate that it rejects keeps its pass-1 slot totals in the
+ *     workspace instead of drawing (no rejection pass re-reads its logits); a leaf's row,
+ *     which serves only its bonus draw, is not read;
  *   - one workgroup per sequence walks the decisions and, where the walk ends at such a
  *     row, takes it up again: the residual pass of its rejection (Eq. 1/2 or GetProxy)
- *     over that row alone, then the inverse-CDF draw, with the same arithmetic on the same
- *     values as resispec_verify_tree.
+ *     over that row alone, or a leaf's pass 1, then the inverse-CDF draw, with the same
+ *     arithmetic on the same values as resispec_verify_tree.
  *   workspace : device buffer of at least resispec_deferred_workspace_bytes(B, N) bytes,
  *               16-byte aligned (node outcomes, then 2 KiB of slot totals per node row);
  *               contents on entry are ignored.  Calls that overlap on one workspace race.

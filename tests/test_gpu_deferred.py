@@ -1,8 +1,9 @@
 """GPU tests of the all-nodes schedule with deferred draws (resispec_verify_tree_deferred,
 and its two launches resispec_decide_nodes and resispec_walk_draw), through the C ABI.
 
-A row that rejects its one candidate, and a leaf, keep their pass-1 slot totals instead of
-drawing; the walk draws where it ends.  Checked here:
+A row that rejects its one candidate keeps its pass-1 slot totals instead of drawing, and a
+leaf's row (which serves only its bonus draw) is not read; the walk draws where it ends.
+Checked here:
   - tokens, accepted lengths and statuses equal the all-nodes schedule's bit for bit, and
     the walks agree with the oracle's sequential walk (exact outside the 1e-6 window,
     admissible inside it);
