@@ -470,8 +470,6 @@ __device__ __forceinline__ void wave_sweep_rc(const float* __restrict__ rc, cons
     }
 }
 
-// RC: the path schedule, whose later ResiSpec rejection passes keep the row's residual
-// in P.rcache when the caller's workspace holds it (see the rejection passes below).
 // How a row's draw is scheduled.  kSchedAll: every row that rejects all its candidates,
 // or has none, draws at once (the all-nodes and path schedules).  kSchedDecide: a row with
 // one candidate that it rejects stops after its test, keeps its pass-1 slot totals in
@@ -499,6 +497,10 @@ __device__ __forceinline__ void keep_slot_totals(const KParams& P, const Smem& s
     }
 }
 
+// One node row's verification (the steps of Algorithm 1 at one node, or its bonus draw).
+// RC: the path schedule, whose later ResiSpec rejection passes keep the row's residual
+// in P.rcache when the caller's workspace holds it (see the rejection passes below).
+// SCHED: how the row's draw is scheduled (above).
 template <typename In, int VEC, int UNR, int MODE, int BLK, bool SPLIT, bool RC = false,
           int SCHED = kSchedAll, typename Emit>
 __device__ __forceinline__ void verify_row(const KParams& P, Smem& sm, const int64_t row,
