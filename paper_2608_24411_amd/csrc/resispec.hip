@@ -526,6 +526,28 @@ __device__ __forceinline__ void verify_row(const KParams& P, Smem& sm, const int
     float* const rc = (RC && MODE == RS_MODE_RESISPEC && P.rcache) ? P.rcache + (int64_t)b * P.rc_stride : nullptr;
 
     using W = Vec<In, VEC>;
+    if constexpr (SCHED == kSchedDecide) {
+        // A leaf's row serves only its bonus draw, which is used only if a walk ends there,
+        // so the row is left whole to the walk.  Every wave reads the tree's parent array
+        // first and a leaf of a well-formed tree ends before any load of its row; other
+        // rows (a malformed tree's included) take the description below.  A root has a
+        // child in every well-formed tree of two or more nodes (node 1's parent), so it
+        // goes straight on.
+        if (!P.flat && (n > 0 || P.N == 1)) {
+            const int32_t* par = P.parent + (int64_t)b * P.N;
+            int kids = 0, bad = 0;
+            for (int m = lane; m < P.N; m += 64) {
+                const int32_t pm = par[m];
+                bad |= (m == 0) ? (pm != -1) : (pm < 0 || pm >= m);
+                kids |= (m > n && pm == n);
+            }
+            if (__ballot(bad) == 0ull && __ballot(kids) == 0ull) {
+                if (tid == 0) emit(-1, -1, P.bonus ? RS_SEQ_DEFERRED : RS_SEQ_OK);
+                if (!P.bonus) zero_residual_row(P, row);
+                return;
+            }
+        }
+    }
     // This wave's first target chunk is requested before anything else, so its latency
     // overlaps the row description below (the first slot of wave w is slot s0 + w).
     typename W::raw pre[UNR];
@@ -676,14 +698,6 @@ __device__ __forceinline__ void verify_row(const KParams& P, Smem& sm, const int
         if (tid == 0) emit(-1, -1, RS_SEQ_OK);
         zero_residual_row(P, row);
         return;
-    }
-    if constexpr (SCHED == kSchedDecide) {
-        // A leaf: its row serves only the bonus draw, which is used only if a walk ends
-        // here, so the row is left whole to the walk (it is not read here).
-        if (nc == 0 && !P.flat) {
-            if (tid == 0) emit(-1, -1, RS_SEQ_DEFERRED);
-            return;
-        }
     }
     if (tid == 0) sm.status = RS_SEQ_OK;
     // candidate logits (their latency overlaps the first chunk's)
