@@ -528,20 +528,28 @@ __device__ __forceinline__ void verify_row(const KParams& P, Smem& sm, const int
     using W = Vec<In, VEC>;
     if constexpr (SCHED == kSchedDecide) {
         // A leaf's row serves only its bonus draw, which is used only if a walk ends there,
-        // so the row is left whole to the walk.  Every wave reads the tree's parent array
-        // first and a leaf of a well-formed tree ends before any load of its row; other
-        // rows (a malformed tree's included) take the description below.  A root has a
-        // child in every well-formed tree of two or more nodes (node 1's parent), so it
-        // goes straight on.
+        // so the row is left whole to the walk.  The tree's parent array is read first and
+        // a leaf of a well-formed tree ends before any load of its row; other rows (a
+        // malformed tree's included) take the description below.  Trees of up to 64 nodes
+        // are read by every wave (one load a lane, no barrier), larger ones once by the
+        // workgroup.  A root has a child in every well-formed tree of two or more nodes
+        // (node 1's parent), so it goes straight on.
         if (!P.flat && (n > 0 || P.N == 1)) {
             const int32_t* par = P.parent + (int64_t)b * P.N;
-            int kids = 0, bad = 0;
-            for (int m = lane; m < P.N; m += 64) {
+            auto other_at = [&](int m) {   // a child of this node, or a parent entry out of place
                 const int32_t pm = par[m];
-                bad |= (m == 0) ? (pm != -1) : (pm < 0 || pm >= m);
-                kids |= (m > n && pm == n);
+                const bool bad = (m == 0) ? (pm != -1) : (pm < 0 || pm >= m);
+                return bad || (m > n && pm == n);
+            };
+            bool leaf;
+            if (P.N <= 64) {
+                leaf = __ballot(lane < P.N && other_at(lane)) == 0ull;
+            } else {
+                int other = 0;
+                for (int m = tid; m < P.N; m += kBlock) other |= other_at(m);
+                leaf = !__syncthreads_or(other);
             }
-            if (__ballot(bad) == 0ull && __ballot(kids) == 0ull) {
+            if (leaf) {
                 if (tid == 0) emit(-1, -1, P.bonus ? RS_SEQ_DEFERRED : RS_SEQ_OK);
                 if (!P.bonus) zero_residual_row(P, row);
                 return;
