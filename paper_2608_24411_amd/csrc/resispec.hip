@@ -556,8 +556,8 @@ __device__ __forceinline__ void verify_row(const KParams& P, Smem& sm, const int
             }
         }
     }
-    // This wave's first target chunk is requested before anything else, so its latency
-    // overlaps the row description below (the first slot of wave w is slot s0 + w).
+    // This wave's first target chunk is requested before the row description, so its
+    // latency overlaps the description below (the first slot of wave w is slot s0 + w).
     typename W::raw pre[UNR];
 #pragma unroll
     for (int u = 0; u < UNR; ++u) pre[u] = W::template load<kNtPass1>(tg, (s0 + wid) * G * CHUNK + lane * VEC + u * 64 * VEC, V);
