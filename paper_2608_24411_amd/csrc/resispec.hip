@@ -1069,6 +1069,11 @@ __device__ __forceinline__ void verify_row(const KParams& P, Smem& sm, const int
                 if (wantB) sm.partB[lane][slot] = accB;
                 accA = accB = 0.0f;
             };
+            // Load policy.  In the decide kernel only rows with several candidates take
+            // rejection passes, and while a candidate is left the row is read again: the
+            // passes keep it in the caches.  Elsewhere a rejection pass is mostly the row's
+            // last use and streams nontemporally.
+            constexpr bool kNtRejPass = SCHED == kSchedDecide ? false : kNtRej;
             // does this slot hold a rejected token? (wave-uniform)
             auto slot_hit = [&](int slot) -> bool {
                 const uint32_t w = __builtin_amdgcn_readfirstlane(sm.hit_slots[slot >> 5]);
@@ -1076,7 +1081,7 @@ __device__ __forceinline__ void verify_row(const KParams& P, Smem& sm, const int
             };
             if (MODE == RS_MODE_SPECINFER) {
                 // A = max(R - C_i Q, 0)
-                wave_sweep<In, VEC, UNR, true, 0, kNtRej>(tg, dg, V, G, nl, s0, reverse, pre, pre, &sm.next_slot,
+                wave_sweep<In, VEC, UNR, true, 0, kNtRejPass>(tg, dg, V, G, nl, s0, reverse, pre, pre, &sm.next_slot,
                     [&](const float (&t)[UNR][VEC], const float (&d)[UNR][VEC], int, int) {
                         float fa = 0.0f;
 #pragma unroll
@@ -1094,7 +1099,7 @@ __device__ __forceinline__ void verify_row(const KParams& P, Smem& sm, const int
                 // first rejection: A = min(c Q, R) / 2^f0 = exp2(min(aR - f0, aQ + e)), one
                 // exponential per element; the sum of R over j != x_0 is 1 - R(x_0)
                 const float f0 = sm.st_f0, kq0 = sm.st_kq0;
-                wave_sweep<In, VEC, UNR, true, 0, kNtRej>(tg, dg, V, G, nl, s0, reverse, pre, pre, &sm.next_slot,
+                wave_sweep<In, VEC, UNR, true, 0, kNtRejPass>(tg, dg, V, G, nl, s0, reverse, pre, pre, &sm.next_slot,
                     [&](const float (&t)[UNR][VEC], const float (&d)[UNR][VEC], int idx0, int slot) {
                         float v[UNR][VEC];
 #pragma unroll
@@ -1154,7 +1159,7 @@ __device__ __forceinline__ void verify_row(const KParams& P, Smem& sm, const int
                     }
                 };
                 if (ii == 1) {
-                    wave_sweep<In, VEC, UNR, true, 0, kNtRej>(tg, dg, V, G, nl, s0, reverse, pre, pre, &sm.next_slot,
+                    wave_sweep<In, VEC, UNR, true, 0, kNtRejPass>(tg, dg, V, G, nl, s0, reverse, pre, pre, &sm.next_slot,
                         [&](const float (&t)[UNR][VEC], const float (&d)[UNR][VEC], int idx0, int slot) {
                             const bool hit = slot_hit(slot);
                             float fa = 0.0f, fb = 0.0f;
@@ -1189,7 +1194,7 @@ __device__ __forceinline__ void verify_row(const KParams& P, Smem& sm, const int
                         flush);
                 }
             } else {
-                wave_sweep<In, VEC, UNR, true, 0, kNtRej>(tg, dg, V, G, nl, s0, reverse, pre, pre, &sm.next_slot,
+                wave_sweep<In, VEC, UNR, true, 0, kNtRejPass>(tg, dg, V, G, nl, s0, reverse, pre, pre, &sm.next_slot,
                     [&](const float (&t)[UNR][VEC], const float (&d)[UNR][VEC], int idx0, int slot) {
                         const bool hit = slot_hit(slot);
                         float R[UNR][VEC], Q[UNR][VEC];
