@@ -1071,9 +1071,10 @@ __device__ __forceinline__ void verify_row(const KParams& P, Smem& sm, const int
             };
             // Load policy.  In the decide kernel only rows with several candidates take
             // rejection passes, and while a candidate is left the row is read again: the
-            // passes keep it in the caches.  Elsewhere a rejection pass is mostly the row's
-            // last use and streams nontemporally.
-            constexpr bool kNtRejPass = SCHED == kSchedDecide ? false : kNtRej;
+            // passes keep it in the caches, as do the path schedule's with its residual
+            // cache (its second pass reads the logits again).  Elsewhere a rejection pass is
+            // mostly the row's last use and streams nontemporally.
+            constexpr bool kNtRejPass = (SCHED == kSchedDecide || RC) ? false : kNtRej;
             // does this slot hold a rejected token? (wave-uniform)
             auto slot_hit = [&](int slot) -> bool {
                 const uint32_t w = __builtin_amdgcn_readfirstlane(sm.hit_slots[slot >> 5]);
